@@ -1,0 +1,242 @@
+"""Benchmark: conv2d forward + backward_filter + backward_data (bias_add and relu
+fused) of the ResNet-shaped layer N=256, C=64, 56x56, F=64, 3x3, stride 1, pad 1,
+in fp64 on one MI355X, as GFLOP/s and a fraction of the fp64 matrix-core peak.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+One step = the three conv passes over one batch already resident in HBM.  The
+timed region is bracketed by device synchronisations; per-pass durations come
+from HIP events recorded on the stream the kernels are launched on.  Also
+reported (extra keys): the fp32 mode of the same layer, the LeNet-style
+training step (batch 64, fp64) in images/s, and the oracle timed on a bounded
+sample of the same layer on the host's cores.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_F64_MFMA = 78.6      # TFLOP/s, MI355X dense fp64 matrix
+PEAK_F32_MFMA = 157.3     # TFLOP/s, MI355X dense fp32 matrix
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_hbm_traffic_resnet_fp64.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--only-f64", action="store_true", help="skip the fp32 and LeNet extras")
+    return ap.parse_args()
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for name in ("conv_igemm.hip", "conv_wgrad.hip", "common.hpp"):
+        with open(os.path.join(ROOT, "paper_1802_04647_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(pass_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when absent or taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"^source_sha=(\w+)", text, re.M)
+    if not m or m.group(1) != kernel_source_sha():
+        return None
+    m = re.search(rf"^{pass_name}_hbm_bytes_per_launch=([0-9.eE+]+)", text, re.M)
+    return float(m.group(1)) if m else None
+
+
+def conv_step_timing(dtype_name, steps, warmup):
+    import torch
+    from paper_1802_04647_amd import dmlnn
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    s = SHAPES["resnet_conv"]
+    tdt = torch.float64 if dtype_name == "f64" else torch.float32
+    X0, W0, b0, dout0 = conv_layer_inputs("resnet_conv")
+    dev = lambda a: torch.from_numpy(a).to(device="cuda", dtype=tdt)  # noqa: E731
+    X, W, b, dout = dev(X0), dev(W0), dev(b0), dev(dout0)
+    del X0, dout0
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=tdt, device="cuda")
+    dW = torch.empty_like(W)
+    db = torch.empty_like(b)
+    dX = torch.empty_like(X)
+    ws = torch.empty(dmlnn.conv2d_backward_filter_workspace_size(tdt, *s.args()),
+                     dtype=torch.uint8, device="cuda")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        dmlnn.conv2d_forward(X, W, b, *a, relu=True, out=out)
+        if ev is not None:
+            ev[1].record()
+        dmlnn.conv2d_backward_filter(X, dout, out, *a, s.F, workspace=ws, dW=dW, db=db)
+        if ev is not None:
+            ev[2].record()
+        dmlnn.conv2d_backward_data(W, dout, out, *a, dX=dX)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {"forward": 0.0, "backward_filter": 0.0, "backward_data": 0.0}
+    for ev in evs:
+        per["forward"] += ev[0].elapsed_time(ev[1])
+        per["backward_filter"] += ev[1].elapsed_time(ev[2])
+        per["backward_data"] += ev[2].elapsed_time(ev[3])
+    per = {k: v / steps for k, v in per.items()}          # ms per launch
+    flops = s.flops_per_pass()
+    return dict(wall_s=wall, per_pass_ms=per, flops_per_pass=flops, N=s.N)
+
+
+def lenet_timing(steps=50, warmup=10):
+    import torch
+    from paper_1802_04647_amd.inputs import lenet_train_inputs
+    from paper_1802_04647_amd.lenet import LeNetTrainer
+
+    X, Y, params = lenet_train_inputs()
+    tr = LeNetTrainer(params)
+    Xd = torch.from_numpy(X).cuda()
+    Yd = torch.from_numpy(Y).cuda()
+    for _ in range(warmup):
+        tr.step(Xd, Yd)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        tr.step(Xd, Yd)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3))
+
+
+def cpu_baseline(target_s=12.0):
+    """The oracle (plain nested loops, OpenMP over independent outputs) on a bounded
+    sample of the same layer: the three passes over n images."""
+    import numpy as np  # noqa: F401
+    import oracle
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    s = SHAPES["resnet_conv"]
+    cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(cores)
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+
+    def run(n):
+        X, W, b, dout = conv_layer_inputs("resnet_conv", N=n)
+        t = time.perf_counter()
+        out, _, _ = oracle.conv2d_forward(X, W, b, *a)
+        oracle.conv2d_backward_filter(X, dout, out, *a, s.F)
+        oracle.conv2d_backward_data(W, dout, out, *a)
+        return time.perf_counter() - t
+
+    t1 = run(1)
+    n = int(max(1, min(s.N, round(target_s / max(t1, 1e-3)))))
+    t = run(n) if n > 1 else t1
+    flops = 3 * 2.0 * n * s.F * s.Hout * s.Wout * s.K
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            m = re.search(r"model name\s*:\s*(.*)", f.read())
+            cpu = m.group(1).strip() if m else platform.processor()
+    except OSError:
+        pass
+    return {"value": round(flops / t / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.get_threads(),
+            "kind": "oracle",
+            "sample": f"fwd+bwd_filter+bwd_data of the 64->64 56x56 3x3 layer on {n} of 256 "
+                      f"images, fp64, {t:.2f} s wall, {cpu}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the data-parallel "
+              "multi-GPU path is a design note, not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("no GPU available", file=sys.stderr)
+        sys.exit(1)
+
+    r = conv_step_timing("f64", args.steps, args.warmup)
+    N, F3 = r["N"], 3 * r["flops_per_pass"]
+    ms_step = r["wall_s"] * 1e3 / args.steps
+    gflops = F3 / (ms_step / 1e3) / 1e9
+    per = r["per_pass_ms"]
+    dom = max(per, key=per.get)
+    achieved = r["flops_per_pass"] / (per[dom] / 1e3) / 1e12
+    sum_ms = sum(per.values())
+    rec = {
+        "metric": "conv2d fwd+bwd GFLOP/s and % of MFMA peak (fp64); training images/sec",
+        "value": round(gflops, 1),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded relu(N(0,1)) activations, He-normal filters, N(0,1) upstream "
+                "gradient)",
+        "config": {"workload": "resnet_conv: conv2d 64->64, 56x56, 3x3, stride 1, pad 1, "
+                               "bias_add+relu fused; forward + backward_filter + backward_data",
+                   "global_batch": N, "seq_len": None, "parallelism": "single GPU"},
+        "pct_of_fp64_mfma_peak": round(100.0 * gflops / 1e3 / PEAK_F64_MFMA, 2),
+        "images_per_s": round(N / (ms_step / 1e3), 1),
+        "per_pass_ms": {k: round(v, 4) for k, v in per.items()},
+        "per_pass_tflops": {k: round(r["flops_per_pass"] / (v / 1e3) / 1e12, 3)
+                            for k, v in per.items()},
+        "event_sum_ms": round(sum_ms, 4),
+        "roofline": {"bound": "mfma", "kernel": f"conv2d_{dom}", "achieved": round(achieved, 3),
+                     "peak": PEAK_F64_MFMA, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_F64_MFMA, 4),
+                     "traffic": measured_traffic(dom)},
+    }
+    if not args.only_f64:
+        r32 = conv_step_timing("f32", args.steps, args.warmup)
+        ms32 = r32["wall_s"] * 1e3 / args.steps
+        rec["f32_mode"] = {"gflops": round(3 * r32["flops_per_pass"] / (ms32 / 1e3) / 1e9, 1),
+                           "ms_per_step": round(ms32, 4),
+                           "pct_of_fp32_mfma_peak": round(
+                               100.0 * 3 * r32["flops_per_pass"] / (ms32 / 1e3) / 1e12
+                               / PEAK_F32_MFMA, 2),
+                           "per_pass_ms": {k: round(v, 4) for k, v in r32["per_pass_ms"].items()}}
+        lt = lenet_timing()
+        rec["lenet_training"] = {"batch": 64, "dtype": "f64",
+                                 "ms_per_step": round(lt["ms_per_step"], 4),
+                                 "images_per_s": round(lt["images_per_s"], 1)}
+    if not args.no_cpu:
+        rec["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

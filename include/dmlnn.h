@@ -1,0 +1,201 @@
+/*
+ * dmlnn.h — C ABI of libdmlnn.so, the MI355X (gfx950) implementation of the
+ * conv2d layer of a DML-style neural-network library and the ops around it.
+ *
+ * Source of the semantics: "Deep Learning with Apache SystemML" (Pansare et
+ * al., arXiv 1802.04647).
+ *   - Section 3, "Tensor Representation": a tensor [N, C, H, W] is stored as a
+ *     matrix with N rows and C*H*W columns (all but the first dimension are
+ *     linearised).  Reading used throughout: row-major, column index
+ *     c*H*W + h*W + w.  Filters are F x (C*Hf*Wf) with column c*Hf*Wf + i*Wf + j.
+ *   - Section 3, "Builtin NN Functions": conv2d and pooling, and their backward
+ *     functions, are builtins.
+ *   - Section 2 (NN library and its softmax-classifier listing): layers with
+ *     init/forward/backward; affine = X %*% W + b; softmax; cross-entropy;
+ *     SGD (and SGD with momentum among the optimizers).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers to contiguous row-major buffers that
+ *     the caller allocates and owns.  The library never allocates device memory
+ *     and keeps no pointer after a call returns.
+ *   - `dtype` selects the element type of every floating-point buffer of the
+ *     call: DMLNN_F64 (double) or DMLNN_F32 (float).  Index buffers are int32.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *     asynchronous on that stream; outputs are valid once the stream reaches
+ *     the call.
+ *   - Outputs are overwritten (never accumulated into).  Inputs are never
+ *     written.  Buffers must not alias, except where a call says so.
+ *   - Every call validates its arguments on the host before launching anything.
+ *     On failure it returns a nonzero dmlnn_status, launches nothing, and
+ *     dmlnn_last_error() describes the problem.  Faults inside a kernel surface
+ *     at the next synchronisation of the stream.
+ *   - Element counts of every buffer must be below 2^31.
+ *   - Entry points keep no state between calls (except the zero-skip mode) and
+ *     may be called from several host threads.
+ */
+#ifndef DMLNN_H
+#define DMLNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__) || defined(__clang__)
+#define DMLNN_API __attribute__((visibility("default")))
+#else
+#define DMLNN_API
+#endif
+
+typedef enum { DMLNN_F64 = 0, DMLNN_F32 = 1 } dmlnn_dtype;
+
+typedef enum {
+    DMLNN_OK = 0,
+    DMLNN_ERR_ARG = 1,       /* a size, stride, pad or flag is out of range       */
+    DMLNN_ERR_NULL = 2,      /* a required pointer is NULL                         */
+    DMLNN_ERR_DTYPE = 3,     /* dtype is not DMLNN_F64 / DMLNN_F32                 */
+    DMLNN_ERR_WORKSPACE = 4, /* workspace missing or smaller than required         */
+    DMLNN_ERR_DEVICE = 5,    /* no usable gfx950 device / HIP runtime error        */
+    DMLNN_ERR_LAUNCH = 6     /* a kernel launch was rejected                       */
+} dmlnn_status;
+
+/* Output size of a convolution or pooling window along one axis:
+ * floor((Hin + 2*pad - Hf) / stride) + 1 (symmetric zero padding).
+ * Host-only.  Returns <= 0 when the arguments are invalid or no window fits. */
+DMLNN_API int conv2d_out_dim(int Hin, int Hf, int stride, int pad);
+
+/* ---------------------------------------------------------------- conv2d ----
+ * Paper: Section 3, "Builtin NN Functions" (conv2d is a builtin) and "Sparse
+ * Operations" (conv2d is computed by lowering: the stored filter matrix times
+ * the patch matrix, i.e. cross-correlation without a filter flip).
+ *
+ * Shapes: X is N x (C*Hin*Win); W is F x (C*Hf*Wf); b has F entries;
+ * out is N x (F*Hout*Wout) with Hout = conv2d_out_dim(Hin,Hf,stride,pad) and
+ * Wout = conv2d_out_dim(Win,Wf,stride,pad), both required to be >= 1.
+ * Requires N, C, Hin, Win, F, Hf, Wf >= 1, stride >= 1, pad >= 0.
+ */
+
+/* Forward with bias_add and relu fused into the epilogue:
+ *   pre[n,f,oh,ow] = b[f] + sum_{c,i,j} W[f,c,i,j] * x[n,c,oh*stride+i-pad,ow*stride+j-pad]
+ *   (x is 0 outside the image);  out = relu ? max(pre, 0) : pre.
+ * b may be NULL (no bias).  relu is 0 or 1. */
+DMLNN_API int conv2d_forward(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
+                   int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                   int stride, int pad, int relu, void *stream);
+
+/* Bytes of device workspace that conv2d_backward_filter needs for these sizes
+ * (a deterministic split of the reduction over images and pixels).  Depends
+ * only on the arguments.  Returns 0 when the arguments are invalid. */
+DMLNN_API size_t conv2d_backward_filter_workspace_size(dmlnn_dtype dtype, int N, int C, int Hin, int Win,
+                                             int F, int Hf, int Wf, int stride, int pad);
+
+/* Filter and bias gradients, with the relu mask fused into the prologue:
+ *   g = dout where out_fwd > 0, else 0   (out_fwd == NULL: g = dout, no relu)
+ *   dW[f,c,i,j] = sum_{n,oh,ow} g[n,f,oh,ow] * x[n,c,oh*stride+i-pad,ow*stride+j-pad]
+ *   db[f]       = sum_{n,oh,ow} g[n,f,oh,ow]              (db may be NULL)
+ * dout and out_fwd are N x (F*Hout*Wout); dW is F x (C*Hf*Wf).
+ * `workspace` is a device buffer of at least
+ * conv2d_backward_filter_workspace_size(...) bytes, owned by the caller; its
+ * contents on entry are ignored and on return are undefined.  The reduction
+ * order is fixed, so results are bitwise reproducible run to run. */
+DMLNN_API int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const void *dout, const void *out_fwd,
+                           void *dW, void *db, int N, int C, int Hin, int Win,
+                           int F, int Hf, int Wf, int stride, int pad,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* Input gradient, with the relu mask fused into the prologue:
+ *   dX[n,c,h,w] = sum_{f,i,j} W[f,c,i,j] * g[n,f,(h+pad-i)/stride,(w+pad-j)/stride]
+ * over the (i,j) whose quotients are exact and inside the output; input cells
+ * that no window covers get 0.  g as in conv2d_backward_filter.
+ * dX is N x (C*Hin*Win). */
+DMLNN_API int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void *dout, const void *out_fwd,
+                         void *dX, int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                         int stride, int pad, void *stream);
+
+/* Zero-skip mode for the conv2d kernels (paper, Section 3 "Sparse Operations":
+ * a sparse-input / dense-filter operator does fewer floating-point operations).
+ * mode 0 = dense (default), 1 = skip every MFMA step whose staged input
+ * fragment is entirely zero (a wavefront ballot).  Results are bitwise equal
+ * to the dense path up to the sign of zero results.  Process-wide setting;
+ * returns the previous mode, or -1 for an invalid mode. */
+DMLNN_API int dmlnn_set_zero_skip(int mode);
+
+/* --------------------------------------------------------- bias_add_relu ----
+ * Paper: Section 3, "Tensor Representation" (broadcasting of vectors over
+ * matrices) and the affine listing (X %*% W + b).
+ *   out[n, c*HW + q] = relu ? max(X[n,c*HW+q] + b[c], 0) : X[n,c*HW+q] + b[c]
+ * X and out are N x (C*HW); b has C entries or is NULL.  out may equal X
+ * (in place). */
+DMLNN_API int bias_add_relu(dmlnn_dtype dtype, const void *X, const void *b, void *out,
+                  int N, int C, int HW, int relu, void *stream);
+
+/* ------------------------------------------------------------ max_pool2d ----
+ * Paper: Section 3, "Builtin NN Functions" (pooling and its backward).
+ * Window Hf x Wf, stride, pad; padded cells count as -infinity.  Requires
+ * pad < Hf and pad < Wf (every window then holds at least one input cell).
+ * X is N x (C*Hin*Win); out and argmax are N x (C*Hout*Wout).
+ * argmax holds the in-row column index c*Hin*Win + h*Win + w of the first
+ * maximum met scanning the window row by row (ties: first wins; +0 == -0).
+ * NaN inputs give undefined results. */
+DMLNN_API int max_pool2d_fwd(dmlnn_dtype dtype, const void *X, void *out, int32_t *argmax,
+                   int N, int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
+                   void *stream);
+
+/* dX[n,k] = sum of dout[n,o] over the outputs o of row n with argmax[n,o] == k,
+ * 0 elsewhere.  dout and argmax are N x (C*Hout*Wout); dX is N x (C*Hin*Win).
+ * argmax must come from max_pool2d_fwd with the same sizes. */
+DMLNN_API int max_pool2d_bwd(dmlnn_dtype dtype, const void *dout, const int32_t *argmax, void *dX,
+                   int N, int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
+                   void *stream);
+
+/* ----------------------------------------------------------------- affine ----
+ * Paper: Section 2 listing (scores = X %*% W + b; backward returns
+ * [dX, dW, db]).  X is N x D, W is D x M, b is 1 x M, out is N x M.
+ *   out = X W + b, then max(., 0) if relu.  b may be NULL. */
+DMLNN_API int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
+               int N, int D, int M, int relu, void *stream);
+
+/* g = dout (masked to out_fwd > 0 when out_fwd != NULL);
+ *   dX = g W^T (N x D, may be NULL), dW = X^T g (D x M), db = column sums of g
+ *   (1 x M, may be NULL). */
+DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W,
+               const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M,
+               void *stream);
+
+/* ----------------------------------------------------------- softmax_xent ----
+ * Paper: Section 2 listing (probs = softmax(scores); cross-entropy backward;
+ * softmax backward), fused.  Per row: p = exp(s - max s) / sum exp(s - max s);
+ *   loss    = -(1/N) sum_{n,k} Y[n,k] * log p[n,k]   (one device scalar)
+ *   dscores = (p * sum_k Y[n,k] - Y) / N
+ * scores, Y, probs, dscores are N x K; probs may be NULL; loss points to one
+ * element of dtype in device memory.  Deterministic reduction order. */
+DMLNN_API int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *probs,
+                 void *dscores, void *loss, int N, int K, void *stream);
+
+/* ---------------------------------------------------- sgd_momentum_update ----
+ * Paper: Section 2 (SGD with momentum is one of the NN library's optimizers;
+ * the listing's plain SGD is W - lr*dW, the case mu = 0).
+ *   v <- mu*v - lr*grad;  theta <- theta + v     (elementwise, in place)
+ * theta, grad and v hold n elements. */
+DMLNN_API int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v,
+                        double lr, double mu, long long n, void *stream);
+
+/* --------------------------------------------------------- count_nonzero ----
+ * Paper: Section 3, "Sparse Operations" (the number of non-zeros of every
+ * intermediate drives the choice of operator).  Writes the number of entries
+ * of X (n elements) different from zero to *out_dev (one int64 in device
+ * memory). */
+DMLNN_API int count_nonzero(dmlnn_dtype dtype, const void *X, long long n, long long *out_dev,
+                  void *stream);
+
+/* Human-readable description of the last failed call on this host thread
+ * ("" if none).  The string stays valid until the next call on the thread. */
+DMLNN_API const char *dmlnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DMLNN_H */

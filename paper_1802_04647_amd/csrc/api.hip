@@ -1,0 +1,305 @@
+// C ABI of libdmlnn.so (declared in include/dmlnn.h): argument validation on the
+// host, then dispatch to the kernel launchers.  Nothing here allocates device
+// memory.  Validation happens before any HIP runtime call, so bad arguments are
+// reported without a GPU and without launching anything.
+#include <atomic>
+#include <climits>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/dmlnn.h"
+#include "internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+std::atomic<int> g_zero_skip{-1};
+
+int fail(int code, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int zero_skip_mode()
+{
+    int m = g_zero_skip.load(std::memory_order_relaxed);
+    if (m < 0) {
+        const char *e = getenv("DMLNN_ZERO_SKIP");
+        m = (e && (strcmp(e, "1") == 0 || strcmp(e, "on") == 0)) ? 1 : 0;
+        int expected = -1;
+        g_zero_skip.compare_exchange_strong(expected, m);
+        m = g_zero_skip.load(std::memory_order_relaxed);
+    }
+    return m;
+}
+
+bool dtype_ok(int dt) { return dt == DMLNN_F64 || dt == DMLNN_F32; }
+
+constexpr long long kMaxElems = (long long)INT_MAX;
+
+bool count_ok(long long a, long long b) { return a >= 1 && b >= 1 && a * b <= kMaxElems; }
+
+// The kernels are built for gfx950 only; check the current device once per id.
+int device_check()
+{
+    static std::mutex mu;
+    static int state[64] = {0};  // 0 unknown, 1 ok, 2 bad
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= 64)
+        return fail(DMLNN_ERR_DEVICE, "no usable HIP device (%s)", hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(mu);
+    if (state[dev] == 0) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess)
+            return fail(DMLNN_ERR_DEVICE, "hipGetDeviceProperties failed: %s", hipGetErrorString(e));
+        state[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+        if (state[dev] == 2)
+            return fail(DMLNN_ERR_DEVICE, "device %d is %s; libdmlnn is built for gfx950", dev,
+                        prop.gcnArchName);
+    }
+    if (state[dev] != 1) return fail(DMLNN_ERR_DEVICE, "device %d is not gfx950", dev);
+    return DMLNN_OK;
+}
+
+int launched(hipError_t e, const char *what)
+{
+    if (e != hipSuccess) return fail(DMLNN_ERR_LAUNCH, "%s: launch failed: %s", what, hipGetErrorString(e));
+    g_err[0] = '\0';
+    return DMLNN_OK;
+}
+
+int conv_dims(dmlnn::ConvDims &d, int N, int C, int Hin, int Win, int F, int Hf, int Wf, int stride,
+              int pad)
+{
+    if (N < 1 || C < 1 || Hin < 1 || Win < 1 || F < 1 || Hf < 1 || Wf < 1)
+        return fail(DMLNN_ERR_ARG, "sizes must be >= 1 (N=%d C=%d Hin=%d Win=%d F=%d Hf=%d Wf=%d)",
+                    N, C, Hin, Win, F, Hf, Wf);
+    if (stride < 1 || pad < 0) return fail(DMLNN_ERR_ARG, "stride must be >= 1 and pad >= 0");
+    d.N = N;
+    d.C = C;
+    d.Hin = Hin;
+    d.Win = Win;
+    d.F = F;
+    d.Hf = Hf;
+    d.Wf = Wf;
+    d.stride = stride;
+    d.pad = pad;
+    d.Hout = conv2d_out_dim(Hin, Hf, stride, pad);
+    d.Wout = conv2d_out_dim(Win, Wf, stride, pad);
+    if (d.Hout < 1 || d.Wout < 1)
+        return fail(DMLNN_ERR_ARG, "no window fits: Hout=%d Wout=%d", d.Hout, d.Wout);
+    if (!count_ok(N, (long long)C * Hin * Win) || !count_ok(N, (long long)F * d.Hout * d.Wout) ||
+        !count_ok(F, (long long)C * Hf * Wf) || (long long)Hin + 2LL * pad > INT_MAX / 4 ||
+        (long long)Win + 2LL * pad > INT_MAX / 4)
+        return fail(DMLNN_ERR_ARG, "tensor too large (element counts must be < 2^31)");
+    return DMLNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int conv2d_out_dim(int Hin, int Hf, int stride, int pad)
+{
+    if (Hin < 1 || Hf < 1 || stride < 1 || pad < 0) return 0;
+    long long span = (long long)Hin + 2LL * pad - Hf;
+    if (span < 0) return 0;
+    long long r = span / stride + 1;
+    return r > INT_MAX ? 0 : (int)r;
+}
+
+const char *dmlnn_last_error(void) { return g_err; }
+
+int dmlnn_set_zero_skip(int mode)
+{
+    if (mode != 0 && mode != 1) return -1;
+    int prev = zero_skip_mode();
+    g_zero_skip.store(mode);
+    return prev;
+}
+
+int conv2d_forward(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
+                   int N, int C, int Hin, int Win, int F, int Hf, int Wf, int stride, int pad,
+                   int relu, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_forward: bad dtype %d", (int)dtype);
+    if (!X || !W || !out) return fail(DMLNN_ERR_NULL, "conv2d_forward: X, W and out are required");
+    if (relu != 0 && relu != 1) return fail(DMLNN_ERR_ARG, "conv2d_forward: relu must be 0 or 1");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_forward(dtype, X, W, b, out, d, relu, zero_skip_mode(),
+                                               (hipStream_t)stream),
+                    "conv2d_forward");
+}
+
+size_t conv2d_backward_filter_workspace_size(dmlnn_dtype dtype, int N, int C, int Hin, int Win,
+                                             int F, int Hf, int Wf, int stride, int pad)
+{
+    if (!dtype_ok(dtype)) return 0;
+    dmlnn::ConvDims d;
+    if (conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return 0;
+    return dmlnn::conv_wgrad_workspace_bytes(dtype, d);
+}
+
+int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const void *dout, const void *out_fwd,
+                           void *dW, void *db, int N, int C, int Hin, int Win, int F, int Hf,
+                           int Wf, int stride, int pad, void *workspace, size_t workspace_bytes,
+                           void *stream)
+{
+    if (!dtype_ok(dtype))
+        return fail(DMLNN_ERR_DTYPE, "conv2d_backward_filter: bad dtype %d", (int)dtype);
+    if (!X || !dout || !dW)
+        return fail(DMLNN_ERR_NULL, "conv2d_backward_filter: X, dout and dW are required");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    const size_t need = dmlnn::conv_wgrad_workspace_bytes(dtype, d);
+    if (need == 0) return fail(DMLNN_ERR_ARG, "conv2d_backward_filter: no tiling fits these sizes");
+    if (!workspace || workspace_bytes < need)
+        return fail(DMLNN_ERR_WORKSPACE, "conv2d_backward_filter: workspace of %zu bytes needed, %zu given",
+                    need, workspace ? workspace_bytes : (size_t)0);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_backward_filter(dtype, X, dout, out_fwd, dW, db, d, workspace,
+                                                       zero_skip_mode(), (hipStream_t)stream),
+                    "conv2d_backward_filter");
+}
+
+int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void *dout, const void *out_fwd,
+                         void *dX, int N, int C, int Hin, int Win, int F, int Hf, int Wf, int stride,
+                         int pad, void *stream)
+{
+    if (!dtype_ok(dtype))
+        return fail(DMLNN_ERR_DTYPE, "conv2d_backward_data: bad dtype %d", (int)dtype);
+    if (!W || !dout || !dX)
+        return fail(DMLNN_ERR_NULL, "conv2d_backward_data: W, dout and dX are required");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_backward_data(dtype, W, dout, out_fwd, dX, d,
+                                                     zero_skip_mode(), (hipStream_t)stream),
+                    "conv2d_backward_data");
+}
+
+int bias_add_relu(dmlnn_dtype dtype, const void *X, const void *b, void *out, int N, int C, int HW,
+                  int relu, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "bias_add_relu: bad dtype %d", (int)dtype);
+    if (!X || !out) return fail(DMLNN_ERR_NULL, "bias_add_relu: X and out are required");
+    if (N < 1 || C < 1 || HW < 1 || !count_ok(N, (long long)C * HW))
+        return fail(DMLNN_ERR_ARG, "bias_add_relu: bad sizes N=%d C=%d HW=%d", N, C, HW);
+    if (relu != 0 && relu != 1) return fail(DMLNN_ERR_ARG, "bias_add_relu: relu must be 0 or 1");
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_bias_add_relu(dtype, X, b, out, N, C, HW, relu, (hipStream_t)stream),
+                    "bias_add_relu");
+}
+
+static int pool_dims(int N, int C, int Hin, int Win, int Hf, int Wf, int stride, int pad, int &Hout,
+                     int &Wout)
+{
+    if (N < 1 || C < 1 || Hin < 1 || Win < 1 || Hf < 1 || Wf < 1 || stride < 1 || pad < 0)
+        return fail(DMLNN_ERR_ARG, "max_pool2d: sizes must be >= 1, stride >= 1, pad >= 0");
+    if (pad >= Hf || pad >= Wf) return fail(DMLNN_ERR_ARG, "max_pool2d: pad must be < Hf and < Wf");
+    Hout = conv2d_out_dim(Hin, Hf, stride, pad);
+    Wout = conv2d_out_dim(Win, Wf, stride, pad);
+    if (Hout < 1 || Wout < 1) return fail(DMLNN_ERR_ARG, "max_pool2d: no window fits");
+    if (!count_ok(N, (long long)C * Hin * Win) || !count_ok(N, (long long)C * Hout * Wout))
+        return fail(DMLNN_ERR_ARG, "max_pool2d: tensor too large");
+    return DMLNN_OK;
+}
+
+int max_pool2d_fwd(dmlnn_dtype dtype, const void *X, void *out, int32_t *argmax, int N, int C,
+                   int Hin, int Win, int Hf, int Wf, int stride, int pad, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "max_pool2d_fwd: bad dtype %d", (int)dtype);
+    if (!X || !out || !argmax) return fail(DMLNN_ERR_NULL, "max_pool2d_fwd: X, out, argmax are required");
+    int Hout, Wout;
+    if (int r = pool_dims(N, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_max_pool_fwd(dtype, X, out, argmax, N, C, Hin, Win, Hf, Wf, stride,
+                                               pad, Hout, Wout, (hipStream_t)stream),
+                    "max_pool2d_fwd");
+}
+
+int max_pool2d_bwd(dmlnn_dtype dtype, const void *dout, const int32_t *argmax, void *dX, int N,
+                   int C, int Hin, int Win, int Hf, int Wf, int stride, int pad, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "max_pool2d_bwd: bad dtype %d", (int)dtype);
+    if (!dout || !argmax || !dX) return fail(DMLNN_ERR_NULL, "max_pool2d_bwd: dout, argmax, dX are required");
+    int Hout, Wout;
+    if (int r = pool_dims(N, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_max_pool_bwd(dtype, dout, argmax, dX, N, C, Hin, Win, Hf, Wf,
+                                               stride, pad, Hout, Wout, (hipStream_t)stream),
+                    "max_pool2d_bwd");
+}
+
+int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out, int N,
+               int D, int M, int relu, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_fwd: bad dtype %d", (int)dtype);
+    if (!X || !W || !out) return fail(DMLNN_ERR_NULL, "affine_fwd: X, W and out are required");
+    if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M))
+        return fail(DMLNN_ERR_ARG, "affine_fwd: bad sizes N=%d D=%d M=%d", N, D, M);
+    if (relu != 0 && relu != 1) return fail(DMLNN_ERR_ARG, "affine_fwd: relu must be 0 or 1");
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_affine_fwd(dtype, X, W, b, out, N, D, M, relu, (hipStream_t)stream),
+                    "affine_fwd");
+}
+
+int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W,
+               const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_bwd: bad dtype %d", (int)dtype);
+    if (!dout || !X || !W || !dW) return fail(DMLNN_ERR_NULL, "affine_bwd: dout, X, W, dW are required");
+    if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M))
+        return fail(DMLNN_ERR_ARG, "affine_bwd: bad sizes N=%d D=%d M=%d", N, D, M);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_affine_bwd(dtype, dout, X, W, out_fwd, dX, dW, db, N, D, M,
+                                             (hipStream_t)stream),
+                    "affine_bwd");
+}
+
+int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *probs, void *dscores,
+                 void *loss, int N, int K, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "softmax_xent: bad dtype %d", (int)dtype);
+    if (!scores || !Y || !dscores || !loss)
+        return fail(DMLNN_ERR_NULL, "softmax_xent: scores, Y, dscores and loss are required");
+    if (!count_ok(N, K)) return fail(DMLNN_ERR_ARG, "softmax_xent: bad sizes N=%d K=%d", N, K);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_softmax_xent(dtype, scores, Y, probs, dscores, loss, N, K,
+                                               (hipStream_t)stream),
+                    "softmax_xent");
+}
+
+int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v, double lr,
+                        double mu, long long n, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "sgd_momentum_update: bad dtype %d", (int)dtype);
+    if (!theta || !grad || !v) return fail(DMLNN_ERR_NULL, "sgd_momentum_update: theta, grad, v are required");
+    if (n < 1 || n > kMaxElems) return fail(DMLNN_ERR_ARG, "sgd_momentum_update: bad n=%lld", n);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_sgd_momentum(dtype, theta, grad, v, lr, mu, n, (hipStream_t)stream),
+                    "sgd_momentum_update");
+}
+
+int count_nonzero(dmlnn_dtype dtype, const void *X, long long n, long long *out_dev, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "count_nonzero: bad dtype %d", (int)dtype);
+    if (!X || !out_dev) return fail(DMLNN_ERR_NULL, "count_nonzero: X and out_dev are required");
+    if (n < 1 || n > kMaxElems) return fail(DMLNN_ERR_ARG, "count_nonzero: bad n=%lld", n);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_count_nonzero(dtype, X, n, out_dev, (hipStream_t)stream),
+                    "count_nonzero");
+}
+
+}  // extern "C"

@@ -1,0 +1,81 @@
+// Device-side building blocks shared by the dmlnn kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dmlnn {
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// One 16x16x4 matrix-core step, D = A(16x4) * B(4x16) + C, per element type.
+//
+// Operand lanes (both types): lane l holds A[l % 16][l / 16] and B[l / 16][l % 16].
+// Accumulator lanes differ between the two instructions on gfx950 (measured):
+//   f64: item r of lane l is D[l / 16 + 4 r][l % 16]
+//   f32: item r of lane l is D[4 (l / 16) + r][l % 16]
+template <typename T>
+struct Mfma;
+
+template <>
+struct Mfma<double> {
+    typedef d4 acc_t;
+    static __device__ __forceinline__ acc_t zero() { return acc_t{0.0, 0.0, 0.0, 0.0}; }
+    static __device__ __forceinline__ acc_t mma(double a, double b, acc_t c)
+    {
+        return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int lane, int r) { return (lane >> 4) + 4 * r; }
+};
+
+template <>
+struct Mfma<float> {
+    typedef f4 acc_t;
+    static __device__ __forceinline__ acc_t zero() { return acc_t{0.f, 0.f, 0.f, 0.f}; }
+    static __device__ __forceinline__ acc_t mma(float a, float b, acc_t c)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int lane, int r) { return 4 * (lane >> 4) + r; }
+};
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// Wave-uniform "is every lane's value zero" test (wavefront ballot).
+template <typename T>
+__device__ __forceinline__ bool wave_all_zero(T v)
+{
+    return __builtin_amdgcn_ballot_w64(v != T(0)) == 0ull;
+}
+
+template <typename T>
+__device__ __forceinline__ T relu_if(T v, int relu)
+{
+    return (relu && !(v > T(0))) ? T(0) : v;
+}
+
+// Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8).
+// Renumber so that logically consecutive blocks share an XCD (and its L2):
+// logical = (b % 8) * ceil(n / 8) + b / 8, valid when the grid is a multiple of 8;
+// otherwise the identity is used.
+__device__ __forceinline__ int xcd_logical_block(int b, int nblocks)
+{
+    if (nblocks % 8 != 0) return b;
+    return (b & 7) * (nblocks >> 3) + (b >> 3);
+}
+
+// Kernels asking for more than 64 KiB of dynamic LDS must opt in (gfx950 has
+// 160 KiB per CU).
+template <typename Kernel>
+inline hipError_t allow_dynamic_lds(Kernel kernel, size_t bytes)
+{
+    if (bytes <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+}  // namespace dmlnn

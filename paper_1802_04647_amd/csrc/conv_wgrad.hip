@@ -1,0 +1,318 @@
+// conv2d backward_filter (+ fused relu mask and bias gradient) on the gfx950
+// matrix cores.
+//
+//   g          = dout masked to out_fwd > 0 (or dout when no mask is given)
+//   dW[f, k]   = sum_{n, q} g[n, f, q] * B_n[k, q],  k = (c, i, j), q = (oh, ow)
+//   db[f]      = sum_{n, q} g[n, f, q]
+// with B_n the (never materialised) patch matrix of image n.  This is a GEMM
+// with a small output (F x C*Hf*Wf) and a very long reduction (N*Hout*Wout), so
+// the reduction is split: block (f-tile, k-range, split) sums its share of the
+// (image, pixel-tile) list into registers and writes one partial dW (and db)
+// to the workspace; a second kernel adds the partials in split order.  The
+// partition depends only on the problem sizes, so results are bitwise
+// reproducible.
+//
+// Per pixel tile the block stages in LDS: the 64 x RQ slice of g (mask applied
+// while loading) and the rows of X that the tile's windows touch for the
+// channels of its k-range (zero padded).  Each of the 4 waves owns all 64 f rows
+// and NBW 16-column blocks of the k-range: per 4-pixel step it reads 4 g
+// fragments and NBW patch fragments and issues 4 x NBW MFMAs.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace dmlnn {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kBM = 64;
+constexpr size_t kLdsBudget = 72 * 1024;
+constexpr int kTargetBlocks = 512;
+
+struct WgradArgs {
+    const void *X, *dout, *mask;
+    void *ws;
+    int N, C, Hin, Win, F, Hf, Wf, HfWf, S, P, Hout, Wout, Q, K;
+    int KR, nkr, nft, RQ, tiles_per_img, T_total, splits;
+    int Wpad, CH, SG;
+};
+
+template <typename T, int NBW>
+__global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
+{
+    using MF = Mfma<T>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_g = reinterpret_cast<T *>(smem);
+    T *s_x = s_g + kBM * a.SG;
+    const int nch_alloc = (a.KR - 1) / a.HfWf + 2;
+    int *s_qoff = reinterpret_cast<int *>(s_x + (size_t)nch_alloc * a.CH);
+
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int L = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int kr = L % a.nkr;
+    const int rest = L / a.nkr;
+    const int ft = rest % a.nft;
+    const int split = rest / a.nft;
+
+    const int kbeg = kr * a.KR;
+    const int kend = min(a.K, kbeg + a.KR);
+    const int c_lo = kbeg / a.HfWf;
+    const int nch = (kend - 1) / a.HfWf - c_lo + 1;
+
+    int koff[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        int k = kbeg + (wave * NBW + nb) * 16 + (lane & 15);
+        int c = k / a.HfWf, t = k - c * a.HfWf;
+        int i = t / a.Wf, j = t - i * a.Wf;
+        koff[nb] = (k < kend) ? (c - c_lo) * a.CH + i * a.Wpad + j : 0;
+    }
+
+    typename MF::acc_t acc[4][NBW];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = MF::zero();
+    T dbacc = T(0);
+
+    const T *X = reinterpret_cast<const T *>(a.X);
+    const T *dout = reinterpret_cast<const T *>(a.dout);
+    const T *mask = reinterpret_cast<const T *>(a.mask);
+    const long long t_begin = (long long)split * a.T_total / a.splits;
+    const long long t_end = (long long)(split + 1) * a.T_total / a.splits;
+
+    for (long long tt = t_begin; tt < t_end; ++tt) {
+        const int n = (int)(tt / a.tiles_per_img);
+        const int qt = (int)(tt - (long long)n * a.tiles_per_img);
+        const int q0 = qt * a.RQ;
+        const int qend = min(q0 + a.RQ, a.Q);
+        const int qy0 = q0 / a.Wout;
+        const int rows_need = ((qend - 1) / a.Wout - qy0) * a.S + a.Hf;
+        const int ybase = qy0 * a.S - a.P;
+
+        __syncthreads();
+        for (int r = wave; r < kBM; r += kThreads / kWave) {
+            int fg = ft * kBM + r;
+            size_t goff = ((size_t)n * a.F + fg) * a.Q;
+            for (int u = lane; u < a.RQ; u += kWave) {
+                int q = q0 + u;
+                T v = T(0);
+                if (fg < a.F && q < qend) {
+                    v = dout[goff + q];
+                    if (mask && !(mask[goff + q] > T(0))) v = T(0);
+                }
+                s_g[r * a.SG + u] = v;
+            }
+        }
+        const int nrows = nch * rows_need;
+        for (int r = wave; r < nrows; r += kThreads / kWave) {
+            int c = r / rows_need, t = r - c * rows_need;
+            int cg = c_lo + c, y = ybase + t;
+            bool rowok = cg < a.C && y >= 0 && y < a.Hin;
+            size_t xoff = (((size_t)n * a.C + cg) * a.Hin + (rowok ? y : 0)) * a.Win;
+            T *dst = s_x + c * a.CH + t * a.Wpad;
+            for (int u = lane; u < a.Wpad; u += kWave) {
+                int x = u - a.P;
+                dst[u] = (rowok && x >= 0 && x < a.Win) ? X[xoff + x] : T(0);
+            }
+        }
+        for (int u = tid; u < a.RQ; u += kThreads) {
+            int q = q0 + u;
+            int qy = q / a.Wout, qx = q - qy * a.Wout;
+            s_qoff[u] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+        }
+        __syncthreads();
+
+        if (kr == 0) {  // bias gradient: thread (f = tid/4, phase = tid%4), fixed order
+            const T *gr = s_g + (tid >> 2) * a.SG;
+            for (int u = tid & 3; u < a.RQ; u += 4) dbacc += gr[u];
+        }
+
+        const T *grow = s_g + (lane & 15) * a.SG + (lane >> 4);
+        const int *qof = s_qoff + (lane >> 4);
+        for (int qq = 0; qq < a.RQ; qq += 4) {
+            const int qo = qof[qq];
+            T av[4];
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG + qq];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                T bv = s_x[koff[nb] + qo];
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
+            }
+        }
+    }
+
+    T *wsp = reinterpret_cast<T *>(a.ws) + (size_t)split * a.F * a.K;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                int f = ft * kBM + mb * 16 + MF::row(lane, r);
+                int k = kbeg + (wave * NBW + nb) * 16 + (lane & 15);
+                if (f < a.F && k < kend) wsp[(size_t)f * a.K + k] = acc[mb][nb][r];
+            }
+
+    if (kr == 0) {
+        __syncthreads();
+        T *s_red = s_g;
+        s_red[tid] = dbacc;
+        __syncthreads();
+        if (tid < kBM) {
+            int f = ft * kBM + tid;
+            if (f < a.F) {
+                T s = s_red[4 * tid] + s_red[4 * tid + 1] + s_red[4 * tid + 2] + s_red[4 * tid + 3];
+                T *wsdb = reinterpret_cast<T *>(a.ws) + (size_t)a.splits * a.F * a.K;
+                wsdb[(size_t)split * a.F + f] = s;
+            }
+        }
+    }
+}
+
+// dW[e] = sum over splits of the partials, in split order (double accumulation);
+// the last F threads do the same for db.
+template <typename T>
+__global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *db, int FK, int F,
+                                                         int splits)
+{
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e < FK) {
+        double s = 0.0;
+        for (int sp = 0; sp < splits; ++sp) s += (double)ws[(size_t)sp * FK + e];
+        dW[e] = (T)s;
+    } else if (db && e < FK + F) {
+        const int f = e - FK;
+        const T *wsdb = ws + (size_t)splits * FK;
+        double s = 0.0;
+        for (int sp = 0; sp < splits; ++sp) s += (double)wsdb[(size_t)sp * F + f];
+        db[f] = (T)s;
+    }
+}
+
+struct WPlan {
+    int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG;
+    long long T_total;
+    size_t lds;
+};
+
+size_t wlds(size_t tsz, int SG, int nch, int CH, int RQ)
+{
+    return tsz * ((size_t)kBM * SG + (size_t)nch * CH) + sizeof(int) * (size_t)RQ;
+}
+
+bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
+{
+    const int K = d.C * d.Hf * d.Wf;
+    const int HfWf = d.Hf * d.Wf;
+    const int Q = d.Hout * d.Wout;
+    p.NBW = K > 128 ? 3 : (K > 64 ? 2 : 1);
+    p.KR = 64 * p.NBW;
+    p.nkr = (K + p.KR - 1) / p.KR;
+    p.nft = (d.F + kBM - 1) / kBM;
+    p.Wpad = (d.Wout - 1) * d.stride + d.Wf;
+    const int nch_alloc = (p.KR - 1) / HfWf + 2;
+    // Pixel tile: whole output rows, about 64 pixels, a multiple of 4.
+    int rq = d.Wout * (d.Wout >= 64 ? 1 : 64 / d.Wout);
+    if (rq > Q) rq = Q;
+    rq = ((rq + 3) / 4) * 4;
+    for (;;) {
+        int rows_max = ((d.Wout + rq - 2) / d.Wout) * d.stride + d.Hf;
+        int CH = rows_max * p.Wpad;
+        int SG = rq + 1;
+        size_t lds = wlds(tsz, SG, nch_alloc, CH, rq);
+        if (lds <= kLdsBudget || rq <= 4) {
+            p.RQ = rq;
+            p.CH = CH;
+            p.SG = SG;
+            p.lds = lds;
+            break;
+        }
+        rq = ((rq / 2 + 3) / 4) * 4;
+    }
+    if (p.lds > 160 * 1024) return false;
+    p.tiles_per_img = (Q + p.RQ - 1) / p.RQ;
+    p.T_total = (long long)d.N * p.tiles_per_img;
+    const int per_split = p.nkr * p.nft;
+    long long splits = (kTargetBlocks + per_split - 1) / per_split;
+    if (splits >= 8) splits = ((splits + 7) / 8) * 8;
+    if (splits > p.T_total) splits = p.T_total;
+    if (splits < 1) splits = 1;
+    p.splits = (int)splits;
+    return true;
+}
+
+template <typename T>
+hipError_t launch_w(const WgradArgs &a, const WPlan &p, void *dW, void *db, hipStream_t s)
+{
+    dim3 grid(p.splits * p.nkr * p.nft), block(kThreads);
+    auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3> : (p.NBW == 2 ? conv_wgrad_kernel<T, 2>
+                                                                : conv_wgrad_kernel<T, 1>);
+    hipError_t e = allow_dynamic_lds(k, p.lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int FK = a.F * a.K;
+    const int total = FK + (db ? a.F : 0);
+    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 255) / 256), dim3(256), 0, s,
+                       reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
+                       reinterpret_cast<T *>(db), FK, a.F, a.splits);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d)
+{
+    const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
+    WPlan p;
+    if (!make_wplan(tsz, d, p)) return 0;
+    const size_t K = (size_t)d.C * d.Hf * d.Wf;
+    return tsz * (size_t)p.splits * ((size_t)d.F * K + (size_t)d.F);
+}
+
+hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
+                                       const void *out_fwd, void *dW, void *db,
+                                       const ConvDims &d, void *ws, int zero_skip,
+                                       hipStream_t s)
+{
+    (void)zero_skip;
+    const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
+    WPlan p;
+    if (!make_wplan(tsz, d, p)) return hipErrorInvalidValue;
+    WgradArgs a = {};
+    a.X = X;
+    a.dout = dout;
+    a.mask = out_fwd;
+    a.ws = ws;
+    a.N = d.N;
+    a.C = d.C;
+    a.Hin = d.Hin;
+    a.Win = d.Win;
+    a.F = d.F;
+    a.Hf = d.Hf;
+    a.Wf = d.Wf;
+    a.HfWf = d.Hf * d.Wf;
+    a.S = d.stride;
+    a.P = d.pad;
+    a.Hout = d.Hout;
+    a.Wout = d.Wout;
+    a.Q = d.Hout * d.Wout;
+    a.K = d.C * d.Hf * d.Wf;
+    a.KR = p.KR;
+    a.nkr = p.nkr;
+    a.nft = p.nft;
+    a.RQ = p.RQ;
+    a.tiles_per_img = p.tiles_per_img;
+    a.T_total = (int)p.T_total;
+    a.splits = p.splits;
+    a.Wpad = p.Wpad;
+    a.CH = p.CH;
+    a.SG = p.SG;
+    if (dtype == 0) return launch_w<double>(a, p, dW, db, s);
+    return launch_w<float>(a, p, dW, db, s);
+}
+
+}  // namespace dmlnn

@@ -1,0 +1,52 @@
+// Host-side launch interface between the C ABI (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dmlnn {
+
+// ---------------------------------------------------------------- conv2d ----
+// Geometry of one conv2d call (already validated).
+struct ConvDims {
+    int N, C, Hin, Win, F, Hf, Wf, stride, pad, Hout, Wout;
+};
+
+// Forward (relu(conv + b)) and input-gradient passes share one implicit-GEMM
+// kernel family; see conv_igemm.hip.
+hipError_t launch_conv_forward(int dtype, const void *X, const void *W, const void *b, void *out,
+                               const ConvDims &d, int relu, int zero_skip, hipStream_t s);
+hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
+                                     const void *out_fwd, void *dX, const ConvDims &d,
+                                     int zero_skip, hipStream_t s);
+
+// Filter/bias gradient: split reduction into a workspace, then a fixed-order sum.
+size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d);
+hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
+                                       const void *out_fwd, void *dW, void *db,
+                                       const ConvDims &d, void *ws, int zero_skip,
+                                       hipStream_t s);
+
+// ----------------------------------------------------------------- others ----
+hipError_t launch_bias_add_relu(int dtype, const void *X, const void *b, void *out, int N, int C,
+                                int HW, int relu, hipStream_t s);
+hipError_t launch_max_pool_fwd(int dtype, const void *X, void *out, int32_t *argmax, int N, int C,
+                               int Hin, int Win, int Hf, int Wf, int stride, int pad, int Hout,
+                               int Wout, hipStream_t s);
+hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax, void *dX, int N,
+                               int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
+                               int Hout, int Wout, hipStream_t s);
+hipError_t launch_affine_fwd(int dtype, const void *X, const void *W, const void *b, void *out,
+                             int N, int D, int M, int relu, hipStream_t s);
+hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const void *W,
+                             const void *out_fwd, void *dX, void *dW, void *db, int N, int D,
+                             int M, hipStream_t s);
+hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
+                               void *loss, int N, int K, hipStream_t s);
+hipError_t launch_sgd_momentum(int dtype, void *theta, const void *grad, void *v, double lr,
+                               double mu, long long n, hipStream_t s);
+hipError_t launch_count_nonzero(int dtype, const void *X, long long n, long long *out,
+                                hipStream_t s);
+
+}  // namespace dmlnn

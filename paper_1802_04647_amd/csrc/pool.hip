@@ -1,0 +1,135 @@
+// max_pool2d forward (value + in-row argmax) and backward (gradient routing).
+// Paper, Section 3 "Builtin NN Functions": pooling and its backward are builtins.
+//
+// Both are memory-bound streaming kernels over the row-major N x (C*H*W)
+// matrices.  Forward: one thread per output, window scanned row by row,
+// replacing the running maximum only on a strictly larger value (first maximum
+// wins ties; +0 and -0 compare equal).  Backward: one thread per INPUT cell
+// gathers the outputs whose window covers it and whose argmax is that cell, so
+// every dX element is written exactly once, without atomics and in a fixed
+// order.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace dmlnn {
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void max_pool_fwd_kernel(const T *__restrict__ X,
+                                                           T *__restrict__ out,
+                                                           int32_t *__restrict__ argmax,
+                                                           long long total, int C, int Hin,
+                                                           int Win, int Hf, int Wf, int S, int P,
+                                                           int Hout, int Wout)
+{
+    for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total;
+         e += (long long)gridDim.x * 256) {
+        const int ow = (int)(e % Wout);
+        long long r = e / Wout;
+        const int oh = (int)(r % Hout);
+        r /= Hout;
+        const int c = (int)(r % C);
+        const long long n = r / C;
+        const T *plane = X + (size_t)n * C * Hin * Win + (size_t)c * Hin * Win;
+        const int h0 = oh * S - P, w0 = ow * S - P;
+        T best = T(0);
+        int bidx = -1;
+        for (int i = 0; i < Hf; ++i) {
+            const int h = h0 + i;
+            if (h < 0 || h >= Hin) continue;
+            for (int j = 0; j < Wf; ++j) {
+                const int w = w0 + j;
+                if (w < 0 || w >= Win) continue;
+                const T v = plane[h * Win + w];
+                if (bidx < 0 || v > best) {
+                    best = v;
+                    bidx = h * Win + w;
+                }
+            }
+        }
+        out[e] = best;
+        argmax[e] = c * Hin * Win + bidx;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void max_pool_bwd_kernel(const T *__restrict__ dout,
+                                                           const int32_t *__restrict__ argmax,
+                                                           T *__restrict__ dX, long long total,
+                                                           int C, int Hin, int Win, int Hf,
+                                                           int Wf, int S, int P, int Hout,
+                                                           int Wout)
+{
+    for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total;
+         e += (long long)gridDim.x * 256) {
+        const int w = (int)(e % Win);
+        long long r = e / Win;
+        const int h = (int)(r % Hin);
+        r /= Hin;
+        const int c = (int)(r % C);
+        const long long n = r / C;
+        const int32_t me = c * Hin * Win + h * Win + w;
+        const size_t obase = (size_t)n * C * Hout * Wout + (size_t)c * Hout * Wout;
+        // outputs (oh, ow) whose window [oh*S-P, oh*S-P+Hf) contains h
+        int oh_lo = h + P - Hf + 1;
+        oh_lo = oh_lo <= 0 ? 0 : (oh_lo + S - 1) / S;
+        int oh_hi = (h + P) / S;
+        if (oh_hi > Hout - 1) oh_hi = Hout - 1;
+        int ow_lo = w + P - Wf + 1;
+        ow_lo = ow_lo <= 0 ? 0 : (ow_lo + S - 1) / S;
+        int ow_hi = (w + P) / S;
+        if (ow_hi > Wout - 1) ow_hi = Wout - 1;
+        T acc = T(0);
+        for (int oh = oh_lo; oh <= oh_hi; ++oh)
+            for (int ow = ow_lo; ow <= ow_hi; ++ow) {
+                const size_t o = obase + (size_t)oh * Wout + ow;
+                if (argmax[o] == me) acc += dout[o];
+            }
+        dX[e] = acc;
+    }
+}
+
+int grid_for(long long total)
+{
+    long long g = (total + 255) / 256;
+    const long long cap = 256LL * 64;
+    return (int)(g < 1 ? 1 : (g > cap ? cap : g));
+}
+
+}  // namespace
+
+hipError_t launch_max_pool_fwd(int dtype, const void *X, void *out, int32_t *argmax, int N, int C,
+                               int Hin, int Win, int Hf, int Wf, int stride, int pad, int Hout,
+                               int Wout, hipStream_t s)
+{
+    const long long total = (long long)N * C * Hout * Wout;
+    const int g = grid_for(total);
+    if (dtype == 0)
+        hipLaunchKernelGGL(max_pool_fwd_kernel<double>, dim3(g), dim3(256), 0, s,
+                           (const double *)X, (double *)out, argmax, total, C, Hin, Win, Hf, Wf,
+                           stride, pad, Hout, Wout);
+    else
+        hipLaunchKernelGGL(max_pool_fwd_kernel<float>, dim3(g), dim3(256), 0, s, (const float *)X,
+                           (float *)out, argmax, total, C, Hin, Win, Hf, Wf, stride, pad, Hout,
+                           Wout);
+    return hipGetLastError();
+}
+
+hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax, void *dX, int N,
+                               int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
+                               int Hout, int Wout, hipStream_t s)
+{
+    const long long total = (long long)N * C * Hin * Win;
+    const int g = grid_for(total);
+    if (dtype == 0)
+        hipLaunchKernelGGL(max_pool_bwd_kernel<double>, dim3(g), dim3(256), 0, s,
+                           (const double *)dout, argmax, (double *)dX, total, C, Hin, Win, Hf, Wf,
+                           stride, pad, Hout, Wout);
+    else
+        hipLaunchKernelGGL(max_pool_bwd_kernel<float>, dim3(g), dim3(256), 0, s,
+                           (const float *)dout, argmax, (float *)dX, total, C, Hin, Win, Hf, Wf,
+                           stride, pad, Hout, Wout);
+    return hipGetLastError();
+}
+
+}  // namespace dmlnn

@@ -1,0 +1,330 @@
+"""Thin Python binding of libdmlnn.so (the C ABI in include/dmlnn.h).
+
+Argument marshalling only: every function checks that its tensors are
+contiguous device tensors of one floating dtype (float64 or float32), passes
+their device pointers, sizes and torch's current HIP stream to the C entry
+point of the same name, and raises :class:`DmlnnError` with the library's
+message on a nonzero status.  Outputs not supplied by the caller are allocated
+with ``torch.empty`` on the inputs' device (torch is used only for memory and
+streams).  Every computation runs in the library's HIP kernels; there is no
+fallback: if the library is missing, the first call raises.
+
+Layer-level signatures follow the paper's DML layers (Section 2 and 3):
+``conv2d_forward(X, W, b, C, Hin, Win, Hf, Wf, stride, pad)`` etc., with N and F
+taken from the row counts of X and W.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdmlnn.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "dmlnn.h")
+
+F64, F32 = 0, 1
+_DT = {torch.float64: F64, torch.float32: F32}
+
+
+class DmlnnError(RuntimeError):
+    def __init__(self, name, status, msg):
+        super().__init__(f"{name} failed with status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+
+
+def load():
+    """Load libdmlnn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_1802_04647_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "conv2d_out_dim": (_i, [_i] * 4),
+        "conv2d_forward": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 10 + [_vp]),
+        "conv2d_backward_filter_workspace_size": (ctypes.c_size_t, [_i] * 10),
+        "conv2d_backward_filter": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9
+                                   + [_vp, ctypes.c_size_t, _vp]),
+        "conv2d_backward_data": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
+        "dmlnn_set_zero_skip": (_i, [_i]),
+        "bias_add_relu": (_i, [_i, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
+        "max_pool2d_fwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
+        "max_pool2d_bwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
+        "affine_fwd": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
+        "affine_bwd": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 3 + [_vp]),
+        "softmax_xent": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _vp]),
+        "sgd_momentum_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_longlong, _vp]),
+        "count_nonzero": (_i, [_i, _vp, ctypes.c_longlong, _vp, _vp]),
+        "dmlnn_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def header_symbols():
+    """Names of the entry points declared in include/dmlnn.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return re.findall(r"^DMLNN_API\s+(?:const\s+)?\w+\s*\**\s*(\w+)\s*\(", text, re.M)
+
+
+def last_error() -> str:
+    return load().dmlnn_last_error().decode()
+
+
+def _check(name, rc):
+    if rc != 0:
+        raise DmlnnError(name, rc, last_error())
+
+
+def _dtype(*ts):
+    dt = None
+    for t in ts:
+        if t is None:
+            continue
+        d = _DT.get(t.dtype)
+        if d is None:
+            raise TypeError(f"unsupported dtype {t.dtype}; use float64 or float32")
+        if dt is not None and d != dt:
+            raise TypeError("all floating tensors of a call must share one dtype")
+        dt = d
+    return dt
+
+
+def _p(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("dmlnn tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("dmlnn tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _need(t, n, name):
+    """Host-side guard: a buffer must hold exactly the elements the call will touch."""
+    if t is not None and t.numel() != n:
+        raise ValueError(f"{name} has {t.numel()} elements, the call needs {n}")
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _empty(shape, like, dtype=None):
+    return torch.empty(shape, dtype=dtype or like.dtype, device=like.device)
+
+
+def conv2d_out_dim(Hin, Hf, stride, pad) -> int:
+    return int(load().conv2d_out_dim(Hin, Hf, stride, pad))
+
+
+def set_zero_skip(mode: int) -> int:
+    """0 = dense, 1 = wavefront-ballot zero skip.  Returns the previous mode."""
+    r = load().dmlnn_set_zero_skip(int(mode))
+    if r < 0:
+        raise ValueError(f"invalid zero-skip mode {mode}")
+    return r
+
+
+# ------------------------------------------------------------------------- conv2d
+def conv2d_forward(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True, out=None):
+    """out = relu(conv2d(X, W) + b): N x (F*Hout*Wout).  Returns (out, Hout, Wout)."""
+    dt = _dtype(X, W, b, out)
+    N, F = X.shape[0], W.shape[0]
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    if out is None:
+        out = _empty((N, F * max(Hout, 0) * max(Wout, 0)), X)
+    _need(X, N * C * Hin * Win, "X")
+    _need(W, F * C * Hf * Wf, "W")
+    _need(b, F, "b")
+    _need(out, N * F * max(Hout, 0) * max(Wout, 0), "out")
+    _check("conv2d_forward", load().conv2d_forward(
+        dt, _p(X), _p(W), _p(b), _p(out), N, C, Hin, Win, F, Hf, Wf, stride, pad,
+        int(bool(relu)), _stream()))
+    return out, Hout, Wout
+
+
+def conv2d_backward_filter_workspace_size(dtype, N, C, Hin, Win, F, Hf, Wf, stride, pad) -> int:
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return int(load().conv2d_backward_filter_workspace_size(dt, N, C, Hin, Win, F, Hf, Wf,
+                                                            stride, pad))
+
+
+def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F,
+                           want_db=True, workspace=None, dW=None, db=None):
+    """Returns (dW F x C*Hf*Wf, db F or None); out_fwd None means no relu mask."""
+    dt = _dtype(X, dout, out_fwd, dW, db)
+    N = X.shape[0]
+    need = conv2d_backward_filter_workspace_size(dt, N, C, Hin, Win, F, Hf, Wf, stride, pad)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=X.device)
+    if dW is None:
+        dW = _empty((F, C * Hf * Wf), X)
+    if db is None and want_db:
+        db = _empty((F,), X)
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    _need(X, N * C * Hin * Win, "X")
+    _need(dout, N * F * max(Hout, 0) * max(Wout, 0), "dout")
+    _need(out_fwd, N * F * max(Hout, 0) * max(Wout, 0), "out_fwd")
+    _need(dW, F * C * Hf * Wf, "dW")
+    _need(db, F, "db")
+    _check("conv2d_backward_filter", load().conv2d_backward_filter(
+        dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
+        stride, pad, _p(workspace), workspace.numel() * workspace.element_size(), _stream()))
+    return dW, db
+
+
+def conv2d_backward_data(W, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+    """Returns dX, N x (C*Hin*Win)."""
+    dt = _dtype(W, dout, out_fwd, dX)
+    N, F = dout.shape[0], W.shape[0]
+    if dX is None:
+        dX = _empty((N, C * Hin * Win), dout)
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    _need(W, F * C * Hf * Wf, "W")
+    _need(dout, N * F * max(Hout, 0) * max(Wout, 0), "dout")
+    _need(out_fwd, N * F * max(Hout, 0) * max(Wout, 0), "out_fwd")
+    _need(dX, N * C * Hin * Win, "dX")
+    _check("conv2d_backward_data", load().conv2d_backward_data(
+        dt, _p(W), _p(dout), _p(out_fwd), _p(dX), N, C, Hin, Win, F, Hf, Wf, stride, pad,
+        _stream()))
+    return dX
+
+
+# -------------------------------------------------------------------------- others
+def bias_add_relu(X, b, C, HW, relu=True, out=None):
+    dt = _dtype(X, b, out)
+    if out is None:
+        out = torch.empty_like(X)
+    _need(X, X.shape[0] * C * HW, "X")
+    _need(b, C, "b")
+    _need(out, X.numel(), "out")
+    _check("bias_add_relu", load().bias_add_relu(dt, _p(X), _p(b), _p(out), X.shape[0], C, HW,
+                                                  int(bool(relu)), _stream()))
+    return out
+
+
+def max_pool2d_fwd(X, C, Hin, Win, Hf, Wf, stride, pad, out=None, argmax=None):
+    """Returns (out, argmax int32, Hout, Wout)."""
+    dt = _dtype(X, out)
+    N = X.shape[0]
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    cols = C * max(Hout, 0) * max(Wout, 0)
+    if out is None:
+        out = _empty((N, cols), X)
+    if argmax is None:
+        argmax = _empty((N, cols), X, dtype=torch.int32)
+    _need(X, N * C * Hin * Win, "X")
+    _need(out, N * cols, "out")
+    _need(argmax, N * cols, "argmax")
+    _check("max_pool2d_fwd", load().max_pool2d_fwd(dt, _p(X), _p(out), _p(argmax), N, C, Hin,
+                                                    Win, Hf, Wf, stride, pad, _stream()))
+    return out, argmax, Hout, Wout
+
+
+def max_pool2d_bwd(dout, argmax, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+    dt = _dtype(dout, dX)
+    if argmax.dtype != torch.int32:
+        raise TypeError("argmax must be int32")
+    N = dout.shape[0]
+    if dX is None:
+        dX = _empty((N, C * Hin * Win), dout)
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    _need(dout, N * C * max(Hout, 0) * max(Wout, 0), "dout")
+    _need(argmax, N * C * max(Hout, 0) * max(Wout, 0), "argmax")
+    _need(dX, N * C * Hin * Win, "dX")
+    _check("max_pool2d_bwd", load().max_pool2d_bwd(dt, _p(dout), _p(argmax), _p(dX), N, C, Hin,
+                                                    Win, Hf, Wf, stride, pad, _stream()))
+    return dX
+
+
+def affine_fwd(X, W, b, relu=False, out=None):
+    dt = _dtype(X, W, b, out)
+    N, D = X.shape
+    M = W.shape[1]
+    if out is None:
+        out = _empty((N, M), X)
+    _need(W, D * M, "W")
+    _need(b, M, "b")
+    _need(out, N * M, "out")
+    _check("affine_fwd", load().affine_fwd(dt, _p(X), _p(W), _p(b), _p(out), N, D, M,
+                                            int(bool(relu)), _stream()))
+    return out
+
+
+def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW=None, db=None):
+    """Returns [dX, dW, db] (dX / db None when not wanted)."""
+    dt = _dtype(dout, X, W, out_fwd, dX, dW, db)
+    N, D = X.shape
+    M = W.shape[1]
+    if dX is None and want_dX:
+        dX = _empty((N, D), X)
+    if dW is None:
+        dW = _empty((D, M), X)
+    if db is None and want_db:
+        db = _empty((M,), X)
+    _need(W, D * M, "W")
+    _need(dout, N * M, "dout")
+    _need(out_fwd, N * M, "out_fwd")
+    _need(dX, N * D, "dX")
+    _need(dW, D * M, "dW")
+    _need(db, M, "db")
+    _check("affine_bwd", load().affine_bwd(dt, _p(dout), _p(X), _p(W), _p(out_fwd), _p(dX),
+                                            _p(dW), _p(db), N, D, M, _stream()))
+    return dX, dW, db
+
+
+def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None):
+    """Returns (loss as a 1-element device tensor, dscores, probs-or-None)."""
+    dt = _dtype(scores, Y, loss, dscores, probs)
+    N, K = scores.shape
+    if loss is None:
+        loss = _empty((1,), scores)
+    if dscores is None:
+        dscores = torch.empty_like(scores)
+    if probs is None and want_probs:
+        probs = torch.empty_like(scores)
+    _need(Y, N * K, "Y")
+    _need(dscores, N * K, "dscores")
+    _need(probs, N * K, "probs")
+    _need(loss, 1, "loss")
+    _check("softmax_xent", load().softmax_xent(dt, _p(scores), _p(Y), _p(probs), _p(dscores),
+                                                _p(loss), N, K, _stream()))
+    return loss, dscores, probs
+
+
+def sgd_momentum_update(theta, grad, v, lr, mu):
+    """In place: v <- mu v - lr grad; theta <- theta + v."""
+    dt = _dtype(theta, grad, v)
+    _need(grad, theta.numel(), "grad")
+    _need(v, theta.numel(), "v")
+    _check("sgd_momentum_update", load().sgd_momentum_update(
+        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream()))
+    return theta, v
+
+
+def count_nonzero(X, out=None):
+    """Number of non-zero entries, as a 1-element int64 device tensor."""
+    dt = _dtype(X)
+    if out is None:
+        out = _empty((1,), X, dtype=torch.int64)
+    if out.dtype != torch.int64 or out.numel() < 1:
+        raise ValueError("out must be an int64 tensor with at least one element")
+    _check("count_nonzero", load().count_nonzero(dt, _p(X), X.numel(), _p(out), _stream()))
+    return out

@@ -1,0 +1,69 @@
+"""One SGD-momentum training step of the LeNet-style network, on the GPU library.
+
+conv(1->32, 5x5, p2)+relu -> max-pool 2x2/2 -> conv(32->64, 5x5, p2)+relu ->
+max-pool 2x2/2 -> affine 3136->512 + relu -> affine 512->10 -> softmax +
+cross-entropy; backward in reverse order; then v <- mu v - lr g and
+theta <- theta + v for the eight parameter tensors (paper, Section 2: the NN
+library's layers, its minibatch training loop and SGD with momentum).
+
+All activations, gradients and the backward-filter workspaces are allocated
+once; ``step`` only enqueues library calls on the current stream (about twenty
+launches) and returns the loss as a device scalar.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import dmlnn
+
+PARAM_ORDER = ("W1", "b1", "W2", "b2", "W3", "b3", "W4", "b4")
+
+
+class LeNetTrainer:
+    def __init__(self, params: dict, N: int = 64, lr: float = 0.01, mu: float = 0.9,
+                 dtype=torch.float64, device="cuda"):
+        self.N, self.lr, self.mu = N, lr, mu
+        kw = dict(dtype=dtype, device=device)
+        self.p = {k: torch.as_tensor(v).to(**kw).contiguous() for k, v in params.items()}
+        self.v = {k: torch.zeros_like(t) for k, t in self.p.items()}
+        self.g = {k: torch.empty_like(t) for k, t in self.p.items()}
+        e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
+        i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
+        self.c1, self.p1, self.i1 = e(N, 32 * 784), e(N, 32 * 196), i32(N, 32 * 196)
+        self.c2, self.p2, self.i2 = e(N, 64 * 196), e(N, 64 * 49), i32(N, 64 * 49)
+        self.h, self.s = e(N, 512), e(N, 10)
+        self.loss, self.ds = e(1), e(N, 10)
+        self.dh, self.dp2, self.dc2 = e(N, 512), e(N, 3136), e(N, 64 * 196)
+        self.dp1, self.dc1 = e(N, 32 * 196), e(N, 32 * 784)
+        ws1 = dmlnn.conv2d_backward_filter_workspace_size(dtype, N, 1, 28, 28, 32, 5, 5, 1, 2)
+        ws2 = dmlnn.conv2d_backward_filter_workspace_size(dtype, N, 32, 14, 14, 64, 5, 5, 1, 2)
+        self.ws1 = torch.empty(ws1, dtype=torch.uint8, device=device)
+        self.ws2 = torch.empty(ws2, dtype=torch.uint8, device=device)
+
+    def forward_backward(self, X, Y):
+        p, g = self.p, self.g
+        dmlnn.conv2d_forward(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, relu=True, out=self.c1)
+        dmlnn.max_pool2d_fwd(self.c1, 32, 28, 28, 2, 2, 2, 0, out=self.p1, argmax=self.i1)
+        dmlnn.conv2d_forward(self.p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, relu=True,
+                             out=self.c2)
+        dmlnn.max_pool2d_fwd(self.c2, 64, 14, 14, 2, 2, 2, 0, out=self.p2, argmax=self.i2)
+        dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h)
+        dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s)
+        dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds)
+        dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"])
+        dmlnn.affine_bwd(self.dh, self.p2, p["W3"], self.h, dX=self.dp2, dW=g["W3"], db=g["b3"])
+        dmlnn.max_pool2d_bwd(self.dp2, self.i2, 64, 14, 14, 2, 2, 2, 0, dX=self.dc2)
+        dmlnn.conv2d_backward_filter(self.p1, self.dc2, self.c2, 32, 14, 14, 5, 5, 1, 2, 64,
+                                     workspace=self.ws2, dW=g["W2"], db=g["b2"])
+        dmlnn.conv2d_backward_data(p["W2"], self.dc2, self.c2, 32, 14, 14, 5, 5, 1, 2,
+                                   dX=self.dp1)
+        dmlnn.max_pool2d_bwd(self.dp1, self.i1, 32, 28, 28, 2, 2, 2, 0, dX=self.dc1)
+        dmlnn.conv2d_backward_filter(X, self.dc1, self.c1, 1, 28, 28, 5, 5, 1, 2, 32,
+                                     workspace=self.ws1, dW=g["W1"], db=g["b1"])
+        return self.loss
+
+    def step(self, X, Y):
+        loss = self.forward_backward(X, Y)
+        for k in PARAM_ORDER:
+            dmlnn.sgd_momentum_update(self.p[k], self.g[k], self.v[k], self.lr, self.mu)
+        return loss

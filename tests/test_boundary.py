@@ -1,0 +1,124 @@
+"""The C ABI boundary on the CPU: the library loads, exports every entry point
+that include/dmlnn.h declares, and rejects bad arguments on the host with the
+documented status codes before launching anything (no GPU needed: every call
+below fails validation, so no pointer is ever dereferenced)."""
+import ctypes
+
+import pytest
+
+from paper_1802_04647_amd import dmlnn
+
+OK, ERR_ARG, ERR_NULL, ERR_DTYPE, ERR_WS, ERR_DEVICE = 0, 1, 2, 3, 4, 5
+FAKE = 0x1000  # never dereferenced: every call using it fails validation first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return dmlnn.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = dmlnn.header_symbols()
+    expected = {"conv2d_out_dim", "conv2d_forward", "conv2d_backward_filter_workspace_size",
+                "conv2d_backward_filter", "conv2d_backward_data", "dmlnn_set_zero_skip",
+                "bias_add_relu", "max_pool2d_fwd", "max_pool2d_bwd", "affine_fwd", "affine_bwd",
+                "softmax_xent", "sgd_momentum_update", "count_nonzero", "dmlnn_last_error"}
+    assert expected <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_out_dim(lib):
+    assert lib.conv2d_out_dim(56, 3, 1, 1) == 56
+    assert lib.conv2d_out_dim(28, 5, 1, 2) == 28
+    assert lib.conv2d_out_dim(28, 2, 2, 0) == 14
+    assert lib.conv2d_out_dim(7, 3, 2, 0) == 3
+    assert lib.conv2d_out_dim(2, 3, 1, 0) <= 0
+    assert lib.conv2d_out_dim(5, 3, 0, 0) <= 0
+    assert lib.conv2d_out_dim(5, 3, 1, -1) <= 0
+
+
+def test_workspace_size(lib):
+    f = lib.conv2d_backward_filter_workspace_size
+    w64 = f(0, 256, 64, 56, 56, 64, 3, 3, 1, 1)
+    w32 = f(1, 256, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert w64 > 0 and w32 > 0 and w64 == 2 * w32
+    assert f(0, 4, 1, 8, 8, 2, 3, 3, 1, 1) > 0
+    assert f(7, 4, 1, 8, 8, 2, 3, 3, 1, 1) == 0          # bad dtype
+    assert f(0, 0, 1, 8, 8, 2, 3, 3, 1, 1) == 0          # N = 0
+    assert f(0, 4, 1, 2, 2, 2, 3, 3, 1, 0) == 0          # no window fits
+
+
+def _conv_fwd(lib, dt=0, X=FAKE, W=FAKE, out=FAKE, N=2, C=1, H=8, Wd=8, F=2, Hf=3, Wf=3, s=1,
+              p=1, relu=1):
+    return lib.conv2d_forward(dt, X, W, None, out, N, C, H, Wd, F, Hf, Wf, s, p, relu, None)
+
+
+def test_conv_forward_validation(lib):
+    assert _conv_fwd(lib, dt=2) == ERR_DTYPE
+    assert _conv_fwd(lib, X=None) == ERR_NULL
+    assert _conv_fwd(lib, out=None) == ERR_NULL
+    assert "required" in dmlnn.last_error()
+    assert _conv_fwd(lib, N=0) == ERR_ARG
+    assert _conv_fwd(lib, s=0) == ERR_ARG
+    assert _conv_fwd(lib, p=-1) == ERR_ARG
+    assert _conv_fwd(lib, H=2, Hf=5, p=0) == ERR_ARG
+    assert _conv_fwd(lib, relu=2) == ERR_ARG
+    assert _conv_fwd(lib, N=70000, C=64, H=100, Wd=100) == ERR_ARG   # > 2^31 elements
+
+
+def test_conv_backward_validation(lib):
+    bf = lib.conv2d_backward_filter
+    need = lib.conv2d_backward_filter_workspace_size(0, 2, 1, 8, 8, 2, 3, 3, 1, 1)
+    assert bf(0, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None, need, None) == ERR_WS
+    assert bf(0, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, FAKE, need - 1,
+              None) == ERR_WS
+    assert "workspace" in dmlnn.last_error()
+    assert bf(0, None, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, FAKE, need,
+              None) == ERR_NULL
+    assert bf(5, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, FAKE, need,
+              None) == ERR_DTYPE
+    bd = lib.conv2d_backward_data
+    assert bd(0, FAKE, FAKE, None, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_NULL
+    assert bd(0, FAKE, FAKE, None, FAKE, 2, 1, 8, 8, 2, 3, 3, 0, 1, None) == ERR_ARG
+
+
+def test_other_validation(lib):
+    assert lib.bias_add_relu(0, None, None, FAKE, 2, 3, 4, 1, None) == ERR_NULL
+    assert lib.bias_add_relu(0, FAKE, None, FAKE, 2, 0, 4, 1, None) == ERR_ARG
+    assert lib.max_pool2d_fwd(0, FAKE, FAKE, None, 1, 1, 4, 4, 2, 2, 2, 0, None) == ERR_NULL
+    assert lib.max_pool2d_fwd(0, FAKE, FAKE, FAKE, 1, 1, 4, 4, 2, 2, 2, 2, None) == ERR_ARG
+    assert lib.max_pool2d_bwd(1, FAKE, FAKE, FAKE, 1, 1, 4, 4, 2, 2, 0, 0, None) == ERR_ARG
+    assert lib.affine_fwd(0, FAKE, FAKE, None, FAKE, 0, 3, 4, 0, None) == ERR_ARG
+    assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, None, None, None, 2, 3, 4, None) == ERR_NULL
+    assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None) == ERR_NULL
+    assert lib.sgd_momentum_update(0, FAKE, FAKE, FAKE, 0.1, 0.9, 0, None) == ERR_ARG
+    assert lib.count_nonzero(3, FAKE, 10, FAKE, None) == ERR_DTYPE
+
+
+def test_zero_skip_mode(lib):
+    prev = lib.dmlnn_set_zero_skip(1)
+    try:
+        assert lib.dmlnn_set_zero_skip(0) == 1
+        assert lib.dmlnn_set_zero_skip(7) == -1
+    finally:
+        lib.dmlnn_set_zero_skip(prev)
+
+
+def test_no_device_is_reported_not_crashed(lib):
+    # Without a GPU a valid call must return DMLNN_ERR_DEVICE rather than abort.
+    import torch
+    if torch.cuda.device_count() > 0:
+        pytest.skip("a GPU is present")
+    assert _conv_fwd(lib) == ERR_DEVICE
+    assert dmlnn.last_error() != ""
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    X = torch.zeros(2, 64, dtype=torch.float64)
+    W = torch.zeros(2, 9, dtype=torch.float64)
+    with pytest.raises(ValueError):
+        dmlnn.conv2d_forward(X, W, None, 1, 8, 8, 3, 3, 1, 1)
+    with pytest.raises(TypeError):
+        dmlnn.conv2d_forward(X.half(), W.half(), None, 1, 8, 8, 3, 3, 1, 1)

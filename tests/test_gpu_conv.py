@@ -1,0 +1,205 @@
+"""GPU parity of the conv2d passes (through the C ABI) against the oracle.
+
+Element-by-element on small shapes that span several tiles, ragged tails,
+strides 1-3, pads 0-3 (including pad >= filter size), non-square filters, more
+than 64 filters and channel counts that leave a ragged channel chunk; the
+LeNet/ResNet-shaped workloads at full size where the oracle finishes in
+seconds; and the 256-image ResNet-shaped workload at full size on sampled
+outputs that the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import TOL, assert_close, dev, host, rounded
+from paper_1802_04647_amd import dmlnn
+from paper_1802_04647_amd.inputs import SHAPES, ConvShape, conv_layer_inputs, random_conv_case
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    ConvShape(2, 3, 7, 6, 5, 3, 3, 1, 1),
+    ConvShape(2, 5, 9, 9, 70, 3, 3, 1, 1),      # two filter tiles
+    ConvShape(1, 9, 13, 11, 8, 5, 5, 2, 2),     # stride 2
+    ConvShape(2, 37, 10, 10, 16, 3, 3, 1, 0),   # ragged channel chunk
+    ConvShape(1, 2, 8, 5, 3, 3, 1, 3, 1),       # non-square filter, stride 3
+    ConvShape(2, 4, 6, 6, 3, 1, 1, 1, 0),       # 1x1
+    ConvShape(1, 3, 5, 6, 2, 3, 3, 1, 3),       # pad >= filter size
+    ConvShape(3, 2, 1, 1, 4, 3, 3, 1, 1),       # 1x1 image
+    ConvShape(2, 2, 9, 7, 3, 2, 3, 2, 0),       # uncovered border cells
+    ConvShape(1, 6, 30, 30, 33, 3, 3, 1, 1),    # many pixel tiles per image
+]
+
+
+def _args(s):
+    return (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+
+
+def _run_all(s, X, W, b, dout, mask, dt, relu=True):
+    """GPU fwd, bwd_filter, bwd_data on identical inputs; returns host arrays."""
+    a = _args(s)
+    print(f"\n[gpu] conv {s} {dt} relu={relu}", flush=True)
+    out, Ho, Wo = dmlnn.conv2d_forward(dev(X, dt), dev(W, dt), dev(b, dt), *a, relu=relu)
+    dW, db = dmlnn.conv2d_backward_filter(dev(X, dt), dev(dout, dt), dev(mask, dt), *a, s.F)
+    dX = dmlnn.conv2d_backward_data(dev(W, dt), dev(dout, dt), dev(mask, dt), *a)
+    torch.cuda.synchronize()
+    return host(out), host(dW), host(db), host(dX), (Ho, Wo)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("s", CASES, ids=str)
+def test_conv_parity_small(s, dt):
+    X0, W0, b0, dout0 = random_conv_case(100, s, zero_frac=0.3)
+    X, W, b, dout = (rounded(v, dt) for v in (X0, W0, b0, dout0))
+    a = _args(s)
+    for relu in (True, False):
+        ref_out, Ho, Wo = oracle.conv2d_forward(X, W, b, *a, relu=relu)
+        # the backward mask source is the oracle's forward output in the mode's type
+        mask = rounded(ref_out, dt) if relu else None
+        out, dW, db, dX, hw = _run_all(s, X, W, b, dout, mask, dt, relu=relu)
+        assert hw == (Ho, Wo)
+        ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, mask, *a, s.F)
+        ref_dX = oracle.conv2d_backward_data(W, dout, mask, *a)
+        assert_close(out, ref_out, dt, "forward")
+        assert_close(dW, ref_dW, dt, "dW")
+        assert_close(db, ref_db, dt, "db")
+        assert_close(dX, ref_dX, dt, "dX")
+        if relu:
+            assert (out >= 0).all()
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("name", ["conv_small", "lenet_conv1", "lenet_conv2"])
+def test_conv_parity_workloads(name, dt):
+    s = SHAPES[name]
+    X0, W0, b0, dout0 = conv_layer_inputs(name)
+    X, W, b = (rounded(v, dt) for v in (X0, W0, b0))
+    a = _args(s)
+    ref_out, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
+    mask = rounded(ref_out, dt)
+    if name == "lenet_conv2":
+        # the conv's upstream gradient comes through the 2x2/2 max-pool backward
+        _, idx, _, _ = oracle.max_pool2d_fwd(mask, s.F, s.Hout, s.Wout, 2, 2, 2, 0)
+        dout = rounded(oracle.max_pool2d_bwd(rounded(dout0, dt), idx, s.F, s.Hout, s.Wout,
+                                             2, 2, 2, 0), dt)
+        assert np.mean(dout == 0) >= 0.75
+    else:
+        dout = rounded(dout0, dt)
+    out, dW, db, dX, _ = _run_all(s, X, W, b, dout, mask, dt)
+    ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, mask, *a, s.F)
+    ref_dX = oracle.conv2d_backward_data(W, dout, mask, *a)
+    assert_close(out, ref_out, dt, "forward")
+    assert_close(dW, ref_dW, dt, "dW")
+    assert_close(db, ref_db, dt, "db")
+    assert_close(dX, ref_dX, dt, "dX")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_conv_parity_resnet_two_images_elementwise(dt):
+    # ResNet-shaped layer (64 -> 64, 56x56, 3x3 p1) on 2 images: every element.
+    s = ConvShape(2, 64, 56, 56, 64, 3, 3, 1, 1)
+    X0, W0, b0, dout0 = conv_layer_inputs("resnet_conv", N=2)
+    X, W, b, dout = (rounded(v, dt) for v in (X0, W0, b0, dout0))
+    a = _args(s)
+    ref_out, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
+    mask = rounded(ref_out, dt)
+    out, dW, db, dX, _ = _run_all(s, X, W, b, dout, mask, dt)
+    assert_close(out, ref_out, dt, "forward")
+    ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, mask, *a, s.F)
+    assert_close(dW, ref_dW, dt, "dW")
+    assert_close(db, ref_db, dt, "db")
+    assert_close(dX, oracle.conv2d_backward_data(W, dout, mask, *a), dt, "dX")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_conv_parity_resnet_full_batch_sampled(dt):
+    """All 256 images, in the launch configuration the benchmark times; the
+    oracle computes sampled output elements one by one.  The relu mask source is
+    an independent relu(N(0,1)) draw of the output's shape (any array works as a
+    mask source; both sides read the same bytes)."""
+    s = SHAPES["resnet_conv"]
+    X0, W0, b0, dout0 = conv_layer_inputs("resnet_conv")
+    g = np.random.Generator(np.random.PCG64(7))
+    mask0 = np.maximum(g.standard_normal(dout0.shape), 0.0)
+    X, W, b, dout, mask = (rounded(v, dt) for v in (X0, W0, b0, dout0, mask0))
+    a = _args(s)
+    out, dW, db, dX, (Ho, Wo) = _run_all(s, X, W, b, dout, mask, dt)
+    Q = Ho * Wo
+    tol = TOL[dt]
+    # forward: 400 sampled outputs, normwise against the sampled oracle values
+    idx = g.integers(0, [s.N, s.F, Ho, Wo], size=(400, 4))
+    ref = np.array([max(oracle.conv2d_forward_pre_elem(X, W, b, *a, *e), 0.0) for e in idx])
+    got = out.reshape(s.N, s.F, Q)[idx[:, 0], idx[:, 1], idx[:, 2] * Wo + idx[:, 3]]
+    assert np.max(np.abs(got - ref)) <= tol * np.max(np.abs(ref))
+    # filter gradient: 48 sampled entries (each a sum over 802,816 terms), all of db
+    sel = g.integers(0, [s.F, s.C, s.Hf, s.Wf], size=(48, 4))
+    refw = np.array([oracle.conv2d_backward_filter_elem(X, dout, mask, s.N, s.C, s.Hin, s.Win,
+                                                        s.F, s.Hf, s.Wf, s.stride, s.pad, *e)
+                     for e in sel])
+    gotw = dW.reshape(s.F, s.C, s.Hf, s.Wf)[sel[:, 0], sel[:, 1], sel[:, 2], sel[:, 3]]
+    assert np.max(np.abs(gotw - refw)) <= tol * np.max(np.abs(refw))
+    refb = np.array([oracle.conv2d_backward_bias_elem(dout, mask, s.N, s.F, Ho, Wo, f)
+                     for f in range(s.F)])
+    assert_close(db, refb, dt, "db")
+    # input gradient: 400 sampled cells
+    idx = g.integers(0, [s.N, s.C, s.Hin, s.Win], size=(400, 4))
+    refx = np.array([oracle.conv2d_backward_data_elem(W, dout, mask, s.C, s.Hin, s.Win, s.F,
+                                                      s.Hf, s.Wf, s.stride, s.pad, *e)
+                     for e in idx])
+    gotx = dX.reshape(s.N, s.C, s.Hin, s.Win)[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
+    assert np.max(np.abs(gotx - refx)) <= tol * np.max(np.abs(refx))
+    # properties at full size
+    assert np.isfinite(out).all() and (out >= 0).all()
+    assert np.isfinite(dX).all() and np.isfinite(dW).all()
+
+
+def test_zero_skip_matches_dense_bitwise():
+    s = SHAPES["lenet_conv1"]
+    X0, W0, b0, dout0 = conv_layer_inputs("lenet_conv1")
+    # structured zeros: blank out whole rows so entire MFMA fragments are zero
+    X0 = X0.reshape(s.N, 28, 28).copy()
+    X0[:, :10, :] = 0.0
+    X0 = X0.reshape(s.N, -1)
+    a = _args(s)
+    res = []
+    prev = dmlnn.set_zero_skip(0)
+    try:
+        for mode in (0, 1):
+            dmlnn.set_zero_skip(mode)
+            out, _, _ = dmlnn.conv2d_forward(dev(X0, "f64"), dev(W0, "f64"), dev(b0, "f64"), *a)
+            dW, db = dmlnn.conv2d_backward_filter(dev(X0, "f64"), dev(dout0, "f64"), out, *a, s.F)
+            dX = dmlnn.conv2d_backward_data(dev(W0, "f64"), dev(dout0, "f64"), out, *a)
+            torch.cuda.synchronize()
+            res.append([t + 0.0 for t in (out, dW, db, dX)])   # +0.0 folds -0 into +0
+    finally:
+        dmlnn.set_zero_skip(prev)
+    for u, v in zip(*res):
+        assert torch.equal(u, v)
+
+
+def test_backward_filter_is_deterministic():
+    s = SHAPES["lenet_conv2"]
+    X0, W0, b0, dout0 = conv_layer_inputs("lenet_conv2")
+    a = _args(s)
+    X = dev(X0, "f32")
+    out, _, _ = dmlnn.conv2d_forward(X, dev(W0, "f32"), dev(b0, "f32"), *a)
+    g = torch.randn(out.shape, generator=torch.Generator().manual_seed(3)).to("cuda", torch.float32)
+    r1 = dmlnn.conv2d_backward_filter(X, g, out, *a, s.F)
+    r2 = dmlnn.conv2d_backward_filter(X, g, out, *a, s.F)
+    torch.cuda.synchronize()
+    assert torch.equal(r1[0], r2[0]) and torch.equal(r1[1], r2[1])
+
+
+def test_identity_filter_is_exact():
+    # 3x3 centre-tap identity with p=1: out = relu(X + b) bit-exactly (one non-zero product).
+    C = 8
+    X = np.random.Generator(np.random.PCG64(11)).standard_normal((3, C * 100))
+    W = np.zeros((C, C * 9))
+    for c in range(C):
+        W[c, c * 9 + 4] = 1.0
+    b = np.linspace(-0.5, 0.5, C)
+    out, _, _ = dmlnn.conv2d_forward(dev(X, "f64"), dev(W, "f64"), dev(b, "f64"), C, 10, 10, 3, 3,
+                                     1, 1)
+    exp = np.maximum(X.reshape(3, C, 100) + b[None, :, None], 0.0).reshape(3, -1)
+    assert np.array_equal(host(out), exp)

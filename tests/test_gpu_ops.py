@@ -1,0 +1,133 @@
+"""GPU parity of the ops around the conv layer (through the C ABI) against the
+oracle: max-pool (argmax bit-exact), bias_add_relu, affine, softmax +
+cross-entropy, SGD-momentum and count_nonzero, in fp64 and fp32."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_close, dev, host, rounded
+from paper_1802_04647_amd import dmlnn
+from paper_1802_04647_amd.inputs import rng
+
+pytestmark = pytest.mark.gpu
+
+POOLS = [  # (N, C, H, W, Hf, Wf, s, p)
+    (64, 64, 14, 14, 2, 2, 2, 0),     # LeNet pool2
+    (64, 32, 28, 28, 2, 2, 2, 0),     # LeNet pool1
+    (2, 3, 7, 9, 3, 3, 2, 1),
+    (2, 2, 6, 5, 2, 3, 1, 1),         # overlapping windows
+    (1, 2, 9, 9, 3, 2, 3, 0),
+]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("cfg", POOLS, ids=str)
+def test_max_pool_parity(cfg, dt):
+    N, C, H, W, Hf, Wf, s, p = cfg
+    print(f"\n[gpu] pool {cfg} {dt}", flush=True)
+    g = rng(40)
+    # relu-like input with many exact-zero ties, plus quantised values
+    X = rounded(np.maximum(np.round(g.standard_normal((N, C * H * W)) * 4) / 4, 0.0), dt)
+    ref_out, ref_idx, Ho, Wo = oracle.max_pool2d_fwd(X, C, H, W, Hf, Wf, s, p)
+    out, idx, Ho2, Wo2 = dmlnn.max_pool2d_fwd(dev(X, dt), C, H, W, Hf, Wf, s, p)
+    dout = rounded(g.standard_normal(ref_out.shape), dt)
+    dX = dmlnn.max_pool2d_bwd(dev(dout, dt), idx, C, H, W, Hf, Wf, s, p)
+    torch.cuda.synchronize()
+    assert (Ho, Wo) == (Ho2, Wo2)
+    assert np.array_equal(idx.cpu().numpy(), ref_idx)            # bit-exact argmax
+    assert np.array_equal(host(out), ref_out)                     # a max is exact
+    ref_dX = oracle.max_pool2d_bwd(dout, ref_idx, C, H, W, Hf, Wf, s, p)
+    assert_close(host(dX), ref_dX, dt, "pool dX")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_bias_add_relu_parity(dt):
+    g = rng(41)
+    N, C, HW = 5, 7, 33
+    X = rounded(g.standard_normal((N, C * HW)), dt)
+    b = rounded(g.standard_normal(C), dt)
+    for relu in (True, False):
+        for bias in (b, None):
+            ref = oracle.bias_add_relu(X, bias, C, HW, relu=relu)
+            got = dmlnn.bias_add_relu(dev(X, dt), dev(bias, dt), C, HW, relu=relu)
+            assert_close(host(got), ref, dt, "bias_add_relu")
+    Xd = dev(X, dt)                                                # in place
+    dmlnn.bias_add_relu(Xd, dev(b, dt), C, HW, relu=True, out=Xd)
+    assert_close(host(Xd), oracle.bias_add_relu(X, b, C, HW, relu=True), dt, "in place")
+
+
+AFFINE = [(64, 3136, 512), (64, 512, 10), (5, 7, 3), (33, 70, 65), (1, 1, 1)]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("shape", AFFINE, ids=str)
+def test_affine_parity(shape, dt):
+    N, D, M = shape
+    print(f"\n[gpu] affine {shape} {dt}", flush=True)
+    g = rng(42)
+    X = rounded(np.maximum(g.standard_normal((N, D)), 0.0), dt)
+    W = rounded(g.standard_normal((D, M)) * np.sqrt(2.0 / D), dt)
+    b = rounded(g.standard_normal(M) * 0.1, dt)
+    dout = rounded(g.standard_normal((N, M)), dt)
+    for relu in (True, False):
+        ref_out = oracle.affine_fwd(X, W, b, relu=relu)
+        out = dmlnn.affine_fwd(dev(X, dt), dev(W, dt), dev(b, dt), relu=relu)
+        assert_close(host(out), ref_out, dt, "affine out")
+        mask = rounded(ref_out, dt) if relu else None
+        rdX, rdW, rdb = oracle.affine_bwd(dout, X, W, mask)
+        dX, dW, db = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), dev(mask, dt))
+        assert_close(host(dX), rdX, dt, "affine dX")
+        assert_close(host(dW), rdW, dt, "affine dW")
+        assert_close(host(db), rdb, dt, "affine db")
+    _, dW2, _ = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), None, want_dX=False,
+                                 want_db=False)
+    assert_close(host(dW2), oracle.affine_bwd(dout, X, W, None)[1], dt, "affine dW only")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("NK", [(64, 10), (7, 3), (5, 130), (1, 1)], ids=str)
+def test_softmax_xent_parity(NK, dt):
+    N, K = NK
+    g = rng(43)
+    S = rounded(g.standard_normal((N, K)) * 3, dt)
+    Y = np.eye(K)[g.integers(0, K, N)]
+    rl, rdS, rP = oracle.softmax_xent(S, Y)
+    loss, dS, P = dmlnn.softmax_xent(dev(S, dt), dev(Y, dt))
+    torch.cuda.synchronize()
+    assert abs(host(loss)[0] - rl) <= {"f64": 1e-10, "f32": 1e-4}[dt] * max(abs(rl), 1e-300)
+    assert_close(host(dS), rdS, dt, "dscores")
+    assert_close(host(P), rP, dt, "probs")
+
+
+def test_softmax_uniform_scores_closed_form():
+    K = 10
+    loss, dS, P = dmlnn.softmax_xent(dev(np.zeros((3, K)), "f64"), dev(np.eye(K)[[1, 4, 9]], "f64"))
+    assert abs(host(loss)[0] - np.log(10.0)) < 1e-14
+    assert np.allclose(host(P), 0.1, rtol=0, atol=1e-16)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_sgd_momentum_parity(dt):
+    g = rng(44)
+    n = 1663370
+    th = rounded(g.standard_normal(n), dt)
+    v = np.zeros(n)
+    tth, tv = dev(th, dt), dev(v, dt)
+    for step in range(3):
+        gr = rounded(g.standard_normal(n), dt)
+        th, v = oracle.sgd_momentum_update(th, gr, v, 0.01, 0.9)
+        dmlnn.sgd_momentum_update(tth, dev(gr, dt), tv, 0.01, 0.9)
+        th, v = rounded(th, dt), rounded(v, dt)     # the GPU keeps state in the mode's type
+    assert_close(host(tth), th, dt, "theta")
+    assert_close(host(tv), v, dt, "velocity")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_count_nonzero_exact(dt):
+    g = rng(45)
+    for n in (1, 63, 64, 65, 1000003):
+        X = rounded(np.where(g.random(n) < 0.2, g.random(n), 0.0), dt)
+        X[:: max(1, n // 7)] = -0.0
+        got = dmlnn.count_nonzero(dev(X, dt))
+        assert int(got.item()) == oracle.count_nonzero(X)

@@ -136,6 +136,25 @@ def lenet_timing(steps=50, warmup=10):
     return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3))
 
 
+def copy_calibration(nbytes=1 << 30, reps=5):
+    """A plain device-to-device copy of known size: the achievable HBM rate, and the
+    reference kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the byte
+    counts of the conv kernels."""
+    import torch
+    x = torch.ones(nbytes // 8, dtype=torch.float64, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"bytes_moved": 2 * nbytes, "ms": round(ms, 4), "gbps": round(2 * nbytes / ms / 1e6, 1)}
+
+
 def cpu_baseline(target_s=12.0):
     """The oracle (plain nested loops, OpenMP over independent outputs) on a bounded
     sample of the same layer: the three passes over n images."""
@@ -220,6 +239,7 @@ def main():
                      "frac": round(achieved / PEAK_F64_MFMA, 4),
                      "traffic": measured_traffic(dom)},
     }
+    rec["hbm_copy"] = copy_calibration()
     if not args.only_f64:
         r32 = conv_step_timing("f32", args.steps, args.warmup)
         ms32 = r32["wall_s"] * 1e3 / args.steps

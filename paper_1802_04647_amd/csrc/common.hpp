@@ -43,7 +43,31 @@ struct Mfma<float> {
 };
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
-__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// Wave index, made visibly wave-uniform so index math on it stays scalar.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// The value of x, hidden from the optimiser: index math derived from it inside
+// a loop is recomputed per iteration instead of being hoisted into registers
+// that stay live across the loop (which would spill next to the accumulators).
+__device__ __forceinline__ int opaque(int x)
+{
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+// floor(n / d) for 0 <= n < 2^16 and 1 <= d < 2^16, with magic = ceil(2^32 / d)
+// computed on the host as a 64-bit value (2^32 itself for d = 1).  n * magic / 2^32
+// exceeds n / d by less than n / 2^32, which is below 1/d when n * d < 2^32, so
+// the floor is exact.
+__device__ __forceinline__ int div_magic(int n, unsigned long long magic)
+{
+    return (int)(((unsigned long long)(unsigned)n * magic) >> 32);
+}
+
+inline unsigned long long host_magic(int d)
+{
+    return (0x100000000ull + (unsigned long long)d - 1ull) / (unsigned long long)d;
+}
 
 // Wave-uniform "is every lane's value zero" test (wavefront ballot).
 template <typename T>

@@ -31,6 +31,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBM = 64;
 constexpr size_t kLdsBudget = 72 * 1024;  // two blocks per CU
+constexpr int kMS = 8;    // source-row slots each wave stages per chunk
+constexpr int kMA = 13;   // filter elements each thread stages per chunk
 
 struct IgemmArgs {
     const void *src;   // [N][Cs][Sh][Sw]
@@ -46,6 +48,8 @@ struct IgemmArgs {
     int tiles_per_img;
     int KC, KCK;
     int Wpad, CH, SA;
+    int pipelined;  // 1: chunk fits the per-thread staging registers
+    unsigned long long magic_kck, magic_hw;
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP>
@@ -67,13 +71,15 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
     const int qy0 = q0 / a.Qw;
     const int rows_need = ((qend - 1) / a.Qw - qy0) * a.S + a.Hf;
     const int ybase = qy0 * a.S - a.Ph;
+    const int CHn = rows_need * a.Wpad;  // channel stride of this tile's staged window
+    const int KCv = a.KC * a.HfWf;       // real (unpadded) k per chunk
 
     for (int kk = tid; kk < a.KCK; kk += kThreads) {
         int off = 0;
-        if (kk < a.KC * a.HfWf) {
+        if (kk < KCv) {
             int c = kk / a.HfWf, t = kk - c * a.HfWf;
             int i = t / a.Wf, j = t - i * a.Wf;
-            off = c * a.CH + i * a.Wpad + j;
+            off = c * CHn + i * a.Wpad + j;
         }
         s_koff[kk] = off;
     }
@@ -97,46 +103,125 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
     const T *msk = (BWD && a.mask) ? reinterpret_cast<const T *>(a.mask) + img : nullptr;
     const T *wgt = reinterpret_cast<const T *>(a.wgt);
 
-    for (int c0 = 0; c0 < a.Cs; c0 += a.KC) {
-        __syncthreads();
-        // (a) source rows, one LDS row per (channel, staged row); lanes walk columns.
-        const int nrows = a.KC * rows_need;
+    // Staging is software-pipelined: the global loads of chunk c0+KC are issued
+    // into registers before the MFMA loop of chunk c0 and written to LDS after
+    // it.  Source rows: wave w owns row slots w, w+4, ... of the chunk's
+    // KC*rows_need staged rows (times 64-wide column groups).  Filter slice:
+    // thread t owns elements t, t+256, ... of the 64 x KCK slice.
+    const int nrows = a.KC * rows_need;
+    const int ncg = (a.Wpad + kWave - 1) / kWave;
+    const int tot_a = kBM * a.KCK;
+    T vs[kMS], vm[kMS], va[kMA];
+
+    auto load = [&](int c0) {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kMS; ++it) {
+            const int slot = wave + 4 * it;
+            const int r = slot / ncg, cgi = slot - r * ncg;
+            T v = T(0), mv = T(1);
+            if (r < nrows) {
+                const int c = r / rows_need, t = r - c * rows_need;
+                const int cg = c0 + c, yv = ybase + t;
+                const int ys = yv / a.up;
+                const int u = lane + kWave * cgi;
+                const int xv = u - a.Pw;
+                const int xs = xv / a.up;
+                if (cg < a.Cs && yv >= 0 && ys * a.up == yv && ys < a.Sh && u < a.Wpad &&
+                    xv >= 0 && xs * a.up == xv && xs < a.Sw) {
+                    const size_t o = ((size_t)cg * a.Sh + ys) * a.Sw + xs;
+                    v = src[o];
+                    if (BWD && msk) mv = msk[o];
+                }
+            }
+            vs[it] = v;
+            vm[it] = mv;
+        }
+#pragma unroll
+        for (int it = 0; it < kMA; ++it) {
+            const int e = tid + kThreads * it;
+            T v = T(0);
+            if (e < tot_a) {
+                const int m = div_magic(e, a.magic_kck);
+                const int kk = e - m * a.KCK;
+                const int c = div_magic(kk, a.magic_hw);
+                const int t = kk - c * a.HfWf;
+                const int mg = m0 + m;
+                if (mg < a.M && kk < KCv && c0 + c < a.Cs) {
+                    if (!BWD)
+                        v = wgt[((size_t)mg * a.Cs + c0) * a.HfWf + kk];
+                    else
+                        v = wgt[((size_t)(c0 + c) * a.M + mg) * a.HfWf + (a.HfWf - 1 - t)];
+                }
+            }
+            va[it] = v;
+        }
+    };
+
+    auto store = [&]() {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kMS; ++it) {
+            const int slot = wave + 4 * it;
+            const int r = slot / ncg, cgi = slot - r * ncg;
+            const int u = lane + kWave * cgi;
+            if (r < nrows && u < a.Wpad) {
+                T v = vs[it];
+                if (BWD && !(vm[it] > T(0))) v = T(0);
+                s_src[r * a.Wpad + u] = v;  // row r = (channel, staged row), dense
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < kMA; ++it) {
+            const int e = tid + kThreads * it;
+            if (e < tot_a) s_a[e + div_magic(e, a.magic_kck)] = va[it];  // row stride KCK + 1
+        }
+    };
+
+    // Fallback for chunks larger than the staging registers: load and store
+    // directly (one memory round trip per row slot; correct for any size).
+    auto stage_direct = [&](int c0) {
         for (int r = wave; r < nrows; r += kThreads / kWave) {
-            int c = r / rows_need, t = r - c * rows_need;
-            int cg = c0 + c, yv = ybase + t;
-            int ys = yv / a.up;
-            bool rowok = cg < a.Cs && yv >= 0 && ys * a.up == yv && ys < a.Sh;
-            size_t roff = ((size_t)cg * a.Sh + (rowok ? ys : 0)) * a.Sw;
-            T *dst = s_src + c * a.CH + t * a.Wpad;
+            const int c = r / rows_need, t = r - c * rows_need;
+            const int cg = c0 + c, yv = ybase + t;
+            const int ys = yv / a.up;
+            const bool rowok = cg < a.Cs && yv >= 0 && ys * a.up == yv && ys < a.Sh;
+            const size_t roff = ((size_t)cg * a.Sh + (rowok ? ys : 0)) * a.Sw;
             for (int u = lane; u < a.Wpad; u += kWave) {
                 T v = T(0);
-                int xv = u - a.Pw;
-                int xs = xv / a.up;
+                const int xv = u - a.Pw;
+                const int xs = xv / a.up;
                 if (rowok && xv >= 0 && xs * a.up == xv && xs < a.Sw) {
                     v = src[roff + xs];
                     if (BWD && msk && !(msk[roff + xs] > T(0))) v = T(0);
                 }
-                dst[u] = v;
+                s_src[r * a.Wpad + u] = v;
             }
         }
-        // (b) the 64 x KCK slice of A (zero outside M, outside Cs and in the k padding).
-        for (int r = wave; r < kBM; r += kThreads / kWave) {
-            int m = m0 + r;
-            T *dst = s_a + r * a.SA;
-            for (int kk = lane; kk < a.KCK; kk += kWave) {
-                T v = T(0);
-                int c = kk / a.HfWf;
-                if (m < a.M && kk < a.KC * a.HfWf && c0 + c < a.Cs) {
-                    int t = kk - c * a.HfWf;
-                    if (!BWD)
-                        v = wgt[((size_t)m * a.Cs + (c0 + c)) * a.HfWf + t];
-                    else
-                        v = wgt[((size_t)(c0 + c) * a.M + m) * a.HfWf + (a.HfWf - 1 - t)];
-                }
-                dst[kk] = v;
+        for (int e = tid; e < tot_a; e += kThreads) {
+            const int m = e / a.KCK, kk = e - m * a.KCK;
+            const int c = kk / a.HfWf, t = kk - c * a.HfWf;
+            const int mg = m0 + m;
+            T v = T(0);
+            if (mg < a.M && kk < KCv && c0 + c < a.Cs) {
+                if (!BWD)
+                    v = wgt[((size_t)mg * a.Cs + c0) * a.HfWf + kk];
+                else
+                    v = wgt[((size_t)(c0 + c) * a.M + mg) * a.HfWf + (a.HfWf - 1 - t)];
             }
+            s_a[m * a.SA + kk] = v;
         }
+    };
+
+    if (a.pipelined) load(0);
+    for (int c0 = 0; c0 < a.Cs; c0 += a.KC) {
         __syncthreads();
+        if (a.pipelined)
+            store();
+        else
+            stage_direct(c0);
+        __syncthreads();
+        if (a.pipelined && c0 + a.KC < a.Cs) load(c0 + a.KC);
 
         const T *arow0 = s_a + (wm * 32 + (lane & 15)) * a.SA + (lane >> 4);
         const T *arow1 = arow0 + 16 * a.SA;
@@ -178,7 +263,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 // Host-side tile selection ----------------------------------------------------
 
 struct Plan {
-    int NB, KC, KCK, Wpad, CH, SA, tiles_per_img, m_tiles;
+    int NB, KC, KCK, Wpad, CH, SA, tiles_per_img, m_tiles, pipelined;
     size_t lds;
 };
 
@@ -190,11 +275,14 @@ size_t lds_bytes(size_t tsz, int KC, int CH, int SA, int KCK)
 bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, int nimg,
                Plan &p)
 {
-    static const int kNB[] = {7, 4, 2, 1};
+    static const int kNB64[] = {7, 4, 2, 1}, kNB32[] = {7, 4, 2, 1};
     const int HfWf = Hf * Wf;
     p.m_tiles = (M + kBM - 1) / kBM;
     double best = -1.0;
-    for (int NB : kNB) {
+    const int *cand = tsz == 8 ? kNB64 : kNB32;
+    const int ncand = 4;
+    for (int ci = 0; ci < ncand; ++ci) {
+        const int NB = cand[ci];
         int BN = 32 * NB;
         int tiles = (Q + BN - 1) / BN;
         double fill = (double)Q / ((double)tiles * BN);
@@ -211,16 +299,26 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
     const int rows_max = ((Qw + BN - 2) / Qw) * S + Hf;
     p.Wpad = (Qw - 1) * S + Wf;
     p.CH = rows_max * p.Wpad;
-    // Largest channel chunk (a multiple of 4 when more than 4 channels) that fits.
+    // Largest channel chunk whose staging fits the per-thread register slots
+    // (pipelined path) and the LDS budget; otherwise the largest that fits the
+    // LDS budget alone (direct-staging path).
+    const int ncg = (p.Wpad + 63) / 64;
+    auto kck_of = [&](int kc) { return ((kc * HfWf + 3) / 4) * 4; };
+    auto fits_lds = [&](int kc) {
+        return lds_bytes(tsz, kc, p.CH, kck_of(kc) + 1, kck_of(kc)) <= kLdsBudget;
+    };
+    auto fits_regs = [&](int kc) {
+        return (kc * rows_max * ncg + 3) / 4 <= kMS && kBM * kck_of(kc) <= kThreads * kMA;
+    };
     int kc = Cs;
-    for (;;) {
-        int kck = ((kc * HfWf + 3) / 4) * 4;
-        int sa = kck + 1;
-        if (lds_bytes(tsz, kc, p.CH, sa, kck) <= kLdsBudget || kc == 1) break;
-        kc = kc > 4 ? ((kc - 1) / 4) * 4 : kc - 1;
+    while (kc > 1 && !(fits_regs(kc) && fits_lds(kc))) --kc;
+    p.pipelined = fits_regs(kc) && fits_lds(kc);
+    if (!p.pipelined) {
+        kc = Cs;
+        while (kc > 1 && !fits_lds(kc)) --kc;
     }
     p.KC = kc;
-    p.KCK = ((kc * HfWf + 3) / 4) * 4;
+    p.KCK = kck_of(kc);
     p.SA = p.KCK + 1;
     p.lds = lds_bytes(tsz, p.KC, p.CH, p.SA, p.KCK);
     return p.lds <= 160 * 1024;
@@ -260,6 +358,9 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.Wpad = p.Wpad;
     a.CH = p.CH;
     a.SA = p.SA;
+    a.pipelined = p.pipelined;
+    a.magic_kck = host_magic(p.KCK);
+    a.magic_hw = host_magic(a.HfWf);
     switch (p.NB) {
     case 7: return launch_nb<T, 7, BWD>(a, p, nimg, zero_skip, s);
     case 4: return launch_nb<T, 4, BWD>(a, p, nimg, zero_skip, s);

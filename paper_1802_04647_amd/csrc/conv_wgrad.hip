@@ -27,6 +27,8 @@ constexpr int kThreads = 256;
 constexpr int kBM = 64;
 constexpr size_t kLdsBudget = 72 * 1024;
 constexpr int kTargetBlocks = 512;
+constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
+constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
 
 struct WgradArgs {
     const void *X, *dout, *mask;
@@ -34,6 +36,9 @@ struct WgradArgs {
     int N, C, Hin, Win, F, Hf, Wf, HfWf, S, P, Hout, Wout, Q, K;
     int KR, nkr, nft, RQ, tiles_per_img, T_total, splits;
     int Wpad, CH, SG;
+    int pipelined;  // 1: a pixel tile fits the per-thread staging registers
+    int rows_max;
+    unsigned long long magic_rq, magic_wpad, magic_ch;
 };
 
 template <typename T, int NBW>
@@ -58,13 +63,14 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     const int c_lo = kbeg / a.HfWf;
     const int nch = (kend - 1) / a.HfWf - c_lo + 1;
 
-    int koff[NBW];
+    // LDS offset of column k (channel relative to c_lo, tap i, j) of this lane's blocks.
+    int kof[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         int k = kbeg + (wave * NBW + nb) * 16 + (lane & 15);
         int c = k / a.HfWf, t = k - c * a.HfWf;
         int i = t / a.Wf, j = t - i * a.Wf;
-        koff[nb] = (k < kend) ? (c - c_lo) * a.CH + i * a.Wpad + j : 0;
+        kof[nb] = (k < kend) ? (c - c_lo) * a.CH + i * a.Wpad + j : 0;
     }
 
     typename MF::acc_t acc[4][NBW];
@@ -80,47 +86,126 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     const long long t_begin = (long long)split * a.T_total / a.splits;
     const long long t_end = (long long)(split + 1) * a.T_total / a.splits;
 
-    for (long long tt = t_begin; tt < t_end; ++tt) {
-        const int n = (int)(tt / a.tiles_per_img);
-        const int qt = (int)(tt - (long long)n * a.tiles_per_img);
-        const int q0 = qt * a.RQ;
-        const int qend = min(q0 + a.RQ, a.Q);
-        const int qy0 = q0 / a.Wout;
-        const int rows_need = ((qend - 1) / a.Wout - qy0) * a.S + a.Hf;
-        const int ybase = qy0 * a.S - a.P;
+    // Pixel tile tt covers pixels [q0, qend) of image n; its X window is the
+    // rows_need input rows of channels c_lo .. c_lo+nch-1 that the windows touch.
+    struct TileGeo {
+        int n, q0, qend, qy0, rows_need, ybase;
+    };
+    auto geo = [&](long long tt) {
+        TileGeo g;
+        g.n = (int)(tt / a.tiles_per_img);
+        const int qt = (int)(tt - (long long)g.n * a.tiles_per_img);
+        g.q0 = qt * a.RQ;
+        g.qend = min(g.q0 + a.RQ, a.Q);
+        g.qy0 = g.q0 / a.Wout;
+        g.rows_need = ((g.qend - 1) / a.Wout - g.qy0) * a.S + a.Hf;
+        g.ybase = g.qy0 * a.S - a.P;
+        return g;
+    };
 
-        __syncthreads();
+    // Software pipeline: the global loads of tile tt+1 are issued into
+    // registers before the MFMA loop of tile tt and written to LDS after it.
+    const int tot_g = kBM * a.RQ;
+    const int tot_x = nch * a.CH;  // channels x rows_max x Wpad (rows past rows_need are 0)
+    T vg[kMG], vm[kMG], vx[kMX];
+    auto load = [&](const TileGeo &g) {
+        const int tid = opaque(threadIdx.x);
+        const size_t gbase = ((size_t)g.n * a.F + ft * kBM) * a.Q;
+#pragma unroll
+        for (int it = 0; it < kMG; ++it) {
+            const int e = tid + kThreads * it;
+            T v = T(0), mv = T(1);
+            if (e < tot_g) {
+                const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
+                const int q = g.q0 + u;
+                if (ft * kBM + r < a.F && q < g.qend) {
+                    const size_t o = gbase + (size_t)r * a.Q + q;
+                    v = dout[o];
+                    if (mask) mv = mask[o];
+                }
+            }
+            vg[it] = v;
+            vm[it] = mv;
+        }
+#pragma unroll
+        for (int it = 0; it < kMX; ++it) {
+            const int e = tid + kThreads * it;
+            T v = T(0);
+            if (e < tot_x) {
+                const int c = div_magic(e, a.magic_ch), rem = e - c * a.CH;
+                const int t = div_magic(rem, a.magic_wpad), u = rem - t * a.Wpad;
+                const int cg = c_lo + c, y = g.ybase + t, x = u - a.P;
+                if (t < g.rows_need && cg < a.C && y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
+                    v = X[(((size_t)g.n * a.C + cg) * a.Hin + y) * a.Win + x];
+            }
+            vx[it] = v;
+        }
+    };
+    auto store = [&](const TileGeo &g) {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kMG; ++it) {
+            const int e = tid + kThreads * it;
+            if (e < tot_g) {
+                const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
+                s_g[r * a.SG + u] = (vm[it] > T(0)) ? vg[it] : T(0);
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < kMX; ++it) {
+            const int e = tid + kThreads * it;
+            if (e < tot_x) s_x[e] = vx[it];  // (c, t, u) at c*CH + t*Wpad + u
+        }
+    };
+    // Fallback for tiles larger than the staging registers.
+    auto stage_direct = [&](const TileGeo &g) {
         for (int r = wave; r < kBM; r += kThreads / kWave) {
             int fg = ft * kBM + r;
-            size_t goff = ((size_t)n * a.F + fg) * a.Q;
+            size_t goff = ((size_t)g.n * a.F + fg) * a.Q;
             for (int u = lane; u < a.RQ; u += kWave) {
-                int q = q0 + u;
+                int q = g.q0 + u;
                 T v = T(0);
-                if (fg < a.F && q < qend) {
+                if (fg < a.F && q < g.qend) {
                     v = dout[goff + q];
                     if (mask && !(mask[goff + q] > T(0))) v = T(0);
                 }
                 s_g[r * a.SG + u] = v;
             }
         }
-        const int nrows = nch * rows_need;
+        const int nrows = nch * g.rows_need;
         for (int r = wave; r < nrows; r += kThreads / kWave) {
-            int c = r / rows_need, t = r - c * rows_need;
-            int cg = c_lo + c, y = ybase + t;
+            int c = r / g.rows_need, t = r - c * g.rows_need;
+            int cg = c_lo + c, y = g.ybase + t;
             bool rowok = cg < a.C && y >= 0 && y < a.Hin;
-            size_t xoff = (((size_t)n * a.C + cg) * a.Hin + (rowok ? y : 0)) * a.Win;
+            size_t xoff = (((size_t)g.n * a.C + cg) * a.Hin + (rowok ? y : 0)) * a.Win;
             T *dst = s_x + c * a.CH + t * a.Wpad;
             for (int u = lane; u < a.Wpad; u += kWave) {
                 int x = u - a.P;
                 dst[u] = (rowok && x >= 0 && x < a.Win) ? X[xoff + x] : T(0);
             }
         }
+    };
+
+    TileGeo cur = geo(t_begin);
+    if (a.pipelined && t_begin < t_end) load(cur);
+    for (long long tt = t_begin; tt < t_end; ++tt) {
+        __syncthreads();
+        if (a.pipelined)
+            store(cur);
+        else
+            stage_direct(cur);
         for (int u = tid; u < a.RQ; u += kThreads) {
-            int q = q0 + u;
+            int q = cur.q0 + u;
             int qy = q / a.Wout, qx = q - qy * a.Wout;
-            s_qoff[u] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+            s_qoff[u] = (q < cur.qend) ? (qy - cur.qy0) * a.S * a.Wpad + qx * a.S : 0;
         }
         __syncthreads();
+        if (a.pipelined && tt + 1 < t_end) {
+            cur = geo(tt + 1);
+            load(cur);
+        } else if (tt + 1 < t_end) {
+            cur = geo(tt + 1);
+        }
 
         if (kr == 0) {  // bias gradient: thread (f = tid/4, phase = tid%4), fixed order
             const T *gr = s_g + (tid >> 2) * a.SG;
@@ -136,7 +221,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG + qq];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) {
-                T bv = s_x[koff[nb] + qo];
+                T bv = s_x[kof[nb] + qo];
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
             }
@@ -192,7 +277,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *
 }
 
 struct WPlan {
-    int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG;
+    int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined;
     long long T_total;
     size_t lds;
 };
@@ -213,12 +298,15 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.nft = (d.F + kBM - 1) / kBM;
     p.Wpad = (d.Wout - 1) * d.stride + d.Wf;
     const int nch_alloc = (p.KR - 1) / HfWf + 2;
-    // Pixel tile: whole output rows, about 64 pixels, a multiple of 4.
-    int rq = d.Wout * (d.Wout >= 64 ? 1 : 64 / d.Wout);
+    // Pixel tile: whole output rows when a row is short (at most 56 pixels so the
+    // g tile fits the staging registers), else a 56-pixel slice; a multiple of 4.
+    int rq = d.Wout <= 56 ? d.Wout * (56 / d.Wout) : 56;
     if (rq > Q) rq = Q;
     rq = ((rq + 3) / 4) * 4;
     for (;;) {
-        int rows_max = ((d.Wout + rq - 2) / d.Wout) * d.stride + d.Hf;
+        const bool aligned = rq % d.Wout == 0;
+        int rows_max = aligned ? (rq / d.Wout - 1) * d.stride + d.Hf
+                               : ((d.Wout + rq - 2) / d.Wout) * d.stride + d.Hf;
         int CH = rows_max * p.Wpad;
         int SG = rq + 1;
         size_t lds = wlds(tsz, SG, nch_alloc, CH, rq);
@@ -226,12 +314,14 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
             p.RQ = rq;
             p.CH = CH;
             p.SG = SG;
+            p.rows_max = rows_max;
             p.lds = lds;
             break;
         }
         rq = ((rq / 2 + 3) / 4) * 4;
     }
     if (p.lds > 160 * 1024) return false;
+    p.pipelined = kBM * p.RQ <= kThreads * kMG && (long long)nch_alloc * p.CH <= kThreads * kMX;
     p.tiles_per_img = (Q + p.RQ - 1) / p.RQ;
     p.T_total = (long long)d.N * p.tiles_per_img;
     const int per_split = p.nkr * p.nft;
@@ -311,6 +401,11 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.Wpad = p.Wpad;
     a.CH = p.CH;
     a.SG = p.SG;
+    a.rows_max = p.rows_max;
+    a.pipelined = p.pipelined;
+    a.magic_rq = host_magic(p.RQ);
+    a.magic_wpad = host_magic(p.Wpad);
+    a.magic_ch = host_magic(p.CH);
     if (dtype == 0) return launch_w<double>(a, p, dW, db, s);
     return launch_w<float>(a, p, dW, db, s);
 }

@@ -83,13 +83,14 @@ __device__ __forceinline__ T relu_if(T v, int relu)
 }
 
 // Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8).
-// Renumber so that logically consecutive blocks share an XCD (and its L2):
-// logical = (b % 8) * ceil(n / 8) + b / 8, valid when the grid is a multiple of 8;
-// otherwise the identity is used.
+// Renumber so that logically consecutive blocks share an XCD (and its L2): with
+// m = floor(n / 8), block b < 8m gets logical id (b % 8) * m + b / 8; the last
+// n % 8 blocks keep their own number.
 __device__ __forceinline__ int xcd_logical_block(int b, int nblocks)
 {
-    if (nblocks % 8 != 0) return b;
-    return (b & 7) * (nblocks >> 3) + (b >> 3);
+    const int m = nblocks >> 3;
+    if (b >= 8 * m) return b;
+    return (b & 7) * m + (b >> 3);
 }
 
 // Kernels asking for more than 64 KiB of dynamic LDS must opt in (gfx950 has
@@ -100,6 +101,20 @@ inline hipError_t allow_dynamic_lds(Kernel kernel, size_t bytes)
     if (bytes <= 64 * 1024) return hipSuccess;
     return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+// Resident blocks of `kernel` per CU for `lds` bytes of dynamic LDS, and the CU
+// count of the current device (both cached per device and LDS size by callers).
+template <typename Kernel>
+inline int resident_slots(Kernel kernel, int threads, size_t lds)
+{
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, lds) != hipSuccess)
+        return 0;
+    return cus * per_cu;
 }
 
 }  // namespace dmlnn

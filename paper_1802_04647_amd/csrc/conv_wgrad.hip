@@ -26,7 +26,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBM = 64;
 constexpr size_t kLdsBudget = 72 * 1024;
-constexpr int kTargetBlocks = 512;
+// Upper bound on resident blocks (256 CUs x 4 blocks) used to size the workspace
+// without a device; the launch uses the measured occupancy, up to this bound.
+constexpr int kMaxResident = 1024;
 constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
 constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
 
@@ -325,22 +327,29 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.tiles_per_img = (Q + p.RQ - 1) / p.RQ;
     p.T_total = (long long)d.N * p.tiles_per_img;
     const int per_split = p.nkr * p.nft;
-    long long splits = (kTargetBlocks + per_split - 1) / per_split;
-    if (splits >= 8) splits = ((splits + 7) / 8) * 8;
+    long long splits = (kMaxResident + per_split - 1) / per_split;
     if (splits > p.T_total) splits = p.T_total;
     if (splits < 1) splits = 1;
-    p.splits = (int)splits;
+    p.splits = (int)splits;  // the most splits a launch may use (workspace size)
     return true;
 }
 
 template <typename T>
-hipError_t launch_w(const WgradArgs &a, const WPlan &p, void *dW, void *db, hipStream_t s)
+hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    dim3 grid(p.splits * p.nkr * p.nft), block(kThreads);
     auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3> : (p.NBW == 2 ? conv_wgrad_kernel<T, 2>
                                                                 : conv_wgrad_kernel<T, 1>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
+    // One resident round: as many splits as the device holds blocks at once (a
+    // second, partial round would nearly double the time), within the workspace.
+    const int per_split = p.nkr * p.nft;
+    int slots = resident_slots(k, kThreads, p.lds);
+    int splits = slots / per_split;
+    if (splits < 1) splits = 1;
+    if (splits > p.splits) splits = p.splits;
+    a.splits = splits;
+    dim3 grid(splits * per_split), block(kThreads);
     hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

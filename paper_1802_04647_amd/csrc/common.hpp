@@ -93,6 +93,40 @@ __device__ __forceinline__ int xcd_logical_block(int b, int nblocks)
     return (b & 7) * m + (b >> 3);
 }
 
+// ---- direct global -> LDS loads (LDS DMA) ----------------------------------
+// A raw buffer resource: 64-bit base, byte range (loads at offsets >= range
+// return 0 without touching memory), and the gfx9-family format word.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+extern "C" __device__ void llvm_amdgcn_raw_buffer_load_lds(i32x4 rsrc, lds_void *lds, int size,
+                                                           int voffset, int soffset, int offset,
+                                                           int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+__device__ __forceinline__ i32x4 buffer_rsrc(const void *base, unsigned range_bytes)
+{
+    const unsigned long long a = (unsigned long long)base;
+    i32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(a & 0xffffffffu));
+    r.y = __builtin_amdgcn_readfirstlane((int)(a >> 32));
+    r.z = __builtin_amdgcn_readfirstlane((int)range_bytes);
+    r.w = 0x00020000;
+    return r;
+}
+
+// Out-of-range voffset: the load writes zeros to LDS.
+constexpr int kDmaZero = (int)0x80000000u;
+
+// One wave-wide DMA of 4 bytes per lane: lane i's dword from byte offset
+// voffset + soffset of the buffer lands at lds_base + 4 i (lds_base wave-uniform).
+__device__ __forceinline__ void dma_dword(i32x4 rsrc, void *lds_base, int voffset, int soffset)
+{
+    llvm_amdgcn_raw_buffer_load_lds(rsrc, (lds_void *)lds_base, 4, voffset, soffset, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Kernels asking for more than 64 KiB of dynamic LDS must opt in (gfx950 has
 // 160 KiB per CU).
 template <typename Kernel>

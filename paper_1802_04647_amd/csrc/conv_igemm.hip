@@ -49,7 +49,7 @@ struct IgemmArgs {
     int KC, KCK;
     int Wpad, CH, SA;
     int pipelined;  // 1: chunk fits the per-thread staging registers
-    unsigned long long magic_kck, magic_hw;
+    unsigned long long magic_kck, magic_hw, magic_wf;
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP>
@@ -260,6 +260,229 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
             }
 }
 
+// ---------------------------------------------------------------------------
+// LDS-DMA variant (the default path).  Same tiling and MFMA loop as above, but
+// each chunk's source window and filter slice are copied global -> LDS by the
+// buffer unit (buffer_load ... lds), double-buffered: the copies of chunk c+1
+// are issued right before the MFMA loop of chunk c, with no register staging
+// and no LDS store phase.  Zero padding, image borders, the k padding and a
+// ragged last channel chunk all come from the buffer range check: lanes whose
+// element lies outside the image (or beyond the tensor) get an out-of-range
+// offset and write 0.  Each lane's byte offset within a chunk is the same for
+// every chunk and stays in a register; the chunk's channel offset is the scalar
+// soffset.  In the backward pass the relu mask source is copied alongside and
+// applied as B fragments are read.
+constexpr int kMaxDmaS = 12;  // source-window DMA instructions per wave per chunk
+constexpr int kMaxDmaA = 20;  // filter-slice DMA instructions per wave per chunk
+constexpr size_t kLdsPerBlock = 80 * 1024;  // two blocks per CU (160 KiB)
+
+struct DmaLayout {
+    int src_bytes, a_bytes, stage_bytes;  // per-stage regions, 256-byte multiples; a_bytes
+                                          // has 256 bytes of slack
+};
+
+template <typename T, int NB, bool BWD, bool ZSKIP>
+__global__ __launch_bounds__(kThreads, 2) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
+                                                                     unsigned w_bytes)
+{
+    using MF = Mfma<T>;
+    constexpr int dpe = sizeof(T) / 4;  // dwords per element
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char *stages = smem;
+
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int wm = wave & 1, wn = wave >> 1;
+    const int n = blockIdx.x / a.tiles_per_img;
+    const int tile = blockIdx.x - n * a.tiles_per_img;
+    const int m0 = blockIdx.y * kBM;
+    const int q0 = tile * (32 * NB);
+    const int qend = min(q0 + 32 * NB, a.Q);
+    const int qy0 = q0 / a.Qw;
+    const int rows_need = ((qend - 1) / a.Qw - qy0) * a.S + a.Hf;
+    const int ybase = qy0 * a.S - a.Ph;
+    const int CHn = rows_need * a.Wpad;
+    const int KCv = a.KC * a.HfWf;
+
+    int lbase[NB];
+#pragma unroll
+    for (int y = 0; y < NB; ++y) {
+        int q = q0 + (wn * NB + y) * 16 + (lane & 15);
+        int qy = q / a.Qw, qx = q - qy * a.Qw;
+        lbase[y] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+    }
+
+    typename MF::acc_t acc[2][NB];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < NB; ++y) acc[x][y] = MF::zero();
+
+    const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
+    const unsigned img_bytes = (unsigned)(img * sizeof(T));
+    const bool has_mask = BWD && a.mask != nullptr;
+    const i32x4 rs_src = buffer_rsrc(reinterpret_cast<const T *>(a.src) + (size_t)n * img, img_bytes);
+    const i32x4 rs_msk = has_mask ? buffer_rsrc(reinterpret_cast<const T *>(a.mask) + (size_t)n * img,
+                                                img_bytes)
+                                  : rs_src;
+    const i32x4 rs_w = buffer_rsrc(a.wgt, w_bytes);
+
+    // Per-lane byte offsets inside a chunk (channel c0 excluded), or kDmaZero.
+    const int Ds = a.KC * CHn * dpe;
+    const int NIs = (Ds + kWave - 1) / kWave;
+    const int Da = kBM * a.SA * dpe;
+    const int NIa = (Da + kWave - 1) / kWave;
+    int vs_off[kMaxDmaS], va_off[kMaxDmaA];
+#pragma unroll
+    for (int j = 0; j < kMaxDmaS; ++j) {
+        const int ii = wave + 4 * j, d = ii * kWave + lane;
+        int off = kDmaZero;
+        if (ii < NIs && d < Ds) {
+            const int e = d / dpe, h = d - e * dpe;
+            const int r = e / a.Wpad, x = e - r * a.Wpad;
+            const int c = r / rows_need, t = r - c * rows_need;
+            const int yv = ybase + t, xv = x - a.Pw;
+            const int ys = yv / a.up, xs = xv / a.up;
+            if (yv >= 0 && ys * a.up == yv && ys < a.Sh && xv >= 0 && xs * a.up == xv && xs < a.Sw)
+                off = (int)((((size_t)c * a.Sh + ys) * a.Sw + xs) * sizeof(T)) + 4 * h;
+        }
+        vs_off[j] = off;
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxDmaA; ++j) {
+        const int ii = wave + 4 * j, d = ii * kWave + lane;
+        int off = kDmaZero;
+        if (ii < NIa && d < Da) {
+            const int e = d / dpe, h = d - e * dpe;
+            const int m = e / a.SA, kk = e - m * a.SA;
+            const int mg = m0 + m;
+            if (mg < a.M && kk < KCv) {
+                size_t el;
+                if (!BWD) {
+                    el = (size_t)mg * a.Cs * a.HfWf + kk;
+                } else {
+                    const int c = kk / a.HfWf, t = kk - c * a.HfWf;
+                    el = ((size_t)c * a.M + mg) * a.HfWf + (a.HfWf - 1 - t);
+                }
+                off = (int)(el * sizeof(T)) + 4 * h;
+            }
+        }
+        va_off[j] = off;
+    }
+
+    // LDS: two stages of [source window][A slice], then one mask window (the
+    // backward pass's relu mask lands there and is folded into the source
+    // window of its stage before that stage's MFMAs read it).
+    auto stage_src = [&](int st) { return reinterpret_cast<T *>(stages + st * L.stage_bytes); };
+    auto stage_a = [&](int st) {
+        return reinterpret_cast<T *>(stages + st * L.stage_bytes + L.src_bytes);
+    };
+    T *const s_msk = reinterpret_cast<T *>(stages + 2 * L.stage_bytes);
+    auto issue = [&](int st, int c0) {
+        unsigned char *ps = reinterpret_cast<unsigned char *>(stage_src(st));
+        unsigned char *pm = reinterpret_cast<unsigned char *>(s_msk);
+        unsigned char *pa = reinterpret_cast<unsigned char *>(stage_a(st));
+        const int so_src = (int)((size_t)c0 * a.Sh * a.Sw * sizeof(T));
+        const int so_w = (int)((size_t)c0 * (BWD ? a.M : 1) * a.HfWf * sizeof(T));
+#pragma unroll
+        for (int j = 0; j < kMaxDmaS; ++j) {
+            const int ii = wave + 4 * j;
+            if (ii < NIs) {
+                dma_dword(rs_src, ps + ii * 256, vs_off[j], so_src);
+                if (has_mask) dma_dword(rs_msk, pm + ii * 256, vs_off[j], so_src);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxDmaA; ++j) {
+            const int ii = wave + 4 * j;
+            if (ii < NIa) dma_dword(rs_w, pa + ii * 256, va_off[j], so_w);
+        }
+    };
+
+    issue(0, 0);
+    wait_dma();
+    __syncthreads();
+    int st = 0;
+    for (int c0 = 0; c0 < a.Cs; c0 += a.KC) {
+        if (has_mask) {
+            // dout * (out_fwd > 0) in place; the mask window is free again after
+            // the barrier, so the next chunk's mask may land in it.
+            T *w = stage_src(st);
+            const int nel = a.KC * CHn;
+            for (int e = tid; e < nel; e += kThreads)
+                if (!(s_msk[e] > T(0))) w[e] = T(0);
+            __syncthreads();
+        }
+        if (c0 + a.KC < a.Cs) issue(st ^ 1, c0 + a.KC);
+
+        const T *s_src = stage_src(st);
+        const T *arow0 = stage_a(st) + (wm * 32 + (lane & 15)) * a.SA + (lane >> 4);
+        const T *arow1 = arow0 + 16 * a.SA;
+        // Fragments are software-pipelined: the A/B fragments of k-step kk+4
+        // are read into their own registers while the MFMAs of step kk issue,
+        // so LDS latency overlaps the matrix pipe.  The tap offset of a step is
+        // computed arithmetically, so the B reads need no dependent LDS read.
+        auto tap_off = [&](int k) {
+            if (k >= KCv) return 0;
+            const int c = div_magic(k, a.magic_hw), t = k - c * a.HfWf;
+            const int i = div_magic(t, a.magic_wf), j = t - i * a.Wf;
+            return c * CHn + i * a.Wpad + j;
+        };
+        T a0 = arow0[0], a1 = arow1[0];
+        T b[NB];
+        {
+            const int ko = tap_off(lane >> 4);
+#pragma unroll
+            for (int y = 0; y < NB; ++y) b[y] = s_src[ko + lbase[y]];
+        }
+        for (int kk = 0; kk < a.KCK; kk += 4) {
+            // Unconditional, so no branch separates these reads from the MFMAs
+            // below; on the last step they read the A slice's slack and tap 0
+            // (in bounds, unused).
+            T nb[NB];
+            const T na0 = arow0[kk + 4], na1 = arow1[kk + 4];
+            {
+                const int ko = tap_off(kk + 4 + (lane >> 4));
+#pragma unroll
+                for (int y = 0; y < NB; ++y) nb[y] = s_src[ko + lbase[y]];
+            }
+#pragma unroll
+            for (int y = 0; y < NB; ++y) {
+                const T bv = b[y];
+                if (ZSKIP && wave_all_zero(bv)) continue;
+                acc[0][y] = MF::mma(a0, bv, acc[0][y]);
+                acc[1][y] = MF::mma(a1, bv, acc[1][y]);
+            }
+            a0 = na0;
+            a1 = na1;
+#pragma unroll
+            for (int y = 0; y < NB; ++y) b[y] = nb[y];
+        }
+        wait_dma();
+        __syncthreads();
+        st ^= 1;
+    }
+
+    T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
+    const T *bias = reinterpret_cast<const T *>(a.bias);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < NB; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                int m = m0 + wm * 32 + x * 16 + MF::row(lane, r);
+                int q = q0 + (wn * NB + y) * 16 + (lane & 15);
+                if (m < a.M && q < qend) {
+                    T v = acc[x][y][r];
+                    if (!BWD) {
+                        if (bias) v += bias[m];
+                        v = relu_if(v, a.relu);
+                    }
+                    out[(size_t)m * a.Q + q] = v;
+                }
+            }
+}
+
 // Host-side tile selection ----------------------------------------------------
 
 struct Plan {
@@ -295,8 +518,16 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
             p.tiles_per_img = tiles;
         }
     }
+    // Input rows a tile of BN consecutive outputs reads: the exact maximum over
+    // the tiles of an image (a tile that starts a row spans one row fewer than
+    // the general bound when BN is a multiple of the output width).
     const int BN = 32 * p.NB;
-    const int rows_max = ((Qw + BN - 2) / Qw) * S + Hf;
+    int rows_max = 0;
+    for (int t = 0; t < p.tiles_per_img; ++t) {
+        const int qa = t * BN, qb = (qa + BN < Q ? qa + BN : Q) - 1;
+        const int r = (qb / Qw - qa / Qw) * S + Hf;
+        rows_max = r > rows_max ? r : rows_max;
+    }
     p.Wpad = (Qw - 1) * S + Wf;
     p.CH = rows_max * p.Wpad;
     // Largest channel chunk whose staging fits the per-thread register slots
@@ -322,6 +553,55 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
     p.SA = p.KCK + 1;
     p.lds = lds_bytes(tsz, p.KC, p.CH, p.SA, p.KCK);
     return p.lds <= 160 * 1024;
+}
+
+// LDS-DMA plan: the largest channel chunk (up to 16) whose per-wave DMA
+// instruction counts fit the offset registers and whose two stages fit the
+// per-block LDS share.  False when the problem needs the register-staged path
+// (very wide rows, very large filters, or tensors of 2 GiB and more, whose byte
+// offsets would reach the out-of-range marker).
+bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpad,
+                   size_t img_bytes, size_t w_bytes, Plan &p, DmaLayout &L)
+{
+    if (img_bytes >= 0x80000000ull || w_bytes >= 0x80000000ull) return false;
+    const long long dpe = (long long)tsz / 4;
+    for (int kc = Cs < 16 ? Cs : 16; kc >= 1; --kc) {
+        const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 1;
+        const long long nis = ((long long)kc * rows_max * Wpad * dpe + kWave - 1) / kWave;
+        const long long nia = ((long long)kBM * sa * dpe + kWave - 1) / kWave;
+        if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > kMaxDmaA) continue;
+        DmaLayout l;
+        l.src_bytes = (int)nis * 256;
+        l.a_bytes = (int)nia * 256 + 256;  // + slack read by the last step's prefetch
+        l.stage_bytes = l.src_bytes + l.a_bytes;
+        const size_t total = 2 * (size_t)l.stage_bytes + (bwd ? (size_t)l.src_bytes : 0);
+        if (total > kLdsPerBlock) continue;
+        p.KC = kc;
+        p.KCK = kck;
+        p.SA = sa;
+        p.lds = total;
+        L = l;
+        return true;
+    }
+    return false;
+}
+
+template <typename T, int NB, bool BWD>
+hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
+                      int nimg, int zero_skip, hipStream_t s)
+{
+    dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
+    hipError_t e;
+    if (zero_skip) {
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, true>;
+        if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
+    } else {
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, false>;
+        if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
+    }
+    return hipGetLastError();
 }
 
 template <typename T, int NB, bool BWD>
@@ -361,6 +641,25 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.pipelined = p.pipelined;
     a.magic_kck = host_magic(p.KCK);
     a.magic_hw = host_magic(a.HfWf);
+    a.magic_wf = host_magic(a.Wf);
+
+    const size_t img_bytes = (size_t)Cs * a.Sh * a.Sw * sizeof(T);
+    const size_t w_bytes = (size_t)M * Cs * a.HfWf * sizeof(T);
+    Plan pd = p;
+    DmaLayout L;
+    if (make_dma_plan(sizeof(T), BWD, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
+                      L)) {
+        IgemmArgs ad = a;
+        ad.KC = pd.KC;
+        ad.KCK = pd.KCK;
+        ad.SA = pd.SA;
+        switch (pd.NB) {
+        case 7: return launch_dma<T, 7, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
+        case 4: return launch_dma<T, 4, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
+        case 2: return launch_dma<T, 2, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
+        default: return launch_dma<T, 1, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
+        }
+    }
     switch (p.NB) {
     case 7: return launch_nb<T, 7, BWD>(a, p, nimg, zero_skip, s);
     case 4: return launch_nb<T, 4, BWD>(a, p, nimg, zero_skip, s);

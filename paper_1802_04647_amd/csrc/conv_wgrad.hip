@@ -40,6 +40,7 @@ struct WgradArgs {
     int Wpad, CH, SG;
     int pipelined;  // 1: a pixel tile fits the per-thread staging registers
     int rows_max;
+    int spr;        // 0: tiles are runs of whole output rows; else slices per output row
     unsigned long long magic_rq, magic_wpad, magic_ch;
 };
 
@@ -88,20 +89,34 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     const long long t_begin = (long long)split * a.T_total / a.splits;
     const long long t_end = (long long)(split + 1) * a.T_total / a.splits;
 
-    // Pixel tile tt covers pixels [q0, qend) of image n; its X window is the
-    // rows_need input rows of channels c_lo .. c_lo+nch-1 that the windows touch.
+    // Pixel tile tt covers pixels [q0, qend) of image n.  Its X window is the
+    // rows_need input rows of channels c_lo .. c_lo+nch-1 that the windows touch,
+    // and Wpad columns starting at input column xbase: the whole padded row when
+    // tiles are runs of whole output rows, or just the columns of one slice of an
+    // output row when rows are wider than a tile (spr > 0).
     struct TileGeo {
-        int n, q0, qend, qy0, rows_need, ybase;
+        int n, q0, qend, qy0, ow0, rows_need, ybase, xbase;
     };
     auto geo = [&](long long tt) {
         TileGeo g;
         g.n = (int)(tt / a.tiles_per_img);
         const int qt = (int)(tt - (long long)g.n * a.tiles_per_img);
-        g.q0 = qt * a.RQ;
-        g.qend = min(g.q0 + a.RQ, a.Q);
-        g.qy0 = g.q0 / a.Wout;
-        g.rows_need = ((g.qend - 1) / a.Wout - g.qy0) * a.S + a.Hf;
+        if (a.spr) {
+            const int oh = qt / a.spr;
+            g.ow0 = (qt - oh * a.spr) * a.RQ;
+            g.q0 = oh * a.Wout + g.ow0;
+            g.qend = g.q0 + min(a.RQ, a.Wout - g.ow0);
+            g.qy0 = oh;
+            g.rows_need = a.Hf;
+        } else {
+            g.ow0 = 0;
+            g.q0 = qt * a.RQ;
+            g.qend = min(g.q0 + a.RQ, a.Q);
+            g.qy0 = g.q0 / a.Wout;
+            g.rows_need = ((g.qend - 1) / a.Wout - g.qy0) * a.S + a.Hf;
+        }
         g.ybase = g.qy0 * a.S - a.P;
+        g.xbase = g.ow0 * a.S - a.P;
         return g;
     };
 
@@ -136,7 +151,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             if (e < tot_x) {
                 const int c = div_magic(e, a.magic_ch), rem = e - c * a.CH;
                 const int t = div_magic(rem, a.magic_wpad), u = rem - t * a.Wpad;
-                const int cg = c_lo + c, y = g.ybase + t, x = u - a.P;
+                const int cg = c_lo + c, y = g.ybase + t, x = g.xbase + u;
                 if (t < g.rows_need && cg < a.C && y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
                     v = X[(((size_t)g.n * a.C + cg) * a.Hin + y) * a.Win + x];
             }
@@ -182,7 +197,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             size_t xoff = (((size_t)g.n * a.C + cg) * a.Hin + (rowok ? y : 0)) * a.Win;
             T *dst = s_x + c * a.CH + t * a.Wpad;
             for (int u = lane; u < a.Wpad; u += kWave) {
-                int x = u - a.P;
+                int x = g.xbase + u;
                 dst[u] = (rowok && x >= 0 && x < a.Win) ? X[xoff + x] : T(0);
             }
         }
@@ -199,7 +214,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
         for (int u = tid; u < a.RQ; u += kThreads) {
             int q = cur.q0 + u;
             int qy = q / a.Wout, qx = q - qy * a.Wout;
-            s_qoff[u] = (q < cur.qend) ? (qy - cur.qy0) * a.S * a.Wpad + qx * a.S : 0;
+            s_qoff[u] = (q < cur.qend) ? (qy - cur.qy0) * a.S * a.Wpad + (qx - cur.ow0) * a.S : 0;
         }
         __syncthreads();
         if (a.pipelined && tt + 1 < t_end) {
@@ -279,7 +294,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *
 }
 
 struct WPlan {
-    int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined;
+    int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined, spr;
     long long T_total;
     size_t lds;
 };
@@ -300,9 +315,35 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.nft = (d.F + kBM - 1) / kBM;
     p.Wpad = (d.Wout - 1) * d.stride + d.Wf;
     const int nch_alloc = (p.KR - 1) / HfWf + 2;
-    // Pixel tile: whole output rows when a row is short (at most 56 pixels so the
-    // g tile fits the staging registers), else a 56-pixel slice; a multiple of 4.
-    int rq = d.Wout <= 56 ? d.Wout * (56 / d.Wout) : 56;
+    p.spr = 0;
+    if (d.Wout > 56) {
+        // Rows wider than a tile: each tile is one slice of an output row (at
+        // most 56 pixels, a multiple of 4) and its X window spans only the
+        // slice's input columns.
+        int spr = (d.Wout + 55) / 56;
+        int rq = ((d.Wout + spr - 1) / spr + 3) / 4 * 4;
+        spr = (d.Wout + rq - 1) / rq;
+        p.spr = spr;
+        p.RQ = rq;
+        p.rows_max = d.Hf;
+        p.Wpad = (rq - 1) * d.stride + d.Wf;
+        p.CH = p.rows_max * p.Wpad;
+        p.SG = rq + 1;
+        p.lds = wlds(tsz, p.SG, nch_alloc, p.CH, rq);
+        if (p.lds > 160 * 1024) return false;
+        p.pipelined = kBM * p.RQ <= kThreads * kMG && (long long)nch_alloc * p.CH <= kThreads * kMX;
+        p.tiles_per_img = d.Hout * spr;
+        p.T_total = (long long)d.N * p.tiles_per_img;
+        const int per_split = p.nkr * p.nft;
+        long long splits = (kMaxResident + per_split - 1) / per_split;
+        if (splits > p.T_total) splits = p.T_total;
+        if (splits < 1) splits = 1;
+        p.splits = (int)splits;
+        return true;
+    }
+    // Pixel tile: whole output rows (at most 56 pixels so the g tile fits the
+    // staging registers), a multiple of 4.
+    int rq = d.Wout * (56 / d.Wout);
     if (rq > Q) rq = Q;
     rq = ((rq + 3) / 4) * 4;
     for (;;) {
@@ -412,6 +453,7 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.SG = p.SG;
     a.rows_max = p.rows_max;
     a.pipelined = p.pipelined;
+    a.spr = p.spr;
     a.magic_rq = host_magic(p.RQ);
     a.magic_wpad = host_magic(p.Wpad);
     a.magic_ch = host_magic(p.CH);

@@ -29,6 +29,8 @@ CASES = [
     ConvShape(3, 2, 1, 1, 4, 3, 3, 1, 1),       # 1x1 image
     ConvShape(2, 2, 9, 7, 3, 2, 3, 2, 0),       # uncovered border cells
     ConvShape(1, 6, 30, 30, 33, 3, 3, 1, 1),    # many pixel tiles per image
+    ConvShape(1, 2, 5, 500, 3, 3, 3, 1, 1),     # rows too wide for LDS-DMA staging
+    ConvShape(1, 3, 4, 700, 2, 3, 3, 2, 1),     # wide rows, stride 2
 ]
 
 

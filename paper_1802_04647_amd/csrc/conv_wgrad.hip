@@ -41,7 +41,7 @@ struct WgradArgs {
     int pipelined;  // 1: a pixel tile fits the per-thread staging registers
     int rows_max;
     int spr;        // 0: tiles are runs of whole output rows; else slices per output row
-    unsigned long long magic_rq, magic_wpad, magic_ch;
+    unsigned long long magic_rq, magic_wpad, magic_ch, magic_wout, magic_hwf, magic_wf;
 };
 
 template <typename T, int NBW>
@@ -51,8 +51,6 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     extern __shared__ __align__(16) unsigned char smem[];
     T *s_g = reinterpret_cast<T *>(smem);
     T *s_x = s_g + kBM * a.SG;
-    const int nch_alloc = (a.KR - 1) / a.HfWf + 2;
-    int *s_qoff = reinterpret_cast<int *>(s_x + (size_t)nch_alloc * a.CH);
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
     const int L = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -205,18 +203,15 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
 
     TileGeo cur = geo(t_begin);
     if (a.pipelined && t_begin < t_end) load(cur);
+    const int lq = lane >> 4;
     for (long long tt = t_begin; tt < t_end; ++tt) {
         __syncthreads();
         if (a.pipelined)
             store(cur);
         else
             stage_direct(cur);
-        for (int u = tid; u < a.RQ; u += kThreads) {
-            int q = cur.q0 + u;
-            int qy = q / a.Wout, qx = q - qy * a.Wout;
-            s_qoff[u] = (q < cur.qend) ? (qy - cur.qy0) * a.S * a.Wpad + (qx - cur.ow0) * a.S : 0;
-        }
         __syncthreads();
+        const TileGeo g = cur;
         if (a.pipelined && tt + 1 < t_end) {
             cur = geo(tt + 1);
             load(cur);
@@ -229,19 +224,43 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             for (int u = tid & 3; u < a.RQ; u += 4) dbacc += gr[u];
         }
 
-        const T *grow = s_g + (lane & 15) * a.SG + (lane >> 4);
-        const int *qof = s_qoff + (lane >> 4);
+        // LDS offset of pixel q0 + qq + lane/16 inside the X window (0 past the
+        // tile's end: such columns of g are zero).  The row is found relative to
+        // the tile's first row, so the magic division stays exact.
+        auto q_off = [&](int qq) {
+            const int q = g.q0 + qq + lq;
+            if (q >= g.qend) return 0;
+            const int rel = q - g.qy0 * a.Wout;
+            const int dy = div_magic(rel, a.magic_wout), qx = rel - dy * a.Wout;
+            return dy * a.S * a.Wpad + (qx - g.ow0) * a.S;
+        };
+        // Fragments are software-pipelined: those of step qq+4 are read while the
+        // MFMAs of step qq issue.  The reads after the last step stay inside LDS
+        // (the g rows are followed by the X window) and are not used.
+        const T *grow = s_g + (lane & 15) * a.SG + lq;
+        T av[4], bv[NBW];
+        {
+            const int qo = q_off(0);
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) bv[nb] = s_x[kof[nb] + qo];
+        }
         for (int qq = 0; qq < a.RQ; qq += 4) {
-            const int qo = qof[qq];
-            T av[4];
+            T nav[4], nbv[NBW];
+            const int nqo = q_off(qq + 4);
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG + qq];
+            for (int mb = 0; mb < 4; ++mb) nav[mb] = grow[mb * 16 * a.SG + qq + 4];
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb) {
-                T bv = s_x[kof[nb] + qo];
+            for (int nb = 0; nb < NBW; ++nb) nbv[nb] = s_x[kof[nb] + nqo];
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
-            }
+            for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv[nb], acc[mb][nb]);
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) av[mb] = nav[mb];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) bv[nb] = nbv[nb];
         }
     }
 
@@ -293,6 +312,231 @@ __global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *
     }
 }
 
+// Row-ring variant for layers whose output rows fit one tile (Wout <= 60).
+// A block of 12 waves covers the whole k range (up to 12 x 16 x NBW columns),
+// so each g tile is staged once for all of dW's columns instead of once per
+// k-range block.  A pixel tile is one output row; consecutive tiles of a block
+// are consecutive rows of one image, so the X window (Hf input rows per
+// channel) is a ring: input row y (counted from the top padding row, yr = y +
+// P) lives in slot yr mod Hf, and the next tile only stages its min(S, Hf) new
+// rows.  The first tile of a block and of each image restages all Hf rows.
+constexpr int kRingThreads = 768;
+constexpr int kRingWaves = kRingThreads / kWave;
+constexpr int kRG = 5;  // g-tile elements each thread stages per tile
+constexpr int kRX = 5;  // new X-row elements each thread stages per tile
+
+template <typename T, int NBW>
+__global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradArgs a)
+{
+    using MF = Mfma<T>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_g = reinterpret_cast<T *>(smem);
+    T *s_x = s_g + kBM * a.SG;  // [channel][slot][Wpad]
+
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int L = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int kr = L % a.nkr;
+    const int rest = L / a.nkr;
+    const int ft = rest % a.nft;
+    const int split = rest / a.nft;
+
+    const int kbeg = kr * a.KR;
+    const int kend = min(a.K, kbeg + a.KR);
+    const int c_lo = kbeg / a.HfWf;
+    const int nch = (kend - 1) / a.HfWf - c_lo + 1;
+    const int nr = min(a.S, a.Hf);  // new input rows per consecutive tile
+
+
+    typename MF::acc_t acc[4][NBW];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = MF::zero();
+    T dbacc = T(0);
+
+    const T *X = reinterpret_cast<const T *>(a.X);
+    const T *dout = reinterpret_cast<const T *>(a.dout);
+    const T *mask = reinterpret_cast<const T *>(a.mask);
+    const long long t_begin = (long long)split * a.T_total / a.splits;
+    const long long t_end = (long long)(split + 1) * a.T_total / a.splits;
+
+    // Input row yr (from the top padding row) of channel c_lo + c, or zeros.
+    auto x_at = [&](int n, int c, int yr, int u) -> T {
+        const int cg = c_lo + c, y = yr - a.P, x = u - a.P;
+        if (cg < a.C && y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
+            return X[(((size_t)n * a.C + cg) * a.Hin + y) * a.Win + x];
+        return T(0);
+    };
+
+    T vg[kRG], vm[kRG], vx[kRX];
+    auto load_g = [&](int n, int oh) {
+        const int tid = opaque(threadIdx.x);
+        const size_t gbase = ((size_t)n * a.F + ft * kBM) * a.Q + (size_t)oh * a.Wout;
+#pragma unroll
+        for (int it = 0; it < kRG; ++it) {
+            const int e = tid + kRingThreads * it;
+            T v = T(0), mv = T(1);
+            if (e < kBM * a.RQ) {
+                const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
+                if (ft * kBM + r < a.F && u < a.Wout) {
+                    const size_t o = gbase + (size_t)r * a.Q + u;
+                    v = dout[o];
+                    if (mask) mv = mask[o];
+                }
+            }
+            vg[it] = v;
+            vm[it] = mv;
+        }
+    };
+    auto store_g = [&]() {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kRG; ++it) {
+            const int e = tid + kRingThreads * it;
+            if (e < kBM * a.RQ) {
+                const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
+                s_g[r * a.SG + u] = (vm[it] > T(0)) ? vg[it] : T(0);
+            }
+        }
+    };
+    // The nr new rows of tile oh (rows yr = oh*S + Hf - nr + r).
+    const int nrw = nr * a.Wpad;
+    auto load_x = [&](int n, int oh) {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kRX; ++it) {
+            const int e = tid + kRingThreads * it;
+            T v = T(0);
+            if (e < nch * nrw) {
+                const int c = div_magic(e, a.magic_ch), rem = e - c * nrw;
+                const int r = div_magic(rem, a.magic_wpad), u = rem - r * a.Wpad;
+                v = x_at(n, c, oh * a.S + a.Hf - nr + r, u);
+            }
+            vx[it] = v;
+        }
+    };
+    auto store_x = [&](int oh) {
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < kRX; ++it) {
+            const int e = tid + kRingThreads * it;
+            if (e < nch * nrw) {
+                const int c = div_magic(e, a.magic_ch), rem = e - c * nrw;
+                const int r = div_magic(rem, a.magic_wpad), u = rem - r * a.Wpad;
+                const int yr = oh * a.S + a.Hf - nr + r;
+                s_x[c * a.CH + (yr % a.Hf) * a.Wpad + u] = vx[it];
+            }
+        }
+    };
+    // All Hf rows of tile oh, straight from global memory (first tile of an image).
+    auto stage_x_full = [&](int n, int oh) {
+        const int tot = nch * a.CH;
+        for (int e = tid; e < tot; e += kRingThreads) {
+            const int c = e / a.CH, rem = e - c * a.CH;
+            const int t = rem / a.Wpad, u = rem - t * a.Wpad;
+            const int yr = oh * a.S + t;
+            s_x[c * a.CH + (yr % a.Hf) * a.Wpad + u] = x_at(n, c, yr, u);
+        }
+    };
+
+    if (t_begin < t_end) {
+        const int n0 = (int)(t_begin / a.Hout), oh0 = (int)(t_begin - (long long)n0 * a.Hout);
+        load_g(n0, oh0);
+        store_g();
+        stage_x_full(n0, oh0);
+        __syncthreads();
+        if (t_begin + 1 < t_end) {
+            const long long t1 = t_begin + 1;
+            const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
+            load_g(n1, oh1);
+            if (oh1 != 0) load_x(n1, oh1);
+        }
+    }
+    const int lq = lane >> 4;
+    for (long long tt = t_begin; tt < t_end; ++tt) {
+        const int n = (int)(tt / a.Hout), oh = (int)(tt - (long long)n * a.Hout);
+        // LDS offset of column k = (c, i, j) of this lane's blocks: filter row i
+        // of this tile sits in slot (oh*S + i) mod Hf.
+        const int rot = (oh * a.S) % a.Hf;
+        int kof[NBW];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            const int k = kbeg + (wave * NBW + nb) * 16 + (lane & 15);
+            const int c = div_magic(k, a.magic_hwf), t = k - c * a.HfWf;
+            const int i = div_magic(t, a.magic_wf), j = t - i * a.Wf;
+            int sl = rot + i;
+            sl -= sl >= a.Hf ? a.Hf : 0;
+            kof[nb] = k < kend ? (c - c_lo) * a.CH + sl * a.Wpad + j : 0;
+        }
+
+        if (kr == 0) {  // bias gradient: thread (f = tid/12, phase = tid%12), fixed order
+            const T *gr = s_g + (tid / 12) * a.SG;
+            for (int u = tid % 12; u < a.RQ; u += 12) dbacc += gr[u];
+        }
+
+        const T *grow = s_g + (lane & 15) * a.SG + lq;
+        for (int qq = 0; qq < a.RQ; qq += 4) {
+            const int qx = qq + lq;
+            const int qo = qx < a.Wout ? qx * a.S : 0;
+            T av[4];
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG + qq];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                const T bv = s_x[kof[nb] + qo];
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
+            }
+        }
+
+        if (tt + 1 < t_end) {
+            const long long t1 = tt + 1;
+            const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
+            __syncthreads();
+            store_g();
+            if (oh1 != 0)
+                store_x(oh1);
+            else
+                stage_x_full(n1, oh1);
+            __syncthreads();
+            if (tt + 2 < t_end) {
+                const long long t2 = tt + 2;
+                const int n2 = (int)(t2 / a.Hout), oh2 = (int)(t2 - (long long)n2 * a.Hout);
+                load_g(n2, oh2);
+                if (oh2 != 0) load_x(n2, oh2);
+            }
+        }
+    }
+
+    T *wsp = reinterpret_cast<T *>(a.ws) + (size_t)split * a.F * a.K;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                int f = ft * kBM + mb * 16 + MF::row(lane, r);
+                int k = kbeg + (wave * NBW + nb) * 16 + (lane & 15);
+                if (f < a.F && k < kend) wsp[(size_t)f * a.K + k] = acc[mb][nb][r];
+            }
+
+    if (kr == 0) {
+        __syncthreads();
+        T *s_red = s_g;
+        s_red[tid] = dbacc;
+        __syncthreads();
+        if (tid < kBM) {
+            int f = ft * kBM + tid;
+            if (f < a.F) {
+                T sum = T(0);
+                for (int p = 0; p < 12; ++p) sum += s_red[12 * tid + p];
+                T *wsdb = reinterpret_cast<T *>(a.ws) + (size_t)a.splits * a.F * a.K;
+                wsdb[(size_t)split * a.F + f] = sum;
+            }
+        }
+    }
+}
+
 struct WPlan {
     int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined, spr;
     long long T_total;
@@ -301,7 +545,8 @@ struct WPlan {
 
 size_t wlds(size_t tsz, int SG, int nch, int CH, int RQ)
 {
-    return tsz * ((size_t)kBM * SG + (size_t)nch * CH) + sizeof(int) * (size_t)RQ;
+    (void)RQ;
+    return tsz * ((size_t)kBM * SG + (size_t)nch * CH);
 }
 
 bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
@@ -375,6 +620,77 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
     return true;
 }
 
+// Plan for the row-ring kernel, or false when the layer does not suit it: rows
+// wider than 60 outputs, a k range that 12 waves cover poorly, or an LDS window
+// over the per-CU budget.
+bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
+{
+    const int K = d.C * d.Hf * d.Wf;
+    const int HfWf = d.Hf * d.Wf;
+    if (d.Wout > 60) return false;
+    double best = 0.0;
+    int nbw = 0;
+    for (int cand = 3; cand >= 1; --cand) {
+        const int kr = 16 * cand * kRingWaves;
+        const int nkr = (K + kr - 1) / kr;
+        const double eff = (double)K / ((double)nkr * kr);
+        if (eff > best + 1e-9) {
+            best = eff;
+            nbw = cand;
+        }
+    }
+    if (best < 0.85) return false;
+    p.NBW = nbw;
+    p.KR = 16 * nbw * kRingWaves;
+    p.nkr = (K + p.KR - 1) / p.KR;
+    p.nft = (d.F + kBM - 1) / kBM;
+    p.RQ = (d.Wout + 3) / 4 * 4;
+    p.SG = p.RQ + 1;
+    p.spr = 0;
+    p.rows_max = d.Hf;
+    p.Wpad = (d.Wout - 1) * d.stride + d.Wf;
+    p.CH = d.Hf * p.Wpad;
+    const int nch_alloc = (p.KR - 1) / HfWf + 2;
+    const int nr = d.stride < d.Hf ? d.stride : d.Hf;
+    if (kBM * p.SG < kRingThreads) return false;  // the db reduction reuses the g tile
+    if (kBM * p.RQ > kRingThreads * kRG) return false;
+    if ((long long)nch_alloc * nr * p.Wpad > (long long)kRingThreads * kRX) return false;
+    p.lds = tsz * ((size_t)kBM * p.SG + (size_t)nch_alloc * p.CH);
+    if (p.lds > 160 * 1024) return false;
+    p.pipelined = 1;
+    p.tiles_per_img = d.Hout;
+    p.T_total = (long long)d.N * d.Hout;
+    const int per_split = p.nkr * p.nft;
+    long long splits = (kMaxResident + per_split - 1) / per_split;
+    if (splits > p.T_total) splits = p.T_total;
+    if (splits < 1) splits = 1;
+    p.splits = (int)splits;
+    return true;
+}
+
+template <typename T>
+hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
+{
+    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3>
+                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2> : conv_wgrad_ring_kernel<T, 1>);
+    hipError_t e = allow_dynamic_lds(k, p.lds);
+    if (e != hipSuccess) return e;
+    const int per_split = p.nkr * p.nft;
+    int splits = resident_slots(k, kRingThreads, p.lds) / per_split;
+    if (splits < 1) splits = 1;
+    if (splits > p.splits) splits = p.splits;
+    a.splits = splits;
+    hipLaunchKernelGGL(k, dim3(splits * per_split), dim3(kRingThreads), p.lds, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int FK = a.F * a.K;
+    const int total = FK + (db ? a.F : 0);
+    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 255) / 256), dim3(256), 0, s,
+                       reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
+                       reinterpret_cast<T *>(db), FK, a.F, a.splits);
+    return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
@@ -407,10 +723,12 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d)
 {
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
-    WPlan p;
+    WPlan p, r;
     if (!make_wplan(tsz, d, p)) return 0;
+    int splits = p.splits;
+    if (make_rplan(tsz, d, r) && r.splits > splits) splits = r.splits;
     const size_t K = (size_t)d.C * d.Hf * d.Wf;
-    return tsz * (size_t)p.splits * ((size_t)d.F * K + (size_t)d.F);
+    return tsz * (size_t)splits * ((size_t)d.F * K + (size_t)d.F);
 }
 
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
@@ -457,6 +775,28 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.magic_rq = host_magic(p.RQ);
     a.magic_wpad = host_magic(p.Wpad);
     a.magic_ch = host_magic(p.CH);
+    a.magic_wout = host_magic(d.Wout);
+    a.magic_hwf = host_magic(a.HfWf);
+    a.magic_wf = host_magic(d.Wf);
+    WPlan r;
+    if (make_rplan(tsz, d, r)) {
+        WgradArgs b = a;
+        b.KR = r.KR;
+        b.nkr = r.nkr;
+        b.RQ = r.RQ;
+        b.tiles_per_img = r.tiles_per_img;
+        b.T_total = (int)r.T_total;
+        b.Wpad = r.Wpad;
+        b.CH = r.CH;
+        b.SG = r.SG;
+        b.rows_max = r.rows_max;
+        b.spr = 0;
+        b.magic_rq = host_magic(r.RQ);
+        b.magic_wpad = host_magic(r.Wpad);
+        b.magic_ch = host_magic((d.stride < d.Hf ? d.stride : d.Hf) * r.Wpad);
+        if (dtype == 0) return launch_ring<double>(b, r, dW, db, s);
+        return launch_ring<float>(b, r, dW, db, s);
+    }
     if (dtype == 0) return launch_w<double>(a, p, dW, db, s);
     return launch_w<float>(a, p, dW, db, s);
 }

@@ -31,6 +31,15 @@ CASES = [
     ConvShape(1, 6, 30, 30, 33, 3, 3, 1, 1),    # many pixel tiles per image
     ConvShape(1, 2, 5, 500, 3, 3, 3, 1, 1),     # rows too wide for LDS-DMA staging
     ConvShape(1, 3, 4, 700, 2, 3, 3, 2, 1),     # wide rows, stride 2
+    # backward_filter row-ring kernel (whole k range per block)
+    ConvShape(2, 64, 7, 12, 3, 3, 3, 1, 1),     # k range 576, image boundary inside a split
+    ConvShape(2, 64, 6, 24, 5, 3, 3, 2, 1),     # stride 2: two new rows per tile
+    ConvShape(1, 42, 12, 13, 4, 3, 3, 1, 0),    # k range 384, no padding
+    ConvShape(3, 7, 10, 20, 3, 5, 5, 1, 2),     # 5x5 filter, five-slot ring
+    ConvShape(1, 21, 9, 40, 2, 3, 3, 3, 1),     # stride equal to the filter height
+    ConvShape(1, 21, 13, 48, 2, 3, 3, 4, 1),    # stride above the filter height
+    ConvShape(2, 192, 4, 12, 2, 1, 1, 1, 0),    # 1x1 filter, one-slot ring
+    ConvShape(1, 128, 3, 12, 2, 3, 3, 1, 1),    # two k ranges
 ]
 
 

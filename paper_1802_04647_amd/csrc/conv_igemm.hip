@@ -282,7 +282,7 @@ struct DmaLayout {
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP>
-__global__ __launch_bounds__(kThreads, 2) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
+__global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
     using MF = Mfma<T>;
@@ -417,46 +417,54 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_dma_kernel(IgemmArgs a
         const T *s_src = stage_src(st);
         const T *arow0 = stage_a(st) + (wm * 32 + (lane & 15)) * a.SA + (lane >> 4);
         const T *arow1 = arow0 + 16 * a.SA;
-        // Fragments are software-pipelined: the A/B fragments of k-step kk+4
-        // are read into their own registers while the MFMAs of step kk issue,
-        // so LDS latency overlaps the matrix pipe.  The tap offset of a step is
-        // computed arithmetically, so the B reads need no dependent LDS read.
+        // Fragments are software-pipelined in two register sets: the A/B
+        // fragments of step kk+4 are read while the MFMAs of step kk issue, so
+        // LDS latency overlaps the matrix pipe.  The empty asm with a memory
+        // clobber keeps the compiler from sinking a set's reads down to its
+        // MFMAs.  Reads past the last step land in the A slice's slack (in
+        // bounds, unused).  The tap offset of a step is computed
+        // arithmetically, so the B reads need no dependent LDS read.
+        // Steps past the chunk's last tap read tap KCv-1 instead: a finite value
+        // that meets a zero column of A, and no branch splits the loop body.
         auto tap_off = [&](int k) {
-            if (k >= KCv) return 0;
-            const int c = div_magic(k, a.magic_hw), t = k - c * a.HfWf;
+            const int kc = min(k, KCv - 1);
+            const int c = div_magic(kc, a.magic_hw), t = kc - c * a.HfWf;
             const int i = div_magic(t, a.magic_wf), j = t - i * a.Wf;
             return c * CHn + i * a.Wpad + j;
         };
-        T a0 = arow0[0], a1 = arow1[0];
-        T b[NB];
-        {
-            const int ko = tap_off(lane >> 4);
+        T a0[2], a1[2], b0[NB], b1[NB];
+        auto frag = [&](int kk, T &fa0, T &fa1, T (&fb)[NB]) {
+            fa0 = arow0[kk];
+            fa1 = arow1[kk];
+            const int ko = tap_off(kk + (lane >> 4));
 #pragma unroll
-            for (int y = 0; y < NB; ++y) b[y] = s_src[ko + lbase[y]];
-        }
-        for (int kk = 0; kk < a.KCK; kk += 4) {
-            // Unconditional, so no branch separates these reads from the MFMAs
-            // below; on the last step they read the A slice's slack and tap 0
-            // (in bounds, unused).
-            T nb[NB];
-            const T na0 = arow0[kk + 4], na1 = arow1[kk + 4];
-            {
-                const int ko = tap_off(kk + 4 + (lane >> 4));
-#pragma unroll
-                for (int y = 0; y < NB; ++y) nb[y] = s_src[ko + lbase[y]];
-            }
+            for (int y = 0; y < NB; ++y) fb[y] = s_src[ko + lbase[y]];
+        };
+        auto mma_step = [&](T fa0, T fa1, const T (&fb)[NB]) {
 #pragma unroll
             for (int y = 0; y < NB; ++y) {
-                const T bv = b[y];
+                const T bv = fb[y];
                 if (ZSKIP && wave_all_zero(bv)) continue;
-                acc[0][y] = MF::mma(a0, bv, acc[0][y]);
-                acc[1][y] = MF::mma(a1, bv, acc[1][y]);
+                acc[0][y] = MF::mma(fa0, bv, acc[0][y]);
+                acc[1][y] = MF::mma(fa1, bv, acc[1][y]);
             }
-            a0 = na0;
-            a1 = na1;
-#pragma unroll
-            for (int y = 0; y < NB; ++y) b[y] = nb[y];
+        };
+        frag(0, a0[0], a1[0], b0);
+        int kk = 0;
+        for (; kk + 4 < a.KCK; kk += 8) {
+            frag(kk + 4, a0[1], a1[1], b1);
+            mma_step(a0[0], a1[0], b0);
+            frag(kk + 8, a0[0], a1[0], b0);
+            mma_step(a0[1], a1[1], b1);
+            if (!ZSKIP) {
+                // Issue order: a set's reads, then the other set's MFMAs.
+                __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+            }
         }
+        if (kk < a.KCK) mma_step(a0[0], a1[0], b0);
         wait_dma();
         __syncthreads();
         st ^= 1;

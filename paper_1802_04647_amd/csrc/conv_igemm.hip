@@ -419,9 +419,9 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         const T *arow1 = arow0 + 16 * a.SA;
         // Fragments are software-pipelined in two register sets: the A/B
         // fragments of step kk+4 are read while the MFMAs of step kk issue, so
-        // LDS latency overlaps the matrix pipe.  The empty asm with a memory
-        // clobber keeps the compiler from sinking a set's reads down to its
-        // MFMAs.  Reads past the last step land in the A slice's slack (in
+        // LDS latency overlaps the matrix pipe.  sched_group_barrier pins that
+        // issue order (the scheduler would otherwise sink a set's reads down to
+        // its MFMAs).  Reads past the last step land in the A slice's slack (in
         // bounds, unused).  The tap offset of a step is computed
         // arithmetically, so the B reads need no dependent LDS read.
         // Steps past the chunk's last tap read tap KCv-1 instead: a finite value

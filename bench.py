@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_F64_MFMA = 78.6      # TFLOP/s, MI355X dense fp64 matrix
 PEAK_F32_MFMA = 157.3     # TFLOP/s, MI355X dense fp32 matrix
+PEAK_HBM_TBPS = 8.0       # TB/s, MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_hbm_traffic_resnet_fp64.txt")
 
 
@@ -36,7 +37,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
-    ap.add_argument("--only-f64", action="store_true", help="skip the fp32 and LeNet extras")
+    ap.add_argument("--only-f64", action="store_true",
+                    help="skip the fp32, LeNet, other-config and other-kernel extras")
     return ap.parse_args()
 
 
@@ -134,6 +136,146 @@ def lenet_timing(steps=50, warmup=10):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3))
+
+
+def _median_ms(fn, reps=20, warmup=3):
+    """Median over reps of HIP-event timings on the current stream."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    ts = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    return ts[len(ts) // 2]
+
+
+def conv_config_timing():
+    """Per-pass GFLOP/s of the LeNet conv layers (configs 2 and 3) in fp64 and fp32."""
+    import torch
+    from paper_1802_04647_amd import dmlnn
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    res = {}
+    for name in ("lenet_conv1", "lenet_conv2"):
+        s = SHAPES[name]
+        X0, W0, b0, dout0 = conv_layer_inputs(name)
+        if dout0.size != s.N * s.F * s.Hout * s.Wout:
+            # config 3's stored upstream gradient is the pooled one; the conv
+            # passes take one of the conv output's shape
+            import numpy as np
+            dout0 = np.random.default_rng(3).standard_normal((s.N, s.F * s.Hout * s.Wout))
+        res[name] = {}
+        for dtn, tdt, peak in (("f64", torch.float64, PEAK_F64_MFMA),
+                               ("f32", torch.float32, PEAK_F32_MFMA)):
+            dev = lambda v: torch.from_numpy(v).to(device="cuda", dtype=tdt)  # noqa: E731
+            X, W, b, dout = dev(X0), dev(W0), dev(b0), dev(dout0)
+            a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+            out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=tdt, device="cuda")
+            dW, db, dX = torch.empty_like(W), torch.empty_like(b), torch.empty_like(X)
+            ws = torch.empty(dmlnn.conv2d_backward_filter_workspace_size(tdt, *s.args()),
+                             dtype=torch.uint8, device="cuda")
+            dmlnn.conv2d_forward(X, W, b, *a, relu=True, out=out)
+            fns = {
+                "forward": lambda: dmlnn.conv2d_forward(X, W, b, *a, relu=True, out=out),
+                "backward_filter": lambda: dmlnn.conv2d_backward_filter(
+                    X, dout, out, *a, s.F, workspace=ws, dW=dW, db=db),
+                "backward_data": lambda: dmlnn.conv2d_backward_data(W, dout, out, *a, dX=dX),
+            }
+            flops = s.flops_per_pass()
+            res[name][dtn] = {}
+            for pname, fn in fns.items():
+                ms = _median_ms(fn)
+                tf = flops / (ms / 1e3) / 1e12
+                res[name][dtn][pname] = {"ms": round(ms, 4), "tflops": round(tf, 3),
+                                         "pct_of_mfma_peak": round(100 * tf / peak, 2)}
+    return res
+
+
+def aux_kernel_timing():
+    """HBM rate of the bandwidth-bound ops (bytes each operand moves once, over the
+    median launch time), and the affine GEMMs of the LeNet step in TFLOP/s."""
+    import torch
+    from paper_1802_04647_amd import dmlnn
+
+    f64 = torch.float64
+    res = {}
+
+    def hbm(name, nbytes, fn, note):
+        ms = _median_ms(fn)
+        gbps = nbytes / (ms / 1e3) / 1e9
+        res[name] = {"ms": round(ms, 4), "bytes": int(nbytes), "gbps": round(gbps, 1),
+                     "pct_of_hbm_peak": round(100 * gbps / (PEAK_HBM_TBPS * 1e3), 2),
+                     "shape": note}
+
+    g = torch.Generator(device="cuda").manual_seed(1802)
+    # bias_add_relu on the ResNet activation shape (256 x 64*56*56)
+    X = torch.randn((256, 64 * 3136), dtype=f64, device="cuda", generator=g)
+    b = torch.randn(64, dtype=f64, device="cuda", generator=g)
+    out = torch.empty_like(X)
+    hbm("bias_add_relu", 2 * X.numel() * 8 + 64 * 8,
+        lambda: dmlnn.bias_add_relu(X, b, 64, 3136, relu=True, out=out),
+        "256 x (64*56*56) fp64, separate output")
+    # max_pool2d 2x2/2 on the same activation
+    pout = torch.empty((256, 64 * 28 * 28), dtype=f64, device="cuda")
+    idx = torch.empty((256, 64 * 28 * 28), dtype=torch.int32, device="cuda")
+    hbm("max_pool2d_fwd", X.numel() * 8 + pout.numel() * 12,
+        lambda: dmlnn.max_pool2d_fwd(X, 64, 56, 56, 2, 2, 2, 0, out=pout, argmax=idx),
+        "256 x 64 x 56x56 -> 28x28, 2x2 stride 2, fp64 + int32 argmax")
+    dX = torch.empty_like(X)
+    hbm("max_pool2d_bwd", pout.numel() * 12 + X.numel() * 8,
+        lambda: dmlnn.max_pool2d_bwd(pout, idx, 64, 56, 56, 2, 2, 2, 0, dX=dX),
+        "256 x 64 x 28x28 -> 56x56 gather, fp64")
+    del X, out, pout, idx, dX
+    # LeNet pool2 (config 3): latency-bound size
+    Xs = torch.randn((64, 64 * 196), dtype=f64, device="cuda", generator=g)
+    ps = torch.empty((64, 64 * 49), dtype=f64, device="cuda")
+    ids = torch.empty((64, 64 * 49), dtype=torch.int32, device="cuda")
+    hbm("max_pool2d_fwd_lenet", Xs.numel() * 8 + ps.numel() * 12,
+        lambda: dmlnn.max_pool2d_fwd(Xs, 64, 14, 14, 2, 2, 2, 0, out=ps, argmax=ids),
+        "64 x 64 x 14x14 -> 7x7 (config 3), fp64")
+    # SGD-momentum over the LeNet parameter count (config 4)
+    n = 1663370
+    th = torch.randn(n, dtype=f64, device="cuda", generator=g)
+    gr = torch.randn(n, dtype=f64, device="cuda", generator=g)
+    v = torch.zeros(n, dtype=f64, device="cuda")
+    hbm("sgd_momentum_update", 5 * n * 8,
+        lambda: dmlnn.sgd_momentum_update(th, gr, v, 0.01, 0.9),
+        "1,663,370 fp64 parameters (LeNet), theta/grad/v read, theta/v written")
+    # softmax + cross-entropy (config 4)
+    S = torch.randn((64, 10), dtype=f64, device="cuda", generator=g)
+    Y = torch.zeros((64, 10), dtype=f64, device="cuda")
+    Y[torch.arange(64), torch.arange(64) % 10] = 1.0
+    loss = torch.empty(1, dtype=f64, device="cuda")
+    dS = torch.empty_like(S)
+    P = torch.empty_like(S)
+    hbm("softmax_xent", 4 * S.numel() * 8 + 8,
+        lambda: dmlnn.softmax_xent(S, Y, loss=loss, dscores=dS, probs=P),
+        "64 x 10 fp64 (config 4): latency-bound")
+    # affine 3136 -> 512 of the LeNet step (config 4), fp64 MFMA
+    A = torch.randn((64, 3136), dtype=f64, device="cuda", generator=g)
+    Wa = torch.randn((3136, 512), dtype=f64, device="cuda", generator=g) * 0.02
+    ba = torch.zeros(512, dtype=f64, device="cuda")
+    oa = torch.empty((64, 512), dtype=f64, device="cuda")
+    dA, dWa, dba = torch.empty_like(A), torch.empty_like(Wa), torch.empty_like(ba)
+    go = torch.randn((64, 512), dtype=f64, device="cuda", generator=g)
+    dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa)
+    for nm, fn, fl in (("affine_fwd", lambda: dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa),
+                        2 * 64 * 3136 * 512),
+                       ("affine_bwd", lambda: dmlnn.affine_bwd(go, A, Wa, out_fwd=oa, dX=dA,
+                                                               dW=dWa, db=dba),
+                        2 * 2 * 64 * 3136 * 512)):
+        ms = _median_ms(fn)
+        tf = fl / (ms / 1e3) / 1e12
+        res[nm] = {"ms": round(ms, 4), "tflops": round(tf, 3),
+                   "pct_of_fp64_mfma_peak": round(100 * tf / PEAK_F64_MFMA, 2),
+                   "shape": "64 x 3136 . 3136 x 512 fp64 (config 4)"}
+    return res
 
 
 def copy_calibration(nbytes=1 << 30, reps=5):
@@ -253,6 +395,8 @@ def main():
         rec["lenet_training"] = {"batch": 64, "dtype": "f64",
                                  "ms_per_step": round(lt["ms_per_step"], 4),
                                  "images_per_s": round(lt["images_per_s"], 1)}
+        rec["conv_configs"] = conv_config_timing()
+        rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)

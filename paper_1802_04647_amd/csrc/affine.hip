@@ -6,19 +6,20 @@
 //   dX = g W^T                    (A = g,        B = W viewed transposed)
 //   dW = X^T g                    (A = X viewed transposed, B = g)
 // where g = dout masked to out_fwd > 0 when a relu mask is given; the mask is
-// applied while the operand tile is staged.  A block owns a 32 x 32 output tile;
-// its 4 waves each take every 4th 4-deep k-step of a staged K-chunk (2 x 2
-// MFMAs per step), and the four partial tiles are added in wave order at the
-// end (deterministic).  Column sums of g (db) use a separate fixed-order kernel.
+// applied as the operand is loaded.  A block owns a 16 x 16 output tile and up
+// to 16 waves that split K (one MFMA per 4-deep k-step); their partial tiles
+// are added in wave order (deterministic).  Column sums of g (db) use a
+// separate fixed-order kernel.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace dmlnn {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kT = 32;    // output tile edge
-constexpr int kKC = 64;   // k per staged chunk
+constexpr int kTJ = 16;      // output tile columns
+constexpr int kMaxKW = 16;   // waves splitting K inside a block
 
 struct GemmArgs {
     const void *A, *Amask;  // A(i,k) = A[i*sAm + k*sAk]; mask has the same strides
@@ -27,117 +28,147 @@ struct GemmArgs {
     void *C;                // C[i*ldc + j]
     long long sAm, sAk, sBk, sBn, ldc;
     int M, N, K, relu;
+    int kw_len;             // k per wave (a multiple of 4)
 };
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g)
+// A block owns a (16 TM) x 16 output tile (each B fragment feeds TM MFMAs, so B
+// is read once per 16 TM rows); its waves split K into contiguous ranges
+// of kw_len and read their MFMA fragments straight from global memory (the
+// products here have at most a few MB of operands, which stay in L2).  The
+// per-wave partial tiles are added in wave order (deterministic).  Rows and
+// columns past the matrix edge read a clamped (valid) row or column: they only
+// feed outputs that are not stored.  The main loop takes whole batches of kU
+// steps with no k test, so its loads issue back to back; the tail zeroes k
+// past the wave's range.  MA / MB: A / B carries a relu mask.
+template <typename T, bool MA, bool MB, int kTM>
+__global__ __launch_bounds__(kMaxKW * kWave) void gemm_kernel(GemmArgs g)
 {
     using MF = Mfma<T>;
-    // operand tiles during the K loop; the four per-wave partial tiles afterwards
-    constexpr int kStage = kT * (kKC + 1) + kKC * (kT + 1);
-    constexpr int kWords = kStage > 4 * kT * kT ? kStage : 4 * kT * kT;
-    __shared__ T smem[kWords];
-    T(*s_a)[kKC + 1] = reinterpret_cast<T(*)[kKC + 1]>(smem);
-    T(*s_b)[kT + 1] = reinterpret_cast<T(*)[kT + 1]>(smem + kT * (kKC + 1));
-    T(*s_red)[kT * kT] = reinterpret_cast<T(*)[kT * kT]>(smem);
+    constexpr int kTI = 16 * kTM;
+    constexpr int kU = kTM == 1 ? 8 : 4;  // 4-deep k-steps loaded before their MFMAs
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_red = reinterpret_cast<T *>(smem);  // [wave][kTI * kTJ]
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-    const int i0 = blockIdx.x * kT, j0 = blockIdx.y * kT;
+    const int nw = blockDim.x / kWave;
+    const int i0 = blockIdx.x * kTI, j0 = blockIdx.y * kTJ;
+    const int kbeg = wave * g.kw_len, kend = min(g.K, kbeg + g.kw_len);
     const T *A = reinterpret_cast<const T *>(g.A);
     const T *Am = reinterpret_cast<const T *>(g.Amask);
     const T *B = reinterpret_cast<const T *>(g.B);
     const T *Bm = reinterpret_cast<const T *>(g.Bmask);
+    const int li = lane & 15, lk = lane >> 4;
+    long long arow[kTM];
+#pragma unroll
+    for (int x = 0; x < kTM; ++x) arow[x] = (long long)min(i0 + 16 * x + li, g.M - 1) * g.sAm;
+    const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
 
-    typename MF::acc_t acc[2][2];
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = MF::zero();
+    auto ldA = [&](int x, int k) -> T {
+        const long long o = arow[x] + (long long)k * g.sAk;
+        const T v = A[o];
+        if (MA) return Am[o] > T(0) ? v : T(0);
+        return v;
+    };
+    auto ldB = [&](int k) -> T {
+        const long long o = (long long)k * g.sBk + bcol;
+        const T v = B[o];
+        if (MB) return Bm[o] > T(0) ? v : T(0);
+        return v;
+    };
 
-    for (int k0 = 0; k0 < g.K; k0 += kKC) {
-        __syncthreads();
-        for (int e = tid; e < kT * kKC; e += kThreads) {
-            // A tile: rows i, columns k (k fastest when A is k-contiguous)
-            int r, c;
-            if (g.sAk == 1) { r = e / kKC; c = e % kKC; } else { c = e / kT; r = e % kT; }
-            int i = i0 + r, k = k0 + c;
-            T v = T(0);
-            if (i < g.M && k < g.K) {
-                long long o = (long long)i * g.sAm + (long long)k * g.sAk;
-                v = A[o];
-                if (Am && !(Am[o] > T(0))) v = T(0);
-            }
-            s_a[r][c] = v;
-        }
-        for (int e = tid; e < kT * kKC; e += kThreads) {
-            int r, c;  // r = k row, c = j column
-            if (g.sBn == 1) { r = e / kT; c = e % kT; } else { c = e / kKC; r = e % kKC; }
-            int k = k0 + r, j = j0 + c;
-            T v = T(0);
-            if (k < g.K && j < g.N) {
-                long long o = (long long)k * g.sBk + (long long)j * g.sBn;
-                v = B[o];
-                if (Bm && !(Bm[o] > T(0))) v = T(0);
-            }
-            s_b[r][c] = v;
-        }
-        __syncthreads();
+    typename MF::acc_t acc[kTM];
 #pragma unroll
-        for (int st = 0; st < kKC / 4 / 4; ++st) {
-            const int kk = (st * 4 + wave) * 4 + (lane >> 4);
-            T a0 = s_a[lane & 15][kk], a1 = s_a[16 + (lane & 15)][kk];
-            T b0 = s_b[kk][lane & 15], b1 = s_b[kk][16 + (lane & 15)];
-            acc[0][0] = MF::mma(a0, b0, acc[0][0]);
-            acc[0][1] = MF::mma(a0, b1, acc[0][1]);
-            acc[1][0] = MF::mma(a1, b0, acc[1][0]);
-            acc[1][1] = MF::mma(a1, b1, acc[1][1]);
+    for (int x = 0; x < kTM; ++x) acc[x] = MF::zero();
+    int kk = kbeg;
+    for (; kk + 4 * kU <= kend; kk += 4 * kU) {
+        T a[kU][kTM], b[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+#pragma unroll
+            for (int x = 0; x < kTM; ++x) a[u][x] = ldA(x, kk + 4 * u + lk);
+            b[u] = ldB(kk + 4 * u + lk);
         }
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+            for (int x = 0; x < kTM; ++x) acc[x] = MF::mma(a[u][x], b[u], acc[x]);
+    }
+    for (; kk < kend; kk += 4) {
+        const int k = kk + lk;
+        const int kc = min(k, kend - 1);
+        T b = ldB(kc);
+        b = k < kend ? b : T(0);
+#pragma unroll
+        for (int x = 0; x < kTM; ++x) acc[x] = MF::mma(ldA(x, kc), b, acc[x]);
     }
 
-    __syncthreads();
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < kTM; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                int i = x * 16 + MF::row(lane, r), j = y * 16 + (lane & 15);
-                s_red[wave][i * kT + j] = acc[x][y][r];
-            }
+        for (int r = 0; r < 4; ++r)
+            s_red[wave * kTI * kTJ + (16 * x + MF::row(lane, r)) * kTJ + li] = acc[x][r];
     __syncthreads();
     T *C = reinterpret_cast<T *>(g.C);
     const T *bias = reinterpret_cast<const T *>(g.bias);
-    for (int e = tid; e < kT * kT; e += kThreads) {
-        int i = i0 + e / kT, j = j0 + e % kT;
+    for (int e = tid; e < kTI * kTJ; e += blockDim.x) {
+        const int i = i0 + e / kTJ, j = j0 + e % kTJ;
         if (i < g.M && j < g.N) {
-            T v = ((s_red[0][e] + s_red[1][e]) + s_red[2][e]) + s_red[3][e];
+            T v = s_red[e];
+            for (int w = 1; w < nw; ++w) v += s_red[w * kTI * kTJ + e];
             if (bias) v += bias[j];
             C[(long long)i * g.ldc + j] = relu_if(v, g.relu);
         }
     }
 }
 
-// db[j] = sum_i g[i, j] (rows in order), g masked by out_fwd > 0 if given.
+// db[j] = sum_i g[i, j], g masked by out_fwd > 0 if given.  A block covers 16
+// columns with 16 row phases each: thread (j, ph) sums rows ph, ph+16, ... in
+// order, and the 16 phase sums are added in phase order (deterministic).
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_kernel(const T *G, const T *mask, T *db, int N,
                                                      int M)
 {
-    const int j = blockIdx.x * 256 + threadIdx.x;
-    if (j >= M) return;
+    __shared__ T s_part[16][17];
+    const int jl = threadIdx.x & 15, ph = threadIdx.x >> 4;
+    const int j = blockIdx.x * 16 + jl;
     T s = T(0);
-    for (int i = 0; i < N; ++i) {
-        T v = G[(size_t)i * M + j];
-        if (mask && !(mask[(size_t)i * M + j] > T(0))) v = T(0);
-        s += v;
+    if (j < M)
+        for (int i = ph; i < N; i += 16) {
+            T v = G[(size_t)i * M + j];
+            if (mask && !(mask[(size_t)i * M + j] > T(0))) v = T(0);
+            s += v;
+        }
+    s_part[ph][jl] = s;
+    __syncthreads();
+    if (ph == 0 && j < M) {
+        T t = s_part[0][jl];
+        for (int q = 1; q < 16; ++q) t += s_part[q][jl];
+        db[j] = t;
     }
-    db[j] = s;
 }
 
+// Waves per block: about 128 k each, at most 16 (a power of two).
 template <typename T>
-hipError_t gemm(const GemmArgs &g, hipStream_t s)
+hipError_t gemm(GemmArgs g, hipStream_t s)
 {
-    dim3 grid((g.M + kT - 1) / kT, (g.N + kT - 1) / kT);
-    hipLaunchKernelGGL(gemm_kernel<T>, grid, dim3(kThreads), 0, s, g);
+    int nw = 1;
+    while (nw < kMaxKW && 2 * nw * 128 <= g.K) nw <<= 1;
+    g.kw_len = ((g.K + nw - 1) / nw + 3) / 4 * 4;
+    // 64-row tiles when that still leaves at least 128 blocks, else 16-row tiles
+    const bool tall = (long long)((g.M + 63) / 64) * ((g.N + kTJ - 1) / kTJ) >= 128;
+    const int kTI = tall ? 64 : 16;
+    const size_t lds = (size_t)nw * kTI * kTJ * sizeof(T);
+    auto pick = [&](auto tm) {
+        constexpr int TM = decltype(tm)::value;
+        return g.Amask ? (g.Bmask ? gemm_kernel<T, true, true, TM> : gemm_kernel<T, true, false, TM>)
+                       : (g.Bmask ? gemm_kernel<T, false, true, TM>
+                                  : gemm_kernel<T, false, false, TM>);
+    };
+    auto k = tall ? pick(std::integral_constant<int, 4>()) : pick(std::integral_constant<int, 1>());
+    hipError_t e = allow_dynamic_lds(k, lds);
+    if (e != hipSuccess) return e;
+    dim3 grid((g.M + kTI - 1) / kTI, (g.N + kTJ - 1) / kTJ);
+    hipLaunchKernelGGL(k, grid, dim3(nw * kWave), lds, s, g);
     return hipGetLastError();
 }
 
@@ -203,7 +234,7 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
         if (e != hipSuccess) return e;
     }
     if (db) {
-        dim3 grid((M + 255) / 256);
+        dim3 grid((M + 15) / 16);
         if (dtype == 0)
             hipLaunchKernelGGL(colsum_kernel<double>, grid, dim3(256), 0, s, (const double *)dout,
                                (const double *)out_fwd, (double *)db, N, M);

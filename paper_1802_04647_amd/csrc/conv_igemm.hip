@@ -49,6 +49,8 @@ struct IgemmArgs {
     int KC, KCK;
     int Wpad, CH, SA;
     int pipelined;  // 1: chunk fits the per-thread staging registers
+    int ksplit;     // LDS-DMA kernel, M <= 32: the two m-halves of waves split the
+                    // k-steps of the same 32 rows instead of taking 32 rows each
     unsigned long long magic_kck, magic_hw, magic_wf;
 };
 
@@ -281,7 +283,7 @@ struct DmaLayout {
                                           // has 256 bytes of slack
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool KS>
 __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
@@ -415,7 +417,8 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         if (c0 + a.KC < a.Cs) issue(st ^ 1, c0 + a.KC);
 
         const T *s_src = stage_src(st);
-        const T *arow0 = stage_a(st) + (wm * 32 + (lane & 15)) * a.SA + (lane >> 4);
+        const int mrow = KS ? 0 : wm * 32;
+        const T *arow0 = stage_a(st) + (mrow + (lane & 15)) * a.SA + (lane >> 4);
         const T *arow1 = arow0 + 16 * a.SA;
         // Fragments are software-pipelined in two register sets: the A/B
         // fragments of step kk+4 are read while the MFMAs of step kk issue, so
@@ -449,12 +452,14 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
                 acc[1][y] = MF::mma(fa1, bv, acc[1][y]);
             }
         };
-        frag(0, a0[0], a1[0], b0);
-        int kk = 0;
-        for (; kk + 4 < a.KCK; kk += 8) {
-            frag(kk + 4, a0[1], a1[1], b1);
+        // With ksplit, wave half wm takes the steps kk = 4*wm, 4*wm + 8, ...
+        const int kstep = KS ? 8 : 4;
+        int kk = KS ? 4 * wm : 0;
+        frag(kk, a0[0], a1[0], b0);
+        for (; kk + kstep < a.KCK; kk += 2 * kstep) {
+            frag(kk + kstep, a0[1], a1[1], b1);
             mma_step(a0[0], a1[0], b0);
-            frag(kk + 8, a0[0], a1[0], b0);
+            frag(kk + 2 * kstep, a0[0], a1[0], b0);
             mma_step(a0[1], a1[1], b1);
             if (!ZSKIP) {
                 // Issue order: a set's reads, then the other set's MFMAs.
@@ -470,6 +475,29 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         st ^= 1;
     }
 
+    if (KS) {
+        // Waves wm = 1 hand their partial tiles to the waves wm = 0 of the same
+        // columns, which add them (fixed order) and store.  The stages are free:
+        // every wave has passed the last chunk's barrier.
+        T *s_red = reinterpret_cast<T *>(smem);
+        if (wm == 1)
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < NB; ++y)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        s_red[(((wn * 2 + x) * NB + y) * 4 + r) * kWave + lane] = acc[x][y][r];
+        __syncthreads();
+        if (wm == 1) return;
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < NB; ++y)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    acc[x][y][r] += s_red[(((wn * 2 + x) * NB + y) * 4 + r) * kWave + lane];
+    }
     T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
     const T *bias = reinterpret_cast<const T *>(a.bias);
 #pragma unroll
@@ -478,7 +506,7 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         for (int y = 0; y < NB; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                int m = m0 + wm * 32 + x * 16 + MF::row(lane, r);
+                int m = m0 + (KS ? 0 : wm * 32) + x * 16 + MF::row(lane, r);
                 int q = q0 + (wn * NB + y) * 16 + (lane & 15);
                 if (m < a.M && q < qend) {
                     T v = acc[x][y][r];
@@ -594,22 +622,30 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
     return false;
 }
 
-template <typename T, int NB, bool BWD>
-hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
-                      int nimg, int zero_skip, hipStream_t s)
+template <typename T, int NB, bool BWD, bool KS>
+hipError_t launch_dma_ks(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
+                         int nimg, int zero_skip, hipStream_t s)
 {
     dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
     hipError_t e;
     if (zero_skip) {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, true>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     } else {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, false>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     }
     return hipGetLastError();
+}
+
+template <typename T, int NB, bool BWD>
+hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
+                      int nimg, int zero_skip, hipStream_t s)
+{
+    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true>(a, p, L, w_bytes, nimg, zero_skip, s);
+    return launch_dma_ks<T, NB, BWD, false>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
 
 template <typename T, int NB, bool BWD>
@@ -661,6 +697,11 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         ad.KC = pd.KC;
         ad.KCK = pd.KCK;
         ad.SA = pd.SA;
+        ad.ksplit = M <= 32;
+        if (ad.ksplit) {  // the partial-tile hand-over reuses the stages
+            const size_t red = sizeof(T) * (size_t)2 * 2 * pd.NB * 4 * kWave;
+            if (pd.lds < red) pd.lds = red;
+        }
         switch (pd.NB) {
         case 7: return launch_dma<T, 7, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
         case 4: return launch_dma<T, 4, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);

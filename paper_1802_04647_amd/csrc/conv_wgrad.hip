@@ -29,6 +29,7 @@ constexpr size_t kLdsBudget = 72 * 1024;
 // Upper bound on resident blocks (256 CUs x 4 blocks) used to size the workspace
 // without a device; the launch uses the measured occupancy, up to this bound.
 constexpr int kMaxResident = 1024;
+constexpr int kMinTiles = 4;  // fewest pixel tiles a split reduces
 constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
 constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
 
@@ -292,23 +293,33 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     }
 }
 
-// dW[e] = sum over splits of the partials, in split order (double accumulation);
-// the last F threads do the same for db.
+// dW[e] (e < FK) and db[f] (e = FK + f) = sum over splits of the partials.  A
+// block covers 16 outputs with 16 split phases each: thread (e, ph) sums splits
+// ph, ph+16, ... in order (double accumulation), and the 16 phase sums are added
+// in phase order, so the result depends only on the split count.
 template <typename T>
 __global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *db, int FK, int F,
                                                          int splits)
 {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e < FK) {
-        double s = 0.0;
-        for (int sp = 0; sp < splits; ++sp) s += (double)ws[(size_t)sp * FK + e];
-        dW[e] = (T)s;
-    } else if (db && e < FK + F) {
-        const int f = e - FK;
-        const T *wsdb = ws + (size_t)splits * FK;
-        double s = 0.0;
-        for (int sp = 0; sp < splits; ++sp) s += (double)wsdb[(size_t)sp * F + f];
-        db[f] = (T)s;
+    __shared__ double s_part[16][17];
+    const int el = threadIdx.x & 15, ph = threadIdx.x >> 4;
+    const int e = blockIdx.x * 16 + el;
+    const int total = FK + (db ? F : 0);
+    double sum = 0.0;
+    if (e < total) {
+        const T *base = e < FK ? ws + e : ws + (size_t)splits * FK + (e - FK);
+        const size_t stride = e < FK ? (size_t)FK : (size_t)F;
+        for (int sp = ph; sp < splits; sp += 16) sum += (double)base[(size_t)sp * stride];
+    }
+    s_part[ph][el] = sum;
+    __syncthreads();
+    if (ph == 0 && e < total) {
+        double t = s_part[0][el];
+        for (int q = 1; q < 16; ++q) t += s_part[q][el];
+        if (e < FK)
+            dW[e] = (T)t;
+        else
+            db[e - FK] = (T)t;
     }
 }
 
@@ -677,6 +688,8 @@ hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStrea
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
     int splits = resident_slots(k, kRingThreads, p.lds) / per_split;
+    const long long cap = p.T_total / kMinTiles;
+    if (splits > cap) splits = (int)cap;
     if (splits < 1) splits = 1;
     if (splits > p.splits) splits = p.splits;
     a.splits = splits;
@@ -685,7 +698,7 @@ hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStrea
     if (e != hipSuccess) return e;
     const int FK = a.F * a.K;
     const int total = FK + (db ? a.F : 0);
-    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 255) / 256), dim3(256), 0, s,
+    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 15) / 16), dim3(256), 0, s,
                        reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
                        reinterpret_cast<T *>(db), FK, a.F, a.splits);
     return hipGetLastError();
@@ -703,6 +716,10 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
     const int per_split = p.nkr * p.nft;
     int slots = resident_slots(k, kThreads, p.lds);
     int splits = slots / per_split;
+    // at least kMinTiles tiles per split: tiny layers would otherwise spend their
+    // time in block start-up and in the split reduction
+    const long long cap = p.T_total / kMinTiles;
+    if (splits > cap) splits = (int)cap;
     if (splits < 1) splits = 1;
     if (splits > p.splits) splits = p.splits;
     a.splits = splits;
@@ -712,7 +729,7 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
     if (e != hipSuccess) return e;
     const int FK = a.F * a.K;
     const int total = FK + (db ? a.F : 0);
-    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 255) / 256), dim3(256), 0, s,
+    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 15) / 16), dim3(256), 0, s,
                        reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
                        reinterpret_cast<T *>(db), FK, a.F, a.splits);
     return hipGetLastError();

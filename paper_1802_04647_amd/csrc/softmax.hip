@@ -4,68 +4,86 @@
 //   p = exp(s - m) / sum exp(s - m)
 //   row loss = -sum_k y (s - m - log sum exp(s - m))
 //   ds = (p * sum_k y - y) / N
-// and loss = (1/N) * sum of row losses.  One block; wave w takes rows w, w+4, ...
-// with lanes across the K columns and butterfly-shuffle reductions; the four wave
-// totals are added in wave order, so the loss is deterministic.
+// and loss = (1/N) * sum of row losses.  One block of 16 waves; lanes run across
+// the K columns of a row with butterfly-shuffle reductions.
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace dmlnn {
 namespace {
 
+// Rows are processed by lane segments of width sw (a power of two >= K, at most
+// 64): a wave holds 64/sw rows at once and the 16 waves of the block take
+// consecutive row groups.  Per-row losses are summed per segment in row order,
+// then over (wave, segment) in order: the loss is deterministic.
 template <typename T>
-__device__ __forceinline__ T wave_sum(T v)
+__device__ __forceinline__ T seg_sum(T v, int sw)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    for (int off = sw >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
     return v;
 }
 
 template <typename T>
-__device__ __forceinline__ T wave_max(T v)
+__device__ __forceinline__ T seg_max(T v, int sw)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
+    for (int off = sw >> 1; off > 0; off >>= 1) {
         T o = __shfl_xor(v, off, kWave);
         v = o > v ? o : v;
     }
     return v;
 }
 
+constexpr int kSmThreads = 1024;
+constexpr int kSmWaves = kSmThreads / kWave;
+
 template <typename T>
-__global__ __launch_bounds__(256) void softmax_xent_kernel(const T *S, const T *Y, T *P, T *dS,
-                                                           T *loss, int N, int K)
+__global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, const T *Y, T *P,
+                                                                  T *dS, T *loss, int N, int K,
+                                                                  int sw)
 {
-    __shared__ T s_tot[4];
+    __shared__ T s_part[kSmThreads];
     const int lane = lane_id(), wave = wave_id();
+    const int rpw = kWave / sw, seg = lane / sw, sl = lane - seg * sw;
     const T invN = T(1) / T(N);
     T total = T(0);
-    for (int n = wave; n < N; n += 4) {
+    for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
+        const int n = r0 + seg;
+        const bool ok = n < N;
         const T *s = S + (size_t)n * K;
         const T *y = Y + (size_t)n * K;
         T m = -INFINITY;
-        for (int k = lane; k < K; k += kWave) m = s[k] > m ? s[k] : m;
-        m = wave_max(m);
+        if (ok)
+            for (int k = sl; k < K; k += sw) m = s[k] > m ? s[k] : m;
+        m = seg_max(m, sw);
         T se = T(0), ys = T(0);
-        for (int k = lane; k < K; k += kWave) {
-            se += exp(s[k] - m);
-            ys += y[k];
-        }
-        se = wave_sum(se);
-        ys = wave_sum(ys);
+        if (ok)
+            for (int k = sl; k < K; k += sw) {
+                se += exp(s[k] - m);
+                ys += y[k];
+            }
+        se = seg_sum(se, sw);
+        ys = seg_sum(ys, sw);
         const T lse = m + log(se);
         T rl = T(0);
-        for (int k = lane; k < K; k += kWave) {
-            const T p = exp(s[k] - m) / se;
-            if (P) P[(size_t)n * K + k] = p;
-            dS[(size_t)n * K + k] = (p * ys - y[k]) * invN;
-            rl -= y[k] * (s[k] - lse);
-        }
-        total += wave_sum(rl);
+        if (ok)
+            for (int k = sl; k < K; k += sw) {
+                const T sk = s[k], yk = y[k];
+                const T p = exp(sk - m) / se;
+                if (P) P[(size_t)n * K + k] = p;
+                dS[(size_t)n * K + k] = (p * ys - yk) * invN;
+                rl -= yk * (sk - lse);
+            }
+        rl = seg_sum(rl, sw);
+        if (ok) total += rl;
     }
-    if (lane == 0) s_tot[wave] = total;
+    s_part[threadIdx.x] = total;
     __syncthreads();
-    if (threadIdx.x == 0) *loss = (((s_tot[0] + s_tot[1]) + s_tot[2]) + s_tot[3]) * invN;
+    if (threadIdx.x == 0) {
+        T t = T(0);
+        for (int w = 0; w < kSmWaves; ++w)
+            for (int g = 0; g < rpw; ++g) t += s_part[w * kWave + g * sw];
+        *loss = t * invN;
+    }
 }
 
 }  // namespace
@@ -73,13 +91,16 @@ __global__ __launch_bounds__(256) void softmax_xent_kernel(const T *S, const T *
 hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
                                void *loss, int N, int K, hipStream_t s)
 {
+    int sw = 1;
+    while (sw < K && sw < kWave) sw <<= 1;
     if (dtype == 0)
-        hipLaunchKernelGGL(softmax_xent_kernel<double>, dim3(1), dim3(256), 0, s,
+        hipLaunchKernelGGL(softmax_xent_kernel<double>, dim3(1), dim3(kSmThreads), 0, s,
                            (const double *)S, (const double *)Y, (double *)P, (double *)dS,
-                           (double *)loss, N, K);
+                           (double *)loss, N, K, sw);
     else
-        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3(1), dim3(256), 0, s, (const float *)S,
-                           (const float *)Y, (float *)P, (float *)dS, (float *)loss, N, K);
+        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3(1), dim3(kSmThreads), 0, s,
+                           (const float *)S, (const float *)Y, (float *)P, (float *)dS,
+                           (float *)loss, N, K, sw);
     return hipGetLastError();
 }
 

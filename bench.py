@@ -155,6 +155,23 @@ def _median_ms(fn, reps=20, warmup=3):
     return ts[len(ts) // 2]
 
 
+def scoring_timing(M=4096):
+    """Forward-only LeNet scoring of M images in batches of 64, on 1 and 4 streams."""
+    import torch
+    from paper_1802_04647_amd.inputs import lenet_train_inputs, sparse_uniform, streams
+    from paper_1802_04647_amd.lenet import LeNetScorer
+
+    _, _, params = lenet_train_inputs()
+    g_x, g_mask = streams(977)[:2]
+    X = torch.from_numpy(sparse_uniform(g_mask, g_x, (M, 784), keep=0.2)).cuda()
+    res = {"images": M, "batch": 64, "dtype": "f64"}
+    for ns in (1, 4):
+        sc = LeNetScorer(params, batch=64, streams=ns)
+        ms = _median_ms(lambda: sc.score(X), reps=5, warmup=2)
+        res[f"streams_{ns}"] = {"ms": round(ms, 3), "images_per_s": round(M / (ms / 1e3), 1)}
+    return res
+
+
 def conv_config_timing():
     """Per-pass GFLOP/s of the LeNet conv layers (configs 2 and 3) in fp64 and fp32."""
     import torch
@@ -395,6 +412,7 @@ def main():
         rec["lenet_training"] = {"batch": 64, "dtype": "f64",
                                  "ms_per_step": round(lt["ms_per_step"], 4),
                                  "images_per_s": round(lt["images_per_s"], 1)}
+        rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
         rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:

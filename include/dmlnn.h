@@ -174,6 +174,14 @@ DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, con
 DMLNN_API int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *probs,
                  void *dscores, void *loss, int N, int K, void *stream);
 
+/* ------------------------------------------------------------- softmax_fwd ----
+ * Paper: Section 2 listing (probs = softmax::forward(scores)), used alone for
+ * forward-only scoring.  Row-wise, max-shifted:
+ *   probs[n,k] = exp(scores[n,k] - max_k scores[n,:]) / sum_k exp(...)
+ * scores and probs are N x K (probs may not alias scores). */
+DMLNN_API int softmax_fwd(dmlnn_dtype dtype, const void *scores, void *probs, int N, int K,
+                          void *stream);
+
 /* ---------------------------------------------------- sgd_momentum_update ----
  * Paper: Section 2 (SGD with momentum is one of the NN library's optimizers;
  * the listing's plain SGD is W - lr*dW, the case mu = 0).
@@ -181,6 +189,45 @@ DMLNN_API int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y,
  * theta, grad and v hold n elements. */
 DMLNN_API int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v,
                         double lr, double mu, long long n, void *stream);
+
+/* ------------------------------------------------------------ optimizers ----
+ * Paper: Section 2, "NN Library" (the library ships six optimizers: Adagrad,
+ * Adam, RMSprop, SGD, SGD with momentum, SGD with Nesterov momentum).  The
+ * paper names them without formulas; each update below is the published
+ * method's usual statement (see the per-call comments).  All are elementwise
+ * and in place over n elements of dtype; theta, grad and the state buffers are
+ * caller-owned device memory, the state starts at zero and persists between
+ * calls; arithmetic is done in dtype.  Returns DMLNN_ERR_NULL for a missing
+ * buffer and DMLNN_ERR_ARG for n outside [1, INT_MAX] or a hyper-parameter
+ * outside its stated range; nothing is launched then. */
+
+/* Plain SGD (the paper's softmax-classifier listing: W = W - lr*dW):
+ *   theta <- theta - lr*grad */
+DMLNN_API int sgd_update(dmlnn_dtype dtype, void *theta, const void *grad, double lr,
+                         long long n, void *stream);
+
+/* SGD with Nesterov momentum, in the form that keeps the current parameters:
+ *   v' = mu*v - lr*grad;  theta <- theta - mu*v + (1 + mu)*v';  v <- v' */
+DMLNN_API int sgd_nesterov_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v,
+                                  double lr, double mu, long long n, void *stream);
+
+/* Adagrad: cache <- cache + grad^2;  theta <- theta - lr*grad / (sqrt(cache) + eps).
+ * eps >= 0. */
+DMLNN_API int adagrad_update(dmlnn_dtype dtype, void *theta, const void *grad, void *cache,
+                             double lr, double eps, long long n, void *stream);
+
+/* RMSprop: cache <- decay*cache + (1 - decay)*grad^2;
+ *          theta <- theta - lr*grad / (sqrt(cache) + eps).   0 <= decay <= 1, eps >= 0. */
+DMLNN_API int rmsprop_update(dmlnn_dtype dtype, void *theta, const void *grad, void *cache,
+                             double lr, double decay, double eps, long long n, void *stream);
+
+/* Adam, step t >= 1 (the caller counts steps from 1):
+ *   m <- beta1*m + (1 - beta1)*grad;  v <- beta2*v + (1 - beta2)*grad^2;
+ *   theta <- theta - lr_t * m / (sqrt(v) + eps),  lr_t = lr*sqrt(1 - beta2^t)/(1 - beta1^t)
+ * (the bias correction folded into the step size).  0 <= beta1, beta2 < 1, eps >= 0. */
+DMLNN_API int adam_update(dmlnn_dtype dtype, void *theta, const void *grad, void *m, void *v,
+                          double lr, double beta1, double beta2, double eps, long long t,
+                          long long n, void *stream);
 
 /* --------------------------------------------------------- count_nonzero ----
  * Paper: Section 3, "Sparse Operations" (the number of non-zeros of every

@@ -72,6 +72,15 @@ def _load():
         "oracle_xent_forward": (ctypes.c_double, [_d, _d, _int, _int]),
         "oracle_xent_backward": (None, [_d, _d, _d, _int, _int]),
         "oracle_softmax_backward": (None, [_d, _d, _d, _int, _int]),
+        "oracle_sgd_update": (None, [_d, _d, ctypes.c_double, ctypes.c_longlong]),
+        "oracle_sgd_nesterov_update": (None, [_d, _d, _d, ctypes.c_double, ctypes.c_double,
+                                              ctypes.c_longlong]),
+        "oracle_adagrad_update": (None, [_d, _d, _d, ctypes.c_double, ctypes.c_double,
+                                         ctypes.c_longlong]),
+        "oracle_rmsprop_update": (None, [_d, _d, _d] + [ctypes.c_double] * 3
+                                  + [ctypes.c_longlong]),
+        "oracle_adam_update": (None, [_d, _d, _d, _d] + [ctypes.c_double] * 4
+                               + [ctypes.c_longlong, ctypes.c_longlong]),
         "oracle_sgd_momentum_update": (None, [_d, _d, _d, ctypes.c_double, ctypes.c_double,
                                               ctypes.c_longlong]),
         "oracle_count_nonzero": (ctypes.c_longlong, [_d, ctypes.c_longlong]),
@@ -266,6 +275,46 @@ def sgd_momentum_update(theta, grad, v, lr, mu):
     _load().oracle_sgd_momentum_update(_p(theta), _p(grad), _p(v), float(lr), float(mu),
                                        theta.size)
     return theta, v
+
+
+def sgd_update(theta, grad, lr):
+    """Returns theta - lr*grad (inputs untouched)."""
+    theta = _f64(theta).copy()
+    grad = _f64(grad)
+    _load().oracle_sgd_update(_p(theta), _p(grad), float(lr), theta.size)
+    return theta
+
+
+def sgd_nesterov_update(theta, grad, v, lr, mu):
+    """Returns (theta_new, v_new)."""
+    theta, v, grad = _f64(theta).copy(), _f64(v).copy(), _f64(grad)
+    _load().oracle_sgd_nesterov_update(_p(theta), _p(grad), _p(v), float(lr), float(mu),
+                                       theta.size)
+    return theta, v
+
+
+def adagrad_update(theta, grad, cache, lr, eps):
+    """Returns (theta_new, cache_new)."""
+    theta, cache, grad = _f64(theta).copy(), _f64(cache).copy(), _f64(grad)
+    _load().oracle_adagrad_update(_p(theta), _p(grad), _p(cache), float(lr), float(eps),
+                                  theta.size)
+    return theta, cache
+
+
+def rmsprop_update(theta, grad, cache, lr, decay, eps):
+    """Returns (theta_new, cache_new)."""
+    theta, cache, grad = _f64(theta).copy(), _f64(cache).copy(), _f64(grad)
+    _load().oracle_rmsprop_update(_p(theta), _p(grad), _p(cache), float(lr), float(decay),
+                                  float(eps), theta.size)
+    return theta, cache
+
+
+def adam_update(theta, grad, m, v, lr, beta1, beta2, eps, t):
+    """Returns (theta_new, m_new, v_new) after step t (t >= 1)."""
+    theta, m, v, grad = _f64(theta).copy(), _f64(m).copy(), _f64(v).copy(), _f64(grad)
+    _load().oracle_adam_update(_p(theta), _p(grad), _p(m), _p(v), float(lr), float(beta1),
+                               float(beta2), float(eps), int(t), theta.size)
+    return theta, m, v
 
 
 def count_nonzero(X):

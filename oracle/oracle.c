@@ -447,6 +447,70 @@ void oracle_sgd_momentum_update(double *theta, const double *grad, double *v,
     }
 }
 
+/* ------------------------------------------------------------------------- */
+/* The other optimizers (Section 2 names Adagrad, Adam, RMSprop, SGD and SGD   */
+/* with Nesterov momentum; it prints no formulas).  Readings, one step each:   */
+/*   SGD:      theta <- theta - lr*g                                           */
+/*   Nesterov: v' = mu*v - lr*g; theta <- theta - mu*v + (1+mu)*v'; v <- v'    */
+/*             (Nesterov's look-ahead step rewritten on the current iterate)   */
+/*   Adagrad:  c <- c + g^2; theta <- theta - lr*g/(sqrt(c) + eps)   (Duchi et */
+/*             al.)                                                            */
+/*   RMSprop:  c <- rho*c + (1-rho)*g^2; theta <- theta - lr*g/(sqrt(c) + eps) */
+/*             (Tieleman and Hinton)                                          */
+/*   Adam:     m <- b1*m + (1-b1)*g; v <- b2*v + (1-b2)*g^2;                   */
+/*             theta <- theta - a_t*m/(sqrt(v) + eps),                         */
+/*             a_t = lr*sqrt(1-b2^t)/(1-b1^t)  (Kingma and Ba, with the bias   */
+/*             corrections folded into the step size), t = 1, 2, ...           */
+/* ------------------------------------------------------------------------- */
+void oracle_sgd_update(double *theta, const double *g, double lr, long long n)
+{
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < n; ++e) theta[e] = theta[e] - lr * g[e];
+}
+
+void oracle_sgd_nesterov_update(double *theta, const double *g, double *v, double lr,
+                                double mu, long long n)
+{
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < n; ++e) {
+        double v_prev = v[e];
+        v[e] = mu * v_prev - lr * g[e];
+        theta[e] = theta[e] - mu * v_prev + (1.0 + mu) * v[e];
+    }
+}
+
+void oracle_adagrad_update(double *theta, const double *g, double *c, double lr, double eps,
+                           long long n)
+{
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < n; ++e) {
+        c[e] = c[e] + g[e] * g[e];
+        theta[e] = theta[e] - lr * g[e] / (sqrt(c[e]) + eps);
+    }
+}
+
+void oracle_rmsprop_update(double *theta, const double *g, double *c, double lr, double rho,
+                           double eps, long long n)
+{
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < n; ++e) {
+        c[e] = rho * c[e] + (1.0 - rho) * g[e] * g[e];
+        theta[e] = theta[e] - lr * g[e] / (sqrt(c[e]) + eps);
+    }
+}
+
+void oracle_adam_update(double *theta, const double *g, double *m, double *v, double lr,
+                        double b1, double b2, double eps, long long t, long long n)
+{
+    double a_t = lr * sqrt(1.0 - pow(b2, (double)t)) / (1.0 - pow(b1, (double)t));
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < n; ++e) {
+        m[e] = b1 * m[e] + (1.0 - b1) * g[e];
+        v[e] = b2 * v[e] + (1.0 - b2) * g[e] * g[e];
+        theta[e] = theta[e] - a_t * m[e] / (sqrt(v[e]) + eps);
+    }
+}
+
 /* Number of entries different from zero (the paper tracks non-zero counts of
  * every intermediate; Section 3 "Sparse Operations"). */
 long long oracle_count_nonzero(const double *X, long long n)

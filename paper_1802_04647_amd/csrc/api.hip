@@ -281,6 +281,17 @@ int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *pro
                     "softmax_xent");
 }
 
+int softmax_fwd(dmlnn_dtype dtype, const void *scores, void *probs, int N, int K, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "softmax_fwd: bad dtype %d", (int)dtype);
+    if (!scores || !probs) return fail(DMLNN_ERR_NULL, "softmax_fwd: scores and probs are required");
+    if (!count_ok(N, K)) return fail(DMLNN_ERR_ARG, "softmax_fwd: bad sizes N=%d K=%d", N, K);
+    if (scores == probs) return fail(DMLNN_ERR_ARG, "softmax_fwd: probs may not alias scores");
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_softmax(dtype, scores, probs, N, K, (hipStream_t)stream),
+                    "softmax_fwd");
+}
+
 int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v, double lr,
                         double mu, long long n, void *stream)
 {
@@ -290,6 +301,71 @@ int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *
     if (int r = device_check()) return r;
     return launched(dmlnn::launch_sgd_momentum(dtype, theta, grad, v, lr, mu, n, (hipStream_t)stream),
                     "sgd_momentum_update");
+}
+
+static int optim_common(const char *name, dmlnn_dtype dtype, const void *theta, const void *grad,
+                        const void *s1, const void *s2, long long n)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "%s: bad dtype %d", name, (int)dtype);
+    if (!theta || !grad || !s1 || !s2)
+        return fail(DMLNN_ERR_NULL, "%s: theta, grad and the state buffers are required", name);
+    if (n < 1 || n > kMaxElems) return fail(DMLNN_ERR_ARG, "%s: bad n=%lld", name, n);
+    return DMLNN_OK;
+}
+
+int sgd_update(dmlnn_dtype dtype, void *theta, const void *grad, double lr, long long n,
+               void *stream)
+{
+    if (int r = optim_common("sgd_update", dtype, theta, grad, theta, theta, n)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_sgd(dtype, theta, grad, lr, n, (hipStream_t)stream),
+                    "sgd_update");
+}
+
+int sgd_nesterov_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v, double lr,
+                        double mu, long long n, void *stream)
+{
+    if (int r = optim_common("sgd_nesterov_update", dtype, theta, grad, v, v, n)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_sgd_nesterov(dtype, theta, grad, v, lr, mu, n,
+                                               (hipStream_t)stream),
+                    "sgd_nesterov_update");
+}
+
+int adagrad_update(dmlnn_dtype dtype, void *theta, const void *grad, void *cache, double lr,
+                   double eps, long long n, void *stream)
+{
+    if (int r = optim_common("adagrad_update", dtype, theta, grad, cache, cache, n)) return r;
+    if (!(eps >= 0.0)) return fail(DMLNN_ERR_ARG, "adagrad_update: eps must be >= 0");
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_adagrad(dtype, theta, grad, cache, lr, eps, n,
+                                          (hipStream_t)stream),
+                    "adagrad_update");
+}
+
+int rmsprop_update(dmlnn_dtype dtype, void *theta, const void *grad, void *cache, double lr,
+                   double decay, double eps, long long n, void *stream)
+{
+    if (int r = optim_common("rmsprop_update", dtype, theta, grad, cache, cache, n)) return r;
+    if (!(decay >= 0.0 && decay <= 1.0) || !(eps >= 0.0))
+        return fail(DMLNN_ERR_ARG, "rmsprop_update: need 0 <= decay <= 1 and eps >= 0");
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_rmsprop(dtype, theta, grad, cache, lr, decay, eps, n,
+                                          (hipStream_t)stream),
+                    "rmsprop_update");
+}
+
+int adam_update(dmlnn_dtype dtype, void *theta, const void *grad, void *m, void *v, double lr,
+                double beta1, double beta2, double eps, long long t, long long n, void *stream)
+{
+    if (int r = optim_common("adam_update", dtype, theta, grad, m, v, n)) return r;
+    if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0))
+        return fail(DMLNN_ERR_ARG, "adam_update: need 0 <= beta1, beta2 < 1 and eps >= 0");
+    if (t < 1) return fail(DMLNN_ERR_ARG, "adam_update: step t=%lld must be >= 1", t);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_adam(dtype, theta, grad, m, v, lr, beta1, beta2, eps, t, n,
+                                       (hipStream_t)stream),
+                    "adam_update");
 }
 
 int count_nonzero(dmlnn_dtype dtype, const void *X, long long n, long long *out_dev, void *stream)

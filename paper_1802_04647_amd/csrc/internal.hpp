@@ -44,9 +44,23 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
                              int M, hipStream_t s);
 hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
                                void *loss, int N, int K, hipStream_t s);
+hipError_t launch_softmax(int dtype, const void *S, void *P, int N, int K, hipStream_t s);
 hipError_t launch_sgd_momentum(int dtype, void *theta, const void *grad, void *v, double lr,
                                double mu, long long n, hipStream_t s);
 hipError_t launch_count_nonzero(int dtype, const void *X, long long n, long long *out,
                                 hipStream_t s);
+
+// ------------------------------------------------------------ optimizers ----
+hipError_t launch_sgd(int dtype, void *theta, const void *grad, double lr, long long n,
+                      hipStream_t s);
+hipError_t launch_sgd_nesterov(int dtype, void *theta, const void *grad, void *v, double lr,
+                               double mu, long long n, hipStream_t s);
+hipError_t launch_adagrad(int dtype, void *theta, const void *grad, void *cache, double lr,
+                          double eps, long long n, hipStream_t s);
+hipError_t launch_rmsprop(int dtype, void *theta, const void *grad, void *cache, double lr,
+                          double decay, double eps, long long n, hipStream_t s);
+hipError_t launch_adam(int dtype, void *theta, const void *grad, void *m, void *v, double lr,
+                       double beta1, double beta2, double eps, long long t, long long n,
+                       hipStream_t s);
 
 }  // namespace dmlnn

@@ -86,7 +86,47 @@ __global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, co
     }
 }
 
+// Row-wise softmax alone (forward-only scoring): same segment layout, no loss.
+template <typename T>
+__global__ __launch_bounds__(kSmThreads) void softmax_kernel(const T *S, T *P, int N, int K, int sw)
+{
+    const int lane = lane_id(), wave = wave_id();
+    const int rpw = kWave / sw, seg = lane / sw, sl = lane - seg * sw;
+    const int wave_g = blockIdx.x * kSmWaves + wave, nwaves = gridDim.x * kSmWaves;
+    for (int r0 = wave_g * rpw; r0 < N; r0 += nwaves * rpw) {
+        const int n = r0 + seg;
+        const bool ok = n < N;
+        const T *s = S + (size_t)n * K;
+        T m = -INFINITY;
+        if (ok)
+            for (int k = sl; k < K; k += sw) m = s[k] > m ? s[k] : m;
+        m = seg_max(m, sw);
+        T se = T(0);
+        if (ok)
+            for (int k = sl; k < K; k += sw) se += exp(s[k] - m);
+        se = seg_sum(se, sw);
+        if (ok)
+            for (int k = sl; k < K; k += sw) P[(size_t)n * K + k] = exp(s[k] - m) / se;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_softmax(int dtype, const void *S, void *P, int N, int K, hipStream_t s)
+{
+    int sw = 1;
+    while (sw < K && sw < kWave) sw <<= 1;
+    const long long rows_per_block = (long long)kSmWaves * (kWave / sw);
+    long long g = (N + rows_per_block - 1) / rows_per_block;
+    if (g > 1024) g = 1024;
+    if (dtype == 0)
+        hipLaunchKernelGGL(softmax_kernel<double>, dim3((int)g), dim3(kSmThreads), 0, s,
+                           (const double *)S, (double *)P, N, K, sw);
+    else
+        hipLaunchKernelGGL(softmax_kernel<float>, dim3((int)g), dim3(kSmThreads), 0, s,
+                           (const float *)S, (float *)P, N, K, sw);
+    return hipGetLastError();
+}
 
 hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
                                void *loss, int N, int K, hipStream_t s)

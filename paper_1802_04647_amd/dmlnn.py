@@ -65,6 +65,16 @@ def load():
         "softmax_xent": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _vp]),
         "sgd_momentum_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_longlong, _vp]),
+        "softmax_fwd": (_i, [_i, _vp, _vp, _i, _i, _vp]),
+        "sgd_update": (_i, [_i, _vp, _vp, ctypes.c_double, ctypes.c_longlong, _vp]),
+        "sgd_nesterov_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_longlong, _vp]),
+        "adagrad_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
+                                ctypes.c_longlong, _vp]),
+        "rmsprop_update": (_i, [_i, _vp, _vp, _vp] + [ctypes.c_double] * 3
+                           + [ctypes.c_longlong, _vp]),
+        "adam_update": (_i, [_i, _vp, _vp, _vp, _vp] + [ctypes.c_double] * 4
+                        + [ctypes.c_longlong, ctypes.c_longlong, _vp]),
         "count_nonzero": (_i, [_i, _vp, ctypes.c_longlong, _vp, _vp]),
         "dmlnn_last_error": (ctypes.c_char_p, []),
     }
@@ -309,6 +319,17 @@ def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None
     return loss, dscores, probs
 
 
+def softmax_fwd(scores, probs=None):
+    """Row-wise softmax of an N x K matrix."""
+    dt = _dtype(scores, probs)
+    N, K = scores.shape
+    if probs is None:
+        probs = _empty((N, K), scores)
+    _need(probs, N * K, "probs")
+    _check("softmax_fwd", load().softmax_fwd(dt, _p(scores), _p(probs), N, K, _stream()))
+    return probs
+
+
 def sgd_momentum_update(theta, grad, v, lr, mu):
     """In place: v <- mu v - lr grad; theta <- theta + v."""
     dt = _dtype(theta, grad, v)
@@ -317,6 +338,59 @@ def sgd_momentum_update(theta, grad, v, lr, mu):
     _check("sgd_momentum_update", load().sgd_momentum_update(
         dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream()))
     return theta, v
+
+
+def sgd_update(theta, grad, lr):
+    """In place: theta <- theta - lr grad."""
+    dt = _dtype(theta, grad)
+    _need(grad, theta.numel(), "grad")
+    _check("sgd_update", load().sgd_update(dt, _p(theta), _p(grad), float(lr), theta.numel(),
+                                           _stream()))
+    return theta
+
+
+def sgd_nesterov_update(theta, grad, v, lr, mu):
+    """In place: v' = mu v - lr grad; theta <- theta - mu v + (1 + mu) v'; v <- v'."""
+    dt = _dtype(theta, grad, v)
+    _need(grad, theta.numel(), "grad")
+    _need(v, theta.numel(), "v")
+    _check("sgd_nesterov_update", load().sgd_nesterov_update(
+        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream()))
+    return theta, v
+
+
+def adagrad_update(theta, grad, cache, lr, eps=1e-6):
+    """In place: cache += grad^2; theta -= lr grad / (sqrt(cache) + eps)."""
+    dt = _dtype(theta, grad, cache)
+    _need(grad, theta.numel(), "grad")
+    _need(cache, theta.numel(), "cache")
+    _check("adagrad_update", load().adagrad_update(
+        dt, _p(theta), _p(grad), _p(cache), float(lr), float(eps), theta.numel(), _stream()))
+    return theta, cache
+
+
+def rmsprop_update(theta, grad, cache, lr, decay=0.99, eps=1e-6):
+    """In place: cache = decay cache + (1-decay) grad^2; theta -= lr grad / (sqrt(cache) + eps)."""
+    dt = _dtype(theta, grad, cache)
+    _need(grad, theta.numel(), "grad")
+    _need(cache, theta.numel(), "cache")
+    _check("rmsprop_update", load().rmsprop_update(
+        dt, _p(theta), _p(grad), _p(cache), float(lr), float(decay), float(eps), theta.numel(),
+        _stream()))
+    return theta, cache
+
+
+def adam_update(theta, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, t=1):
+    """In place, step t >= 1: m, v moments; theta -= lr_t m / (sqrt(v) + eps),
+    lr_t = lr sqrt(1 - beta2^t) / (1 - beta1^t)."""
+    dt = _dtype(theta, grad, m, v)
+    _need(grad, theta.numel(), "grad")
+    _need(m, theta.numel(), "m")
+    _need(v, theta.numel(), "v")
+    _check("adam_update", load().adam_update(
+        dt, _p(theta), _p(grad), _p(m), _p(v), float(lr), float(beta1), float(beta2), float(eps),
+        int(t), theta.numel(), _stream()))
+    return theta, m, v
 
 
 def count_nonzero(X, out=None):

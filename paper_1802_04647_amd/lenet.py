@@ -8,7 +8,8 @@ library's layers, its minibatch training loop and SGD with momentum).
 
 All activations, gradients and the backward-filter workspaces are allocated
 once; ``step`` only enqueues library calls on the current stream (about twenty
-launches) and returns the loss as a device scalar.
+launches, one of them the optimizer update over the flat parameter buffer) and
+returns the loss as a device scalar.
 """
 from __future__ import annotations
 
@@ -24,9 +25,23 @@ class LeNetTrainer:
                  dtype=torch.float64, device="cuda"):
         self.N, self.lr, self.mu = N, lr, mu
         kw = dict(dtype=dtype, device=device)
-        self.p = {k: torch.as_tensor(v).to(**kw).contiguous() for k, v in params.items()}
-        self.v = {k: torch.zeros_like(t) for k, t in self.p.items()}
-        self.g = {k: torch.empty_like(t) for k, t in self.p.items()}
+        # Parameters, gradients and velocities each live in one flat buffer (the
+        # tensors are contiguous views into it), so the optimizer update of all
+        # eight tensors is a single elementwise launch.
+        shapes = {k: tuple(torch.as_tensor(params[k]).shape) for k in PARAM_ORDER}
+        sizes = {k: int(torch.Size(sh).numel()) for k, sh in shapes.items()}
+        total = sum(sizes.values())
+        self.p_flat = torch.empty(total, **kw)
+        self.g_flat = torch.empty(total, **kw)
+        self.v_flat = torch.zeros(total, **kw)
+        self.p, self.g, self.v = {}, {}, {}
+        off = 0
+        for k in PARAM_ORDER:
+            n = sizes[k]
+            for d, flat in ((self.p, self.p_flat), (self.g, self.g_flat), (self.v, self.v_flat)):
+                d[k] = flat[off:off + n].view(shapes[k])
+            self.p[k].copy_(torch.as_tensor(params[k]).to(**kw))
+            off += n
         e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
         i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
         self.c1, self.p1, self.i1 = e(N, 32 * 784), e(N, 32 * 196), i32(N, 32 * 196)
@@ -64,6 +79,55 @@ class LeNetTrainer:
 
     def step(self, X, Y):
         loss = self.forward_backward(X, Y)
-        for k in PARAM_ORDER:
-            dmlnn.sgd_momentum_update(self.p[k], self.g[k], self.v[k], self.lr, self.mu)
+        dmlnn.sgd_momentum_update(self.p_flat, self.g_flat, self.v_flat, self.lr, self.mu)
         return loss
+
+
+class LeNetScorer:
+    """Forward-only batched scoring of the same network (the paper's parfor-style
+    scoring: every minibatch is independent, Section 3 "Distributed
+    Operations"), on one GPU: the batches are dealt round-robin to ``streams``
+    HIP streams, each with its own activation buffers, so the small per-batch
+    kernels of different batches overlap.  Returns the class probabilities."""
+
+    def __init__(self, params: dict, batch: int = 64, streams: int = 4,
+                 dtype=torch.float64, device="cuda"):
+        kw = dict(dtype=dtype, device=device)
+        self.batch, self.dtype, self.device = batch, dtype, device
+        self.p = {k: torch.as_tensor(v).to(**kw).contiguous() for k, v in params.items()}
+        self.streams = [torch.cuda.Stream(device=device) for _ in range(streams)]
+        e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
+        i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
+        B = batch
+        self.buf = [dict(c1=e(B, 32 * 784), p1=e(B, 32 * 196), i1=i32(B, 32 * 196),
+                         c2=e(B, 64 * 196), p2=e(B, 64 * 49), i2=i32(B, 64 * 49),
+                         h=e(B, 512), s=e(B, 10)) for _ in range(streams)]
+
+    def _forward(self, X, out, b):
+        p = self.p
+        dmlnn.conv2d_forward(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, relu=True, out=b["c1"])
+        dmlnn.max_pool2d_fwd(b["c1"], 32, 28, 28, 2, 2, 2, 0, out=b["p1"], argmax=b["i1"])
+        dmlnn.conv2d_forward(b["p1"], p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, relu=True,
+                             out=b["c2"])
+        dmlnn.max_pool2d_fwd(b["c2"], 64, 14, 14, 2, 2, 2, 0, out=b["p2"], argmax=b["i2"])
+        dmlnn.affine_fwd(b["p2"], p["W3"], p["b3"], relu=True, out=b["h"])
+        dmlnn.affine_fwd(b["h"], p["W4"], p["b4"], relu=False, out=b["s"])
+        dmlnn.softmax_fwd(b["s"], probs=out)
+
+    def score(self, X):
+        """X: M x 784 on the device (M a multiple of the batch size)."""
+        M = X.shape[0]
+        if M % self.batch:
+            raise ValueError(f"{M} rows is not a multiple of the batch size {self.batch}")
+        probs = torch.empty((M, 10), dtype=self.dtype, device=self.device)
+        main = torch.cuda.current_stream()
+        for s in self.streams:
+            s.wait_stream(main)  # X and the parameters are ready
+        for k in range(M // self.batch):
+            j = k % len(self.streams)
+            lo = k * self.batch
+            with torch.cuda.stream(self.streams[j]):
+                self._forward(X[lo:lo + self.batch], probs[lo:lo + self.batch], self.buf[j])
+        for s in self.streams:
+            main.wait_stream(s)
+        return probs

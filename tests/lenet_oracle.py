@@ -48,3 +48,14 @@ def train_step(X, Y, params, vel, lr=0.01, mu=0.9):
 
 def zero_velocities(params):
     return {k: np.zeros_like(v) for k, v in params.items()}
+
+
+def forward_probs(X, p):
+    """Forward-only scoring: class probabilities of each row of X."""
+    c1, _, _ = oracle.conv2d_forward(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, relu=True)
+    p1, _, _, _ = oracle.max_pool2d_fwd(c1, 32, 28, 28, 2, 2, 2, 0)
+    c2, _, _ = oracle.conv2d_forward(p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, relu=True)
+    p2, _, _, _ = oracle.max_pool2d_fwd(c2, 64, 14, 14, 2, 2, 2, 0)
+    h = oracle.affine_fwd(p2, p["W3"], p["b3"], relu=True)
+    s = oracle.affine_fwd(h, p["W4"], p["b4"], relu=False)
+    return oracle.softmax_forward(s)

@@ -122,3 +122,21 @@ def test_binding_rejects_host_tensors():
         dmlnn.conv2d_forward(X, W, None, 1, 8, 8, 3, 3, 1, 1)
     with pytest.raises(TypeError):
         dmlnn.conv2d_forward(X.half(), W.half(), None, 1, 8, 8, 3, 3, 1, 1)
+
+
+def test_optimizer_validation(lib):
+    d = ctypes.c_double
+    assert lib.sgd_update(0, None, FAKE, d(0.1), 10, None) == ERR_NULL
+    assert lib.sgd_update(5, FAKE, FAKE, d(0.1), 10, None) == ERR_DTYPE
+    assert lib.sgd_update(0, FAKE, FAKE, d(0.1), 0, None) == ERR_ARG
+    assert lib.sgd_nesterov_update(0, FAKE, FAKE, None, d(0.1), d(0.9), 10, None) == ERR_NULL
+    assert lib.adagrad_update(0, FAKE, FAKE, FAKE, d(0.1), d(-1.0), 10, None) == ERR_ARG
+    assert lib.rmsprop_update(0, FAKE, FAKE, FAKE, d(0.1), d(1.5), d(1e-6), 10, None) == ERR_ARG
+    assert lib.rmsprop_update(0, FAKE, FAKE, None, d(0.1), d(0.9), d(1e-6), 10, None) == ERR_NULL
+    adam = lib.adam_update
+    assert adam(0, FAKE, FAKE, FAKE, FAKE, d(1e-3), d(0.9), d(0.999), d(1e-8), 0, 10, None) \
+        == ERR_ARG                                                       # t = 0
+    assert adam(0, FAKE, FAKE, FAKE, FAKE, d(1e-3), d(1.0), d(0.999), d(1e-8), 1, 10, None) \
+        == ERR_ARG                                                       # beta1 = 1
+    assert adam(0, FAKE, FAKE, FAKE, None, d(1e-3), d(0.9), d(0.999), d(1e-8), 1, 10, None) \
+        == ERR_NULL

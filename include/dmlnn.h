@@ -150,6 +150,34 @@ DMLNN_API int max_pool2d_bwd(dmlnn_dtype dtype, const void *dout, const int32_t 
                    int N, int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
                    void *stream);
 
+/* ------------------------------------------------------ conv2d_forward_pool ----
+ * Paper: Section "Future Work" (vertical fusion across layers); the layers are
+ * Section 2's conv2d -> relu -> max_pool2d.  One call computes
+ *   c = relu?(conv2d(X, W) + b)                      (as conv2d_forward)
+ *   pooled, argmax = max_pool2d_fwd(c, F, Hout, Wout, pool_h, pool_w, pool_stride, pool_pad)
+ * pooled and argmax are N x (F*Hp*Wp); argmax is the in-row index of each window's
+ * first maximum within a row of c (as max_pool2d_fwd).  c is written to out
+ * when out is not NULL.  When pool_pad == 0 and pool_stride >= pool_h the pool
+ * runs in the convolution's epilogue and c need not be stored (out may be NULL);
+ * otherwise the call runs the two steps back to back and out is required
+ * (DMLNN_ERR_ARG if NULL). */
+DMLNN_API int conv2d_forward_pool(dmlnn_dtype dtype, const void *X, const void *W, const void *b,
+                                  void *out, void *pooled, int32_t *argmax, int N, int C, int Hin,
+                                  int Win, int F, int Hf, int Wf, int stride, int pad, int relu,
+                                  int pool_h, int pool_w, int pool_stride, int pool_pad,
+                                  void *stream);
+
+/* ------------------------------------------------------ max_pool2d_bwd_relu ----
+ * The backward of relu -> max_pool2d with the relu mask folded in, so that the
+ * conv backward passes can take the result as dout with out_fwd = NULL (and the
+ * conv output of the forward need not be kept):
+ *   dX[n,k] = sum of dout[n,o] over outputs o with argmax[n,o] == k and pooled[n,o] > 0.
+ * (The cell an output routes to holds the pooled value, so its relu mask is
+ * pooled > 0.)  Sizes and argmax as max_pool2d_bwd; pooled is N x (C*Hout*Wout). */
+DMLNN_API int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int32_t *argmax,
+                                  const void *pooled, void *dX, int N, int C, int Hin, int Win,
+                                  int Hf, int Wf, int stride, int pad, void *stream);
+
 /* ----------------------------------------------------------------- affine ----
  * Paper: Section 2 listing (scores = X %*% W + b; backward returns
  * [dX, dW, db]).  X is N x D, W is D x M, b is 1 x M, out is N x M.

@@ -237,9 +237,61 @@ int max_pool2d_bwd(dmlnn_dtype dtype, const void *dout, const int32_t *argmax, v
     int Hout, Wout;
     if (int r = pool_dims(N, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout)) return r;
     if (int r = device_check()) return r;
-    return launched(dmlnn::launch_max_pool_bwd(dtype, dout, argmax, dX, N, C, Hin, Win, Hf, Wf,
-                                               stride, pad, Hout, Wout, (hipStream_t)stream),
+    return launched(dmlnn::launch_max_pool_bwd(dtype, dout, argmax, nullptr, dX, N, C, Hin, Win,
+                                               Hf, Wf, stride, pad, Hout, Wout,
+                                               (hipStream_t)stream),
                     "max_pool2d_bwd");
+}
+
+int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int32_t *argmax,
+                        const void *pooled, void *dX, int N, int C, int Hin, int Win, int Hf,
+                        int Wf, int stride, int pad, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "max_pool2d_bwd_relu: bad dtype %d", (int)dtype);
+    if (!dout || !argmax || !pooled || !dX)
+        return fail(DMLNN_ERR_NULL, "max_pool2d_bwd_relu: dout, argmax, pooled, dX are required");
+    int Hout, Wout;
+    if (int r = pool_dims(N, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout)) return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_max_pool_bwd(dtype, dout, argmax, pooled, dX, N, C, Hin, Win,
+                                               Hf, Wf, stride, pad, Hout, Wout,
+                                               (hipStream_t)stream),
+                    "max_pool2d_bwd_relu");
+}
+
+int conv2d_forward_pool(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
+                        void *pooled, int32_t *argmax, int N, int C, int Hin, int Win, int F,
+                        int Hf, int Wf, int stride, int pad, int relu, int pool_h, int pool_w,
+                        int pool_stride, int pool_pad, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_forward_pool: bad dtype %d", (int)dtype);
+    if (!X || !W || !pooled || !argmax)
+        return fail(DMLNN_ERR_NULL, "conv2d_forward_pool: X, W, pooled and argmax are required");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    int Hp, Wp;
+    if (int r = pool_dims(N, F, d.Hout, d.Wout, pool_h, pool_w, pool_stride, pool_pad, Hp, Wp))
+        return r;
+    if (int r = device_check()) return r;
+    const hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipErrorNotSupported;
+    if (pool_pad == 0)
+        e = dmlnn::launch_conv_forward_pool(dtype, X, W, b, out, pooled, argmax, d, relu, pool_h,
+                                            pool_w, pool_stride, Hp, Wp, zero_skip_mode(), s);
+    if (e == hipErrorNotSupported) {
+        // Unfused: the conv output is needed as the pool's input.
+        if (!out)
+            return fail(DMLNN_ERR_ARG,
+                        "conv2d_forward_pool: this pooling (%dx%d stride %d pad %d after a "
+                        "%dx%d output) is not fusable; pass the conv output buffer",
+                        pool_h, pool_w, pool_stride, pool_pad, d.Hout, d.Wout);
+        (void)hipGetLastError();
+        e = dmlnn::launch_conv_forward(dtype, X, W, b, out, d, relu, zero_skip_mode(), s);
+        if (e == hipSuccess)
+            e = dmlnn::launch_max_pool_fwd(dtype, out, pooled, argmax, N, F, d.Hout, d.Wout,
+                                           pool_h, pool_w, pool_stride, pool_pad, Hp, Wp, s);
+    }
+    return launched(e, "conv2d_forward_pool");
 }
 
 int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out, int N,

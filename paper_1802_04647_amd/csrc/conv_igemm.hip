@@ -46,11 +46,19 @@ struct IgemmArgs {
     int S, Ph, Pw;
     int relu;
     int tiles_per_img;
+    int TS;         // pixels between consecutive tile origins (<= 32 NB; less when a
+                    // fused pool needs tiles of whole row groups)
     int KC, KCK;
     int Wpad, CH, SA;
     int pipelined;  // 1: chunk fits the per-thread staging registers
     int ksplit;     // LDS-DMA kernel, M <= 32: the two m-halves of waves split the
                     // k-steps of the same 32 rows instead of taking 32 rows each
+    // Fused max-pool epilogue (forward, LDS-DMA kernel): PH x PW windows at
+    // stride PS, no padding, giving Hp x Wp per filter; pooled [N][M][Hp*Wp]
+    // and the in-row argmax of each window within the conv output row.
+    void *pool_out;
+    int32_t *pool_idx;
+    int PH, PW, PS, Hp, Wp;
     unsigned long long magic_kck, magic_hw, magic_wf;
 };
 
@@ -68,8 +76,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
     const int n = blockIdx.x / a.tiles_per_img;
     const int tile = blockIdx.x - n * a.tiles_per_img;
     const int m0 = blockIdx.y * kBM;
-    const int q0 = tile * (32 * NB);
-    const int qend = min(q0 + 32 * NB, a.Q);
+    const int q0 = tile * a.TS;
+    const int qend = min(q0 + a.TS, a.Q);
     const int qy0 = q0 / a.Qw;
     const int rows_need = ((qend - 1) / a.Qw - qy0) * a.S + a.Hf;
     const int ybase = qy0 * a.S - a.Ph;
@@ -283,7 +291,7 @@ struct DmaLayout {
                                           // has 256 bytes of slack
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP, bool KS>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL>
 __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
@@ -297,8 +305,8 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     const int n = blockIdx.x / a.tiles_per_img;
     const int tile = blockIdx.x - n * a.tiles_per_img;
     const int m0 = blockIdx.y * kBM;
-    const int q0 = tile * (32 * NB);
-    const int qend = min(q0 + 32 * NB, a.Q);
+    const int q0 = tile * a.TS;
+    const int qend = min(q0 + a.TS, a.Q);
     const int qy0 = q0 / a.Qw;
     const int rows_need = ((qend - 1) / a.Qw - qy0) * a.S + a.Hf;
     const int ybase = qy0 * a.S - a.Ph;
@@ -475,6 +483,7 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         st ^= 1;
     }
 
+    bool active = true;  // this wave holds final values of its rows
     if (KS) {
         // Waves wm = 1 hand their partial tiles to the waves wm = 0 of the same
         // columns, which add them (fixed order) and store.  The stages are free:
@@ -489,40 +498,103 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
                     for (int r = 0; r < 4; ++r)
                         s_red[(((wn * 2 + x) * NB + y) * 4 + r) * kWave + lane] = acc[x][y][r];
         __syncthreads();
-        if (wm == 1) return;
+        if (wm == 1) {
+            if (!POOL) return;
+            active = false;
+        } else {
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < NB; ++y)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        acc[x][y][r] += s_red[(((wn * 2 + x) * NB + y) * 4 + r) * kWave + lane];
+        }
+    }
+    const int mbase = m0 + (KS ? 0 : wm * 32);
+    if (!BWD && active) {  // bias and relu, in place
+        const T *bias = reinterpret_cast<const T *>(a.bias);
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = mbase + x * 16 + MF::row(lane, r);
+                const T bm = (bias && m < a.M) ? bias[m] : T(0);
+#pragma unroll
+                for (int y = 0; y < NB; ++y) acc[x][y][r] = relu_if(acc[x][y][r] + bm, a.relu);
+            }
+    }
+    if (active && a.out) {
+        T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
             for (int y = 0; y < NB; ++y)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    acc[x][y][r] += s_red[(((wn * 2 + x) * NB + y) * 4 + r) * kWave + lane];
-    }
-    T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
-    const T *bias = reinterpret_cast<const T *>(a.bias);
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < NB; ++y)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                int m = m0 + (KS ? 0 : wm * 32) + x * 16 + MF::row(lane, r);
-                int q = q0 + (wn * NB + y) * 16 + (lane & 15);
-                if (m < a.M && q < qend) {
-                    T v = acc[x][y][r];
-                    if (!BWD) {
-                        if (bias) v += bias[m];
-                        v = relu_if(v, a.relu);
-                    }
-                    out[(size_t)m * a.Q + q] = v;
+                for (int r = 0; r < 4; ++r) {
+                    const int m = mbase + x * 16 + MF::row(lane, r);
+                    const int q = q0 + (wn * NB + y) * 16 + (lane & 15);
+                    if (m < a.M && q < qend) out[(size_t)m * a.Q + q] = acc[x][y][r];
                 }
+    }
+    if (POOL) {
+        // The tile is whole rows of conv output [y_lo, y_hi); the pooled rows
+        // whose windows start in it lie wholly inside it (PS >= PH, tiles a
+        // multiple of PS rows).  Per 32-row half: the half's values go to LDS
+        // ([32][32 NB]), then every thread scans windows (first maximum wins,
+        // strict >, as the standalone pooling kernel does).
+        constexpr int BN = 32 * NB;
+        T *s_t = reinterpret_cast<T *>(smem);
+        const int y_lo = q0 / a.Qw, y_hi = qend / a.Qw;  // q0, qend: multiples of Qw
+        const int py_lo = y_lo / a.PS;
+        const int py_hi = min(a.Hp, (y_hi + a.PS - 1) / a.PS);
+        const int npool = (py_hi - py_lo) * a.Wp;
+        T *pout = reinterpret_cast<T *>(a.pool_out) + (size_t)n * a.M * a.Hp * a.Wp;
+        int32_t *pidx = a.pool_idx + (size_t)n * a.M * a.Hp * a.Wp;
+        for (int half = 0; half < (KS ? 1 : 2); ++half) {
+            __syncthreads();
+            if (active && (KS || wm == half))
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < NB; ++y)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int u = (wn * NB + y) * 16 + (lane & 15);
+                            if (q0 + u < qend)
+                                s_t[(x * 16 + MF::row(lane, r)) * BN + u] = acc[x][y][r];
+                        }
+            __syncthreads();
+            for (int e = tid; e < 32 * npool; e += kThreads) {
+                const int rr = e / npool, pe = e - rr * npool;
+                const int m = m0 + half * 32 + rr;
+                if (m >= a.M) continue;
+                const int py = py_lo + pe / a.Wp, px = pe - (pe / a.Wp) * a.Wp;
+                T best = T(0);
+                int bidx = -1;
+                for (int i = 0; i < a.PH; ++i) {
+                    const int yy = py * a.PS + i;
+                    for (int j = 0; j < a.PW; ++j) {
+                        const int xx = px * a.PS + j;
+                        const T v = s_t[rr * BN + (yy - y_lo) * a.Qw + xx];
+                        if (bidx < 0 || v > best) {
+                            best = v;
+                            bidx = yy * a.Qw + xx;
+                        }
+                    }
+                }
+                const size_t o = (size_t)m * a.Hp * a.Wp + (size_t)py * a.Wp + px;
+                pout[o] = best;
+                pidx[o] = m * a.Q + bidx;
             }
+        }
+    }
 }
 
 // Host-side tile selection ----------------------------------------------------
 
 struct Plan {
-    int NB, KC, KCK, Wpad, CH, SA, tiles_per_img, m_tiles, pipelined;
+    int NB, KC, KCK, Wpad, CH, SA, tiles_per_img, TS, m_tiles, pipelined;
     size_t lds;
 };
 
@@ -532,7 +604,7 @@ size_t lds_bytes(size_t tsz, int KC, int CH, int SA, int KCK)
 }
 
 bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, int nimg,
-               Plan &p)
+               Plan &p, int align = 0)
 {
     static const int kNB64[] = {7, 4, 2, 1}, kNB32[] = {7, 4, 2, 1};
     const int HfWf = Hf * Wf;
@@ -543,7 +615,12 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
     for (int ci = 0; ci < ncand; ++ci) {
         const int NB = cand[ci];
         int BN = 32 * NB;
-        int tiles = (Q + BN - 1) / BN;
+        // a fused epilogue needs tiles of whole row groups (or one tile per
+        // image): the tile origins step by the largest multiple of the group
+        // that fits, and the rest of the 32 NB pixels is masked
+        const int TS = (!align || BN >= Q) ? BN : (BN / align) * align;
+        if (TS == 0) continue;
+        int tiles = (Q + TS - 1) / TS;
         double fill = (double)Q / ((double)tiles * BN);
         double blocks = (double)nimg * tiles * p.m_tiles;
         double occ = blocks >= 512.0 ? 1.0 : blocks / 512.0;
@@ -552,15 +629,16 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
             best = score;
             p.NB = NB;
             p.tiles_per_img = tiles;
+            p.TS = TS;
         }
     }
-    // Input rows a tile of BN consecutive outputs reads: the exact maximum over
+    if (best < 0.0) return false;
+    // Input rows a tile of TS consecutive outputs reads: the exact maximum over
     // the tiles of an image (a tile that starts a row spans one row fewer than
-    // the general bound when BN is a multiple of the output width).
-    const int BN = 32 * p.NB;
+    // the general bound when TS is a multiple of the output width).
     int rows_max = 0;
     for (int t = 0; t < p.tiles_per_img; ++t) {
-        const int qa = t * BN, qb = (qa + BN < Q ? qa + BN : Q) - 1;
+        const int qa = t * p.TS, qb = (qa + p.TS < Q ? qa + p.TS : Q) - 1;
         const int r = (qb / Qw - qa / Qw) * S + Hf;
         rows_max = r > rows_max ? r : rows_max;
     }
@@ -622,18 +700,18 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
     return false;
 }
 
-template <typename T, int NB, bool BWD, bool KS>
+template <typename T, int NB, bool BWD, bool KS, bool POOL>
 hipError_t launch_dma_ks(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                          int nimg, int zero_skip, hipStream_t s)
 {
     dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
     hipError_t e;
     if (zero_skip) {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS, POOL>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     } else {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS, POOL>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     }
@@ -644,8 +722,13 @@ template <typename T, int NB, bool BWD>
 hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                       int nimg, int zero_skip, hipStream_t s)
 {
-    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true>(a, p, L, w_bytes, nimg, zero_skip, s);
-    return launch_dma_ks<T, NB, BWD, false>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (!BWD && a.pool_out) {
+        if (a.ksplit)
+            return launch_dma_ks<T, NB, false, true, true>(a, p, L, w_bytes, nimg, zero_skip, s);
+        return launch_dma_ks<T, NB, false, false, true>(a, p, L, w_bytes, nimg, zero_skip, s);
+    }
+    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true, false>(a, p, L, w_bytes, nimg, zero_skip, s);
+    return launch_dma_ks<T, NB, BWD, false, false>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
 
 template <typename T, int NB, bool BWD>
@@ -675,8 +758,11 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.Qw = Qw;
     a.Q = Qh * Qw;
     a.HfWf = a.Hf * a.Wf;
-    if (!make_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, nimg, p)) return hipErrorInvalidValue;
+    const bool pool = !BWD && a.pool_out;
+    if (!make_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, nimg, p, pool ? Qw * a.PS : 0))
+        return pool ? hipErrorNotSupported : hipErrorInvalidValue;
     a.tiles_per_img = p.tiles_per_img;
+    a.TS = p.TS;
     a.KC = p.KC;
     a.KCK = p.KCK;
     a.Wpad = p.Wpad;
@@ -702,6 +788,11 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
             const size_t red = sizeof(T) * (size_t)2 * 2 * pd.NB * 4 * kWave;
             if (pd.lds < red) pd.lds = red;
         }
+        if (pool) {  // so does the pooling tile (32 rows x 32 NB)
+            const size_t pt = sizeof(T) * (size_t)32 * 32 * pd.NB;
+            if (pd.lds < pt) pd.lds = pt;
+            if (pd.lds > kLdsPerBlock) return hipErrorNotSupported;
+        }
         switch (pd.NB) {
         case 7: return launch_dma<T, 7, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
         case 4: return launch_dma<T, 4, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
@@ -709,6 +800,7 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         default: return launch_dma<T, 1, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
         }
     }
+    if (pool) return hipErrorNotSupported;  // the fused epilogue is LDS-DMA only
     switch (p.NB) {
     case 7: return launch_nb<T, 7, BWD>(a, p, nimg, zero_skip, s);
     case 4: return launch_nb<T, 4, BWD>(a, p, nimg, zero_skip, s);
@@ -737,6 +829,41 @@ hipError_t launch_conv_forward(int dtype, const void *X, const void *W, const vo
     a.Ph = d.pad;
     a.Pw = d.pad;
     a.relu = relu;
+    if (dtype == 0)
+        return launch_typed<double, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+    return launch_typed<float, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+}
+
+hipError_t launch_conv_forward_pool(int dtype, const void *X, const void *W, const void *b,
+                                    void *out, void *pooled, int32_t *argmax, const ConvDims &d,
+                                    int relu, int ph, int pw, int ps, int Hp, int Wp,
+                                    int zero_skip, hipStream_t s)
+{
+    // Fused only when every pooled window lies inside one tile of whole rows:
+    // no pool padding and a stride no smaller than the window height.
+    if (ps < ph) return hipErrorNotSupported;
+    IgemmArgs a = {};
+    a.src = X;
+    a.mask = nullptr;
+    a.wgt = W;
+    a.bias = b;
+    a.out = out;
+    a.Sh = d.Hin;
+    a.Sw = d.Win;
+    a.up = 1;
+    a.Hf = d.Hf;
+    a.Wf = d.Wf;
+    a.S = d.stride;
+    a.Ph = d.pad;
+    a.Pw = d.pad;
+    a.relu = relu;
+    a.pool_out = pooled;
+    a.pool_idx = argmax;
+    a.PH = ph;
+    a.PW = pw;
+    a.PS = ps;
+    a.Hp = Hp;
+    a.Wp = Wp;
     if (dtype == 0)
         return launch_typed<double, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
     return launch_typed<float, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);

@@ -17,6 +17,12 @@ struct ConvDims {
 // kernel family; see conv_igemm.hip.
 hipError_t launch_conv_forward(int dtype, const void *X, const void *W, const void *b, void *out,
                                const ConvDims &d, int relu, int zero_skip, hipStream_t s);
+// relu(conv + b) followed by max-pooling in the same kernel's epilogue (out may be
+// null).  hipErrorNotSupported when the shape does not allow the fused epilogue.
+hipError_t launch_conv_forward_pool(int dtype, const void *X, const void *W, const void *b,
+                                    void *out, void *pooled, int32_t *argmax, const ConvDims &d,
+                                    int relu, int ph, int pw, int ps, int Hp, int Wp,
+                                    int zero_skip, hipStream_t s);
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
                                      const void *out_fwd, void *dX, const ConvDims &d,
                                      int zero_skip, hipStream_t s);
@@ -34,9 +40,12 @@ hipError_t launch_bias_add_relu(int dtype, const void *X, const void *b, void *o
 hipError_t launch_max_pool_fwd(int dtype, const void *X, void *out, int32_t *argmax, int N, int C,
                                int Hin, int Win, int Hf, int Wf, int stride, int pad, int Hout,
                                int Wout, hipStream_t s);
-hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax, void *dX, int N,
-                               int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
-                               int Hout, int Wout, hipStream_t s);
+// pooled (the forward's pooled values) may be null; when given, a route only
+// counts where pooled > 0 (the relu mask of the pooled layer).
+hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax,
+                               const void *pooled, void *dX, int N, int C, int Hin, int Win,
+                               int Hf, int Wf, int stride, int pad, int Hout, int Wout,
+                               hipStream_t s);
 hipError_t launch_affine_fwd(int dtype, const void *X, const void *W, const void *b, void *out,
                              int N, int D, int M, int relu, hipStream_t s);
 hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const void *W,

@@ -55,6 +55,7 @@ __global__ __launch_bounds__(256) void max_pool_fwd_kernel(const T *__restrict__
 template <typename T>
 __global__ __launch_bounds__(256) void max_pool_bwd_kernel(const T *__restrict__ dout,
                                                            const int32_t *__restrict__ argmax,
+                                                           const T *__restrict__ pooled,
                                                            T *__restrict__ dX, long long total,
                                                            int C, int Hin, int Win, int Hf,
                                                            int Wf, int S, int P, int Hout,
@@ -83,7 +84,10 @@ __global__ __launch_bounds__(256) void max_pool_bwd_kernel(const T *__restrict__
         for (int oh = oh_lo; oh <= oh_hi; ++oh)
             for (int ow = ow_lo; ow <= ow_hi; ++ow) {
                 const size_t o = obase + (size_t)oh * Wout + ow;
-                if (argmax[o] == me) acc += dout[o];
+                // with pooled given, the relu before the pool gates the route:
+                // the routed cell holds the pooled value, so its relu mask is
+                // pooled > 0
+                if (argmax[o] == me && (!pooled || pooled[o] > T(0))) acc += dout[o];
             }
         dX[e] = acc;
     }
@@ -115,19 +119,22 @@ hipError_t launch_max_pool_fwd(int dtype, const void *X, void *out, int32_t *arg
     return hipGetLastError();
 }
 
-hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax, void *dX, int N,
-                               int C, int Hin, int Win, int Hf, int Wf, int stride, int pad,
-                               int Hout, int Wout, hipStream_t s)
+hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argmax,
+                               const void *pooled, void *dX, int N, int C, int Hin, int Win,
+                               int Hf, int Wf, int stride, int pad, int Hout, int Wout,
+                               hipStream_t s)
 {
     const long long total = (long long)N * C * Hin * Win;
     const int g = grid_for(total);
     if (dtype == 0)
         hipLaunchKernelGGL(max_pool_bwd_kernel<double>, dim3(g), dim3(256), 0, s,
-                           (const double *)dout, argmax, (double *)dX, total, C, Hin, Win, Hf, Wf,
+                           (const double *)dout, argmax, (const double *)pooled, (double *)dX,
+                           total, C, Hin, Win, Hf, Wf,
                            stride, pad, Hout, Wout);
     else
         hipLaunchKernelGGL(max_pool_bwd_kernel<float>, dim3(g), dim3(256), 0, s,
-                           (const float *)dout, argmax, (float *)dX, total, C, Hin, Win, Hf, Wf,
+                           (const float *)dout, argmax, (const float *)pooled, (float *)dX, total,
+                           C, Hin, Win, Hf, Wf,
                            stride, pad, Hout, Wout);
     return hipGetLastError();
 }

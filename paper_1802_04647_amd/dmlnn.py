@@ -66,6 +66,8 @@ def load():
         "sgd_momentum_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_longlong, _vp]),
         "softmax_fwd": (_i, [_i, _vp, _vp, _i, _i, _vp]),
+        "conv2d_forward_pool": (_i, [_i] + [_vp] * 6 + [_i] * 14 + [_vp]),
+        "max_pool2d_bwd_relu": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "sgd_update": (_i, [_i, _vp, _vp, ctypes.c_double, ctypes.c_longlong, _vp]),
         "sgd_nesterov_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_longlong, _vp]),
@@ -261,6 +263,53 @@ def max_pool2d_bwd(dout, argmax, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
     _need(dX, N * C * Hin * Win, "dX")
     _check("max_pool2d_bwd", load().max_pool2d_bwd(dt, _p(dout), _p(argmax), _p(dX), N, C, Hin,
                                                     Win, Hf, Wf, stride, pad, _stream()))
+    return dX
+
+
+def conv2d_forward_pool(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, pool_h, pool_w, pool_stride,
+                        pool_pad, relu=True, out=None, pooled=None, argmax=None, keep_out=False):
+    """relu(conv + b) then max-pool in one call.  Returns (out or None, pooled, argmax,
+    Hp, Wp); the conv output is only materialised when out is given or keep_out."""
+    dt = _dtype(X, W, b, out, pooled)
+    N, F = X.shape[0], W.shape[0]
+    Hout = conv2d_out_dim(Hin, Hf, stride, pad)
+    Wout = conv2d_out_dim(Win, Wf, stride, pad)
+    Hp = conv2d_out_dim(Hout, pool_h, pool_stride, pool_pad)
+    Wp = conv2d_out_dim(Wout, pool_w, pool_stride, pool_pad)
+    _need(X, N * C * Hin * Win, "X")
+    _need(W, F * C * Hf * Wf, "W")
+    _need(b, F, "b")
+    if out is None and keep_out:
+        out = _empty((N, F * max(Hout, 0) * max(Wout, 0)), X)
+    _need(out, N * F * max(Hout, 0) * max(Wout, 0), "out")
+    if pooled is None:
+        pooled = _empty((N, F * max(Hp, 0) * max(Wp, 0)), X)
+    if argmax is None:
+        argmax = _empty((N, F * max(Hp, 0) * max(Wp, 0)), X, torch.int32)
+    _need(pooled, N * F * max(Hp, 0) * max(Wp, 0), "pooled")
+    _need(argmax, N * F * max(Hp, 0) * max(Wp, 0), "argmax")
+    _check("conv2d_forward_pool", load().conv2d_forward_pool(
+        dt, _p(X), _p(W), _p(b), _p(out), _p(pooled), _p(argmax), N, C, Hin, Win, F, Hf, Wf,
+        stride, pad, int(relu), pool_h, pool_w, pool_stride, pool_pad, _stream()))
+    return out, pooled, argmax, Hp, Wp
+
+
+def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+    """Pool backward with the preceding relu's mask (pooled > 0) folded in."""
+    dt = _dtype(dout, pooled, dX)
+    N = dout.shape[0]
+    Hout = conv2d_out_dim(Hin, Hf, stride, pad)
+    Wout = conv2d_out_dim(Win, Wf, stride, pad)
+    if dX is None:
+        dX = _empty((N, C * Hin * Win), dout)
+    n_out = N * C * max(Hout, 0) * max(Wout, 0)
+    _need(dout, n_out, "dout")
+    _need(argmax, n_out, "argmax")
+    _need(pooled, n_out, "pooled")
+    _need(dX, N * C * Hin * Win, "dX")
+    _check("max_pool2d_bwd_relu", load().max_pool2d_bwd_relu(
+        dt, _p(dout), _p(argmax), _p(pooled), _p(dX), N, C, Hin, Win, Hf, Wf, stride, pad,
+        _stream()))
     return dX
 
 

@@ -4,7 +4,9 @@ conv(1->32, 5x5, p2)+relu -> max-pool 2x2/2 -> conv(32->64, 5x5, p2)+relu ->
 max-pool 2x2/2 -> affine 3136->512 + relu -> affine 512->10 -> softmax +
 cross-entropy; backward in reverse order; then v <- mu v - lr g and
 theta <- theta + v for the eight parameter tensors (paper, Section 2: the NN
-library's layers, its minibatch training loop and SGD with momentum).
+library's layers, its minibatch training loop and SGD with momentum).  Each
+conv+relu+pool runs as one fused call, and each pool backward carries the relu
+mask, so the conv outputs are never stored.
 
 All activations, gradients and the backward-filter workspaces are allocated
 once; ``step`` only enqueues library calls on the current stream (about twenty
@@ -44,8 +46,10 @@ class LeNetTrainer:
             off += n
         e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
         i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
-        self.c1, self.p1, self.i1 = e(N, 32 * 784), e(N, 32 * 196), i32(N, 32 * 196)
-        self.c2, self.p2, self.i2 = e(N, 64 * 196), e(N, 64 * 49), i32(N, 64 * 49)
+        # conv outputs are never stored: the pools run in the convolutions'
+        # epilogues and the pool backward folds in the relu mask (pooled > 0)
+        self.p1, self.i1 = e(N, 32 * 196), i32(N, 32 * 196)
+        self.p2, self.i2 = e(N, 64 * 49), i32(N, 64 * 49)
         self.h, self.s = e(N, 512), e(N, 10)
         self.loss, self.ds = e(1), e(N, 10)
         self.dh, self.dp2, self.dc2 = e(N, 512), e(N, 3136), e(N, 64 * 196)
@@ -57,23 +61,24 @@ class LeNetTrainer:
 
     def forward_backward(self, X, Y):
         p, g = self.p, self.g
-        dmlnn.conv2d_forward(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, relu=True, out=self.c1)
-        dmlnn.max_pool2d_fwd(self.c1, 32, 28, 28, 2, 2, 2, 0, out=self.p1, argmax=self.i1)
-        dmlnn.conv2d_forward(self.p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, relu=True,
-                             out=self.c2)
-        dmlnn.max_pool2d_fwd(self.c2, 64, 14, 14, 2, 2, 2, 0, out=self.p2, argmax=self.i2)
+        dmlnn.conv2d_forward_pool(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, 2, 2, 2, 0,
+                                  pooled=self.p1, argmax=self.i1)
+        dmlnn.conv2d_forward_pool(self.p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, 2, 2, 2, 0,
+                                  pooled=self.p2, argmax=self.i2)
         dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h)
         dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s)
         dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds)
         dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"])
         dmlnn.affine_bwd(self.dh, self.p2, p["W3"], self.h, dX=self.dp2, dW=g["W3"], db=g["b3"])
-        dmlnn.max_pool2d_bwd(self.dp2, self.i2, 64, 14, 14, 2, 2, 2, 0, dX=self.dc2)
-        dmlnn.conv2d_backward_filter(self.p1, self.dc2, self.c2, 32, 14, 14, 5, 5, 1, 2, 64,
+        dmlnn.max_pool2d_bwd_relu(self.dp2, self.i2, self.p2, 64, 14, 14, 2, 2, 2, 0,
+                                  dX=self.dc2)
+        dmlnn.conv2d_backward_filter(self.p1, self.dc2, None, 32, 14, 14, 5, 5, 1, 2, 64,
                                      workspace=self.ws2, dW=g["W2"], db=g["b2"])
-        dmlnn.conv2d_backward_data(p["W2"], self.dc2, self.c2, 32, 14, 14, 5, 5, 1, 2,
+        dmlnn.conv2d_backward_data(p["W2"], self.dc2, None, 32, 14, 14, 5, 5, 1, 2,
                                    dX=self.dp1)
-        dmlnn.max_pool2d_bwd(self.dp1, self.i1, 32, 28, 28, 2, 2, 2, 0, dX=self.dc1)
-        dmlnn.conv2d_backward_filter(X, self.dc1, self.c1, 1, 28, 28, 5, 5, 1, 2, 32,
+        dmlnn.max_pool2d_bwd_relu(self.dp1, self.i1, self.p1, 32, 28, 28, 2, 2, 2, 0,
+                                  dX=self.dc1)
+        dmlnn.conv2d_backward_filter(X, self.dc1, None, 1, 28, 28, 5, 5, 1, 2, 32,
                                      workspace=self.ws1, dW=g["W1"], db=g["b1"])
         return self.loss
 
@@ -99,17 +104,16 @@ class LeNetScorer:
         e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
         i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
         B = batch
-        self.buf = [dict(c1=e(B, 32 * 784), p1=e(B, 32 * 196), i1=i32(B, 32 * 196),
-                         c2=e(B, 64 * 196), p2=e(B, 64 * 49), i2=i32(B, 64 * 49),
+        self.buf = [dict(p1=e(B, 32 * 196), i1=i32(B, 32 * 196),
+                         p2=e(B, 64 * 49), i2=i32(B, 64 * 49),
                          h=e(B, 512), s=e(B, 10)) for _ in range(streams)]
 
     def _forward(self, X, out, b):
         p = self.p
-        dmlnn.conv2d_forward(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, relu=True, out=b["c1"])
-        dmlnn.max_pool2d_fwd(b["c1"], 32, 28, 28, 2, 2, 2, 0, out=b["p1"], argmax=b["i1"])
-        dmlnn.conv2d_forward(b["p1"], p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, relu=True,
-                             out=b["c2"])
-        dmlnn.max_pool2d_fwd(b["c2"], 64, 14, 14, 2, 2, 2, 0, out=b["p2"], argmax=b["i2"])
+        dmlnn.conv2d_forward_pool(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, 2, 2, 2, 0,
+                                  pooled=b["p1"], argmax=b["i1"])
+        dmlnn.conv2d_forward_pool(b["p1"], p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, 2, 2, 2, 0,
+                                  pooled=b["p2"], argmax=b["i2"])
         dmlnn.affine_fwd(b["p2"], p["W3"], p["b3"], relu=True, out=b["h"])
         dmlnn.affine_fwd(b["h"], p["W4"], p["b4"], relu=False, out=b["s"])
         dmlnn.softmax_fwd(b["s"], probs=out)

@@ -1,0 +1,82 @@
+"""Vertical fusion: conv2d + bias + relu + max_pool2d in one call, and the pool
+backward with the relu mask folded in.  Checked against the oracle: the conv
+output within tolerance, and the pooled values / argmax exactly equal to the
+oracle's pooling of the call's own conv output (so a rounding difference in the
+convolution cannot move an argmax)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_close, dev, host, rounded
+from paper_1802_04647_amd import dmlnn
+from paper_1802_04647_amd.inputs import ConvShape, random_conv_case
+
+pytestmark = pytest.mark.gpu
+
+# (conv shape, pool_h, pool_w, pool_stride)
+CASES = [
+    (ConvShape(4, 1, 28, 28, 32, 5, 5, 1, 2), 2, 2, 2),    # LeNet conv1 + pool1 (F <= 32 path)
+    (ConvShape(3, 32, 14, 14, 64, 5, 5, 1, 2), 2, 2, 2),   # LeNet conv2 + pool2 (one tile/image)
+    (ConvShape(1, 8, 56, 56, 70, 3, 3, 1, 1), 2, 2, 2),    # two filter tiles, 56-wide rows
+    (ConvShape(2, 3, 15, 13, 5, 3, 3, 1, 1), 3, 3, 3),     # windows leave trailing rows/cols
+    (ConvShape(2, 4, 10, 20, 6, 3, 3, 1, 1), 2, 3, 3),     # gaps between windows
+    (ConvShape(1, 5, 17, 9, 3, 3, 3, 2, 1), 1, 1, 1),      # 1x1 pool (identity)
+]
+
+
+def _fused(s, X, W, b, dt, ph, pw, ps, keep):
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    out, pooled, idx, Hp, Wp = dmlnn.conv2d_forward_pool(dev(X, dt), dev(W, dt), dev(b, dt), *a,
+                                                        ph, pw, ps, 0, keep_out=keep)
+    torch.cuda.synchronize()
+    return (host(out) if out is not None else None), host(pooled), idx.cpu().numpy(), Hp, Wp
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"{c[0]}-pool{c[1]}x{c[2]}s{c[3]}")
+def test_conv_forward_pool(case, dt):
+    s, ph, pw, ps = case
+    X0, W0, b0, _ = random_conv_case(31, s, zero_frac=0.3)
+    X, W, b = (rounded(v, dt) for v in (X0, W0, b0))
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    out, pooled, idx, Hp, Wp = _fused(s, X, W, b, dt, ph, pw, ps, keep=True)
+    ref_out, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
+    assert_close(out, ref_out, dt, "conv out")
+    rp, ri, _, _ = oracle.max_pool2d_fwd(out, s.F, s.Hout, s.Wout, ph, pw, ps, 0)
+    assert np.array_equal(pooled, rp)
+    assert np.array_equal(idx, ri)
+    # without the conv output buffer: same pooled values and indices
+    none_out, pooled2, idx2, _, _ = _fused(s, X, W, b, dt, ph, pw, ps, keep=False)
+    assert none_out is None
+    assert np.array_equal(pooled2, pooled) and np.array_equal(idx2, idx)
+
+
+def test_conv_forward_pool_unfusable_needs_out():
+    s = ConvShape(1, 2, 9, 9, 3, 3, 3, 1, 1)
+    X, W, b, _ = random_conv_case(5, s)
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    # overlapping windows (stride 1 < 3) are not fused: the call runs conv then pool
+    out, pooled, idx, Hp, Wp = dmlnn.conv2d_forward_pool(dev(X, "f64"), dev(W, "f64"),
+                                                        dev(b, "f64"), *a, 3, 3, 1, 0,
+                                                        keep_out=True)
+    torch.cuda.synchronize()
+    rp, ri, _, _ = oracle.max_pool2d_fwd(host(out), s.F, s.Hout, s.Wout, 3, 3, 1, 0)
+    assert np.array_equal(host(pooled), rp) and np.array_equal(idx.cpu().numpy(), ri)
+    with pytest.raises(dmlnn.DmlnnError):
+        dmlnn.conv2d_forward_pool(dev(X, "f64"), dev(W, "f64"), dev(b, "f64"), *a, 3, 3, 1, 0)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_max_pool2d_bwd_relu(dt):
+    r = np.random.default_rng(77)
+    N, C, H, Wd = 3, 5, 12, 10
+    Xp = rounded(np.maximum(r.standard_normal((N, C * H * Wd)), 0.0), dt)   # relu output
+    pooled, idx, Ho, Wo = oracle.max_pool2d_fwd(Xp, C, H, Wd, 2, 2, 2, 0)
+    dout = rounded(r.standard_normal(pooled.shape), dt)
+    got = dmlnn.max_pool2d_bwd_relu(dev(dout, dt), torch.from_numpy(idx).cuda(),
+                                    dev(pooled, dt), C, H, Wd, 2, 2, 2, 0)
+    torch.cuda.synchronize()
+    # routing is linear: masking the pooled gradient first gives the same result
+    ref = oracle.max_pool2d_bwd(dout * (pooled > 0), idx, C, H, Wd, 2, 2, 2, 0)
+    assert np.array_equal(host(got), ref)

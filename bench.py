@@ -172,6 +172,34 @@ def scoring_timing(M=4096):
     return res
 
 
+def horizontal_fusion_timing():
+    """Three 3x3 filter banks (16, 16 and 32 filters) over one 256 x 64 x 28x28
+    input: one horizontally fused launch (the banks fill one 64-row tile, so each
+    input tile is staged once for all of them) against three conv2d_forward
+    calls (fp64)."""
+    import torch
+    from paper_1802_04647_amd import dmlnn
+
+    g = torch.Generator(device="cuda").manual_seed(7)
+    N, C, H, Fs = 256, 64, 28, (16, 16, 32)
+    X = torch.relu(torch.randn((N, C * H * H), dtype=torch.float64, device="cuda", generator=g))
+    Ws = [torch.randn((F, C * 9), dtype=torch.float64, device="cuda", generator=g) * 0.06
+          for F in Fs]
+    bs = [torch.zeros(F, dtype=torch.float64, device="cuda") for F in Fs]
+    outs = [torch.empty((N, F * H * H), dtype=torch.float64, device="cuda") for F in Fs]
+    Wcat, bcat = torch.cat(Ws).contiguous(), torch.cat(bs).contiguous()
+    a = (C, H, H, 3, 3, 1, 1)
+    fused = _median_ms(lambda: dmlnn.conv2d_forward_multi(X, Ws, bs, *a, outs=outs, Wcat=Wcat,
+                                                          bcat=bcat))
+    sep = _median_ms(lambda: [dmlnn.conv2d_forward(X, W, b, *a, out=o)
+                              for W, b, o in zip(Ws, bs, outs)])
+    flops = 2.0 * N * sum(Fs) * H * H * C * 9
+    return {"shape": "256 x 64 x 28x28, banks of 16, 16 and 32 filters 3x3 p1, fp64",
+            "fused_ms": round(fused, 4), "separate_ms": round(sep, 4),
+            "fused_tflops": round(flops / (fused / 1e3) / 1e12, 3),
+            "separate_tflops": round(flops / (sep / 1e3) / 1e12, 3)}
+
+
 def conv_config_timing():
     """Per-pass GFLOP/s of the LeNet conv layers (configs 2 and 3) in fp64 and fp32."""
     import torch
@@ -414,6 +442,7 @@ def main():
                                  "images_per_s": round(lt["images_per_s"], 1)}
         rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
+        rec["horizontal_fusion"] = horizontal_fusion_timing()
         rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline()

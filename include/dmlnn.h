@@ -167,6 +167,22 @@ DMLNN_API int conv2d_forward_pool(dmlnn_dtype dtype, const void *X, const void *
                                   int pool_h, int pool_w, int pool_stride, int pool_pad,
                                   void *stream);
 
+/* ----------------------------------------------------- conv2d_forward_multi ----
+ * Paper: Section "Future Work" (horizontal fusion for shared inputs: several
+ * conv operators consuming the same input reuse one im2col intermediate).
+ * nbanks (1..8) filter banks with the same Hf, Wf, stride and pad run over one
+ * input X as one implicit GEMM whose rows are the banks' filters stacked:
+ *   outs[b] = relu?(conv2d(X, W_b) + b_b)        (each as conv2d_forward)
+ * Wcat is the banks' filters stacked row-wise ((sum Fs) x C*Hf*Wf), bcat their
+ * biases stacked (NULL for none); outs (host array of nbanks device pointers)
+ * and Fs (host array of nbanks filter counts) are read during the call only.
+ * outs[b] is N x (Fs[b]*Hout*Wout).  Each input tile is staged once for every
+ * 64 stacked filters. */
+DMLNN_API int conv2d_forward_multi(dmlnn_dtype dtype, const void *X, const void *Wcat,
+                                   const void *bcat, void *const *outs, const int *Fs,
+                                   int nbanks, int N, int C, int Hin, int Win, int Hf, int Wf,
+                                   int stride, int pad, int relu, void *stream);
+
 /* ------------------------------------------------------ max_pool2d_bwd_relu ----
  * The backward of relu -> max_pool2d with the relu mask folded in, so that the
  * conv backward passes can take the result as dout with out_fwd = NULL (and the

@@ -243,6 +243,47 @@ int max_pool2d_bwd(dmlnn_dtype dtype, const void *dout, const int32_t *argmax, v
                     "max_pool2d_bwd");
 }
 
+int conv2d_forward_multi(dmlnn_dtype dtype, const void *X, const void *Wcat, const void *bcat,
+                         void *const *outs, const int *Fs, int nbanks, int N, int C, int Hin,
+                         int Win, int Hf, int Wf, int stride, int pad, int relu, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_forward_multi: bad dtype %d", (int)dtype);
+    if (!X || !Wcat || !outs || !Fs)
+        return fail(DMLNN_ERR_NULL, "conv2d_forward_multi: X, Wcat, outs and Fs are required");
+    if (nbanks < 1 || nbanks > 8)
+        return fail(DMLNN_ERR_ARG, "conv2d_forward_multi: nbanks=%d outside [1, 8]", nbanks);
+    long long Ftot = 0;
+    for (int b = 0; b < nbanks; ++b) {
+        if (Fs[b] < 1) return fail(DMLNN_ERR_ARG, "conv2d_forward_multi: bank %d has F=%d", b, Fs[b]);
+        if (!outs[b]) return fail(DMLNN_ERR_NULL, "conv2d_forward_multi: outs[%d] is NULL", b);
+        Ftot += Fs[b];
+    }
+    if (Ftot > INT_MAX) return fail(DMLNN_ERR_ARG, "conv2d_forward_multi: too many filters");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, (int)Ftot, Hf, Wf, stride, pad)) return r;
+    if (int r = device_check()) return r;
+    const hipStream_t s = (hipStream_t)stream;
+    hipError_t e = dmlnn::launch_conv_forward_multi(dtype, X, Wcat, bcat, outs, Fs, nbanks, d,
+                                                    relu, zero_skip_mode(), s);
+    if (e == hipErrorNotSupported) {
+        // The register-staged path has no per-bank epilogue: one launch per bank.
+        (void)hipGetLastError();
+        const size_t tsz = dtype == DMLNN_F64 ? 8 : 4;
+        const size_t K = (size_t)C * Hf * Wf;
+        long long off = 0;
+        e = hipSuccess;
+        for (int b = 0; b < nbanks && e == hipSuccess; ++b) {
+            dmlnn::ConvDims db = d;
+            db.F = Fs[b];
+            const char *wb = (const char *)Wcat + (size_t)off * K * tsz;
+            const char *bb = bcat ? (const char *)bcat + (size_t)off * tsz : nullptr;
+            e = dmlnn::launch_conv_forward(dtype, X, wb, bb, outs[b], db, relu, zero_skip_mode(), s);
+            off += Fs[b];
+        }
+    }
+    return launched(e, "conv2d_forward_multi");
+}
+
 int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int32_t *argmax,
                         const void *pooled, void *dX, int N, int C, int Hin, int Win, int Hf,
                         int Wf, int stride, int pad, void *stream)

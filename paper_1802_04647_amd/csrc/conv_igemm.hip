@@ -29,6 +29,7 @@ namespace dmlnn {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kMaxBanks = 8;  // filter banks one horizontally fused launch may carry
 constexpr int kBM = 64;
 constexpr size_t kLdsBudget = 72 * 1024;  // two blocks per CU
 constexpr int kMS = 8;    // source-row slots each wave stages per chunk
@@ -59,6 +60,13 @@ struct IgemmArgs {
     void *pool_out;
     int32_t *pool_idx;
     int PH, PW, PS, Hp, Wp;
+    // Horizontal fusion (forward): rows [bank_off[b], bank_off[b+1]) of M belong
+    // to filter bank b, whose output is bank_out[b] ([N][F_b][Q]).  nbanks <= 1:
+    // a single output at out.
+    int nbanks;
+    int bank_off[kMaxBanks + 1];
+    void *bank_out[kMaxBanks];
+    int require_dma;  // 1: return hipErrorNotSupported instead of using the register path
     unsigned long long magic_kck, magic_hw, magic_wf;
 };
 
@@ -529,13 +537,23 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int y = 0; y < NB; ++y)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = mbase + x * 16 + MF::row(lane, r);
-                    const int q = q0 + (wn * NB + y) * 16 + (lane & 15);
-                    if (m < a.M && q < qend) out[(size_t)m * a.Q + q] = acc[x][y][r];
+            for (int r = 0; r < 4; ++r) {
+                const int m = mbase + x * 16 + MF::row(lane, r);
+                if (m >= a.M) continue;
+                T *orow = out + (size_t)m * a.Q;
+                if (!BWD && a.nbanks > 1) {  // the row's filter bank and its output
+                    int b = 0;
+                    while (b + 1 < a.nbanks && m >= a.bank_off[b + 1]) ++b;
+                    const int Fb = a.bank_off[b + 1] - a.bank_off[b];
+                    orow = reinterpret_cast<T *>(a.bank_out[b]) +
+                           ((size_t)n * Fb + (m - a.bank_off[b])) * a.Q;
                 }
+#pragma unroll
+                for (int y = 0; y < NB; ++y) {
+                    const int q = q0 + (wn * NB + y) * 16 + (lane & 15);
+                    if (q < qend) orow[q] = acc[x][y][r];
+                }
+            }
     }
     if (POOL) {
         // The tile is whole rows of conv output [y_lo, y_hi); the pooled rows
@@ -800,7 +818,7 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         default: return launch_dma<T, 1, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
         }
     }
-    if (pool) return hipErrorNotSupported;  // the fused epilogue is LDS-DMA only
+    if (pool || a.require_dma) return hipErrorNotSupported;  // fused epilogues: LDS-DMA only
     switch (p.NB) {
     case 7: return launch_nb<T, 7, BWD>(a, p, nimg, zero_skip, s);
     case 4: return launch_nb<T, 4, BWD>(a, p, nimg, zero_skip, s);
@@ -867,6 +885,39 @@ hipError_t launch_conv_forward_pool(int dtype, const void *X, const void *W, con
     if (dtype == 0)
         return launch_typed<double, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
     return launch_typed<float, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+}
+
+hipError_t launch_conv_forward_multi(int dtype, const void *X, const void *Wcat,
+                                     const void *bcat, void *const *outs, const int *Fs,
+                                     int nbanks, const ConvDims &d, int relu, int zero_skip,
+                                     hipStream_t s)
+{
+    if (nbanks < 1 || nbanks > kMaxBanks) return hipErrorInvalidValue;
+    IgemmArgs a = {};
+    a.src = X;
+    a.mask = nullptr;
+    a.wgt = Wcat;
+    a.bias = bcat;
+    a.out = outs[0];
+    a.Sh = d.Hin;
+    a.Sw = d.Win;
+    a.up = 1;
+    a.Hf = d.Hf;
+    a.Wf = d.Wf;
+    a.S = d.stride;
+    a.Ph = d.pad;
+    a.Pw = d.pad;
+    a.relu = relu;
+    a.nbanks = nbanks;
+    a.bank_off[0] = 0;
+    for (int b = 0; b < nbanks; ++b) {
+        a.bank_off[b + 1] = a.bank_off[b] + Fs[b];
+        a.bank_out[b] = outs[b];
+    }
+    a.require_dma = 1;
+    const int M = a.bank_off[nbanks];
+    if (dtype == 0) return launch_typed<double, false>(a, M, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+    return launch_typed<float, false>(a, M, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
 }
 
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,

@@ -23,6 +23,14 @@ hipError_t launch_conv_forward_pool(int dtype, const void *X, const void *W, con
                                     void *out, void *pooled, int32_t *argmax, const ConvDims &d,
                                     int relu, int ph, int pw, int ps, int Hp, int Wp,
                                     int zero_skip, hipStream_t s);
+// Several filter banks over one input in one launch (horizontal fusion): Wcat is
+// the banks' filters stacked ([sum F][C*Hf*Wf]), bcat their biases (or null);
+// bank b writes outs[b] ([N][Fs[b]*Hout*Wout]).  At most 8 banks.
+// hipErrorNotSupported when the shape needs the register-staged path.
+hipError_t launch_conv_forward_multi(int dtype, const void *X, const void *Wcat,
+                                     const void *bcat, void *const *outs, const int *Fs,
+                                     int nbanks, const ConvDims &d, int relu, int zero_skip,
+                                     hipStream_t s);
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
                                      const void *out_fwd, void *dX, const ConvDims &d,
                                      int zero_skip, hipStream_t s);

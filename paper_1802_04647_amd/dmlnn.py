@@ -67,6 +67,7 @@ def load():
                                      ctypes.c_longlong, _vp]),
         "softmax_fwd": (_i, [_i, _vp, _vp, _i, _i, _vp]),
         "conv2d_forward_pool": (_i, [_i] + [_vp] * 6 + [_i] * 14 + [_vp]),
+        "conv2d_forward_multi": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 10 + [_vp]),
         "max_pool2d_bwd_relu": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "sgd_update": (_i, [_i, _vp, _vp, ctypes.c_double, ctypes.c_longlong, _vp]),
         "sgd_nesterov_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
@@ -292,6 +293,37 @@ def conv2d_forward_pool(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, pool_h, pool_
         dt, _p(X), _p(W), _p(b), _p(out), _p(pooled), _p(argmax), N, C, Hin, Win, F, Hf, Wf,
         stride, pad, int(relu), pool_h, pool_w, pool_stride, pool_pad, _stream()))
     return out, pooled, argmax, Hp, Wp
+
+
+def conv2d_forward_multi(X, Ws, bs, C, Hin, Win, Hf, Wf, stride, pad, relu=True, outs=None,
+                         Wcat=None, bcat=None):
+    """Several filter banks over one input in one launch.  Ws / bs: lists of the
+    banks' filters (F_b x C*Hf*Wf) and biases (or None).  Wcat / bcat may pass the
+    stacked copies already made; returns the list of outputs."""
+    dt = _dtype(X, *Ws)
+    N, nb = X.shape[0], len(Ws)
+    Fs = [int(W.shape[0]) for W in Ws]
+    Hout = conv2d_out_dim(Hin, Hf, stride, pad)
+    Wout = conv2d_out_dim(Win, Wf, stride, pad)
+    _need(X, N * C * Hin * Win, "X")
+    for W, F in zip(Ws, Fs):
+        _need(W, F * C * Hf * Wf, "W")
+    if Wcat is None:
+        Wcat = torch.cat([W.reshape(F, -1) for W, F in zip(Ws, Fs)]).contiguous()
+    if bcat is None and bs is not None and any(b is not None for b in bs):
+        bcat = torch.cat([b if b is not None else torch.zeros(F, dtype=X.dtype, device=X.device)
+                          for b, F in zip(bs, Fs)]).contiguous()
+    if outs is None:
+        outs = [_empty((N, F * max(Hout, 0) * max(Wout, 0)), X) for F in Fs]
+    for o, F in zip(outs, Fs):
+        _need(o, N * F * max(Hout, 0) * max(Wout, 0), "out")
+    ptrs = (ctypes.c_void_p * nb)(*[_p(o) for o in outs])
+    fs = (ctypes.c_int * nb)(*Fs)
+    _check("conv2d_forward_multi", load().conv2d_forward_multi(
+        dt, _p(X), _p(Wcat), _p(bcat), ctypes.cast(ptrs, ctypes.c_void_p),
+        ctypes.cast(fs, ctypes.c_void_p), nb, N, C, Hin, Win, Hf, Wf, stride, pad, int(relu),
+        _stream()))
+    return outs
 
 
 def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, dX=None):

@@ -80,3 +80,29 @@ def test_max_pool2d_bwd_relu(dt):
     # routing is linear: masking the pooled gradient first gives the same result
     ref = oracle.max_pool2d_bwd(dout * (pooled > 0), idx, C, H, Wd, 2, 2, 2, 0)
     assert np.array_equal(host(got), ref)
+
+
+HCASES = [
+    (ConvShape(2, 5, 12, 11, 0, 3, 3, 1, 1), (16, 40, 70)),   # banks straddle 64-row tiles
+    (ConvShape(3, 4, 9, 9, 0, 3, 3, 2, 1), (16, 16)),         # 32 rows: the k-split path
+    (ConvShape(1, 3, 6, 500, 0, 3, 3, 1, 1), (5, 7)),         # wide rows: one launch per bank
+    (ConvShape(2, 64, 14, 14, 0, 1, 1, 1, 0), (64, 32, 8)),   # 1x1 banks (inception-style)
+]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("case", HCASES, ids=lambda c: f"{c[0]}-banks{c[1]}")
+def test_conv_forward_multi(case, dt):
+    s0, Fs = case
+    r = np.random.default_rng(sum(Fs) * 7 + s0.C)
+    X = rounded(np.maximum(r.standard_normal((s0.N, s0.C * s0.Hin * s0.Win)), 0), dt)
+    K = s0.C * s0.Hf * s0.Wf
+    Ws = [rounded(r.standard_normal((F, K)) * np.sqrt(2.0 / K), dt) for F in Fs]
+    bs = [rounded(r.standard_normal(F) * 0.1, dt) for F in Fs]
+    a = (s0.C, s0.Hin, s0.Win, s0.Hf, s0.Wf, s0.stride, s0.pad)
+    outs = dmlnn.conv2d_forward_multi(dev(X, dt), [dev(W, dt) for W in Ws],
+                                      [dev(b, dt) for b in bs], *a)
+    torch.cuda.synchronize()
+    for k, (W, b) in enumerate(zip(Ws, bs)):
+        ref, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
+        assert_close(host(outs[k]), ref, dt, f"bank {k}")

@@ -200,6 +200,52 @@ def horizontal_fusion_timing():
             "separate_tflops": round(flops / (sep / 1e3) / 1e12, 3)}
 
 
+def sparse_conv_timing():
+    """conv2d forward of a CSR input against the dense forward of the same matrix:
+    the LeNet conv1 layer (64 x 1x28x28, ~80% zeros) and a 256 x 16x56x56 input
+    with 98% zeros (fp64)."""
+    import numpy as np
+    import torch
+    from paper_1802_04647_amd import dmlnn
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    def csr_of(Xd):
+        # host-side CSR construction of the benchmark input (not timed)
+        X = Xd.cpu().numpy()
+        nz = X != 0
+        rowptr = np.concatenate([[0], np.cumsum(nz.sum(axis=1))]).astype(np.int32)
+        cols = np.nonzero(nz)[1].astype(np.int32)
+        return (torch.from_numpy(rowptr).cuda(), torch.from_numpy(cols).cuda(),
+                Xd[torch.from_numpy(nz).cuda()].contiguous())
+
+    res = {}
+    s = SHAPES["lenet_conv1"]
+    X0, W0, b0, _ = conv_layer_inputs("lenet_conv1")
+    cases = [("lenet_conv1", s, torch.from_numpy(X0).cuda(), torch.from_numpy(W0).cuda(),
+              torch.from_numpy(b0).cuda())]
+    g = torch.Generator(device="cuda").manual_seed(11)
+    N, C, H, F = 256, 16, 56, 32
+    Xs = torch.randn((N, C * H * H), dtype=torch.float64, device="cuda", generator=g)
+    Xs[torch.rand(Xs.shape, device="cuda", generator=g) < 0.98] = 0.0
+    from paper_1802_04647_amd.inputs import ConvShape
+    cases.append(("sparse_98pct_256x16x56x56", ConvShape(N, C, H, H, F, 3, 3, 1, 1), Xs,
+                  torch.randn((F, C * 9), dtype=torch.float64, device="cuda", generator=g) * 0.1,
+                  torch.zeros(F, dtype=torch.float64, device="cuda")))
+    for name, s, X, W, b in cases:
+        rowptr, cols, vals = csr_of(X)
+        a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+        out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=torch.float64, device="cuda")
+        ri = torch.empty(s.N * s.C * s.Hin + 1, dtype=torch.int32, device="cuda")
+        csr_ms = _median_ms(lambda: dmlnn.conv2d_forward_csr(rowptr, cols, vals, W, b, *a,
+                                                             out=out, row_index=ri))
+        dense_ms = _median_ms(lambda: dmlnn.conv2d_forward(X, W, b, *a, out=out))
+        res[name] = {"density": round(vals.numel() / X.numel(), 4), "csr_ms": round(csr_ms, 4),
+                     "dense_ms": round(dense_ms, 4),
+                     "csr_bytes": int(vals.numel() * 12 + rowptr.numel() * 4),
+                     "dense_bytes": int(X.numel() * 8)}
+    return res
+
+
 def conv_config_timing():
     """Per-pass GFLOP/s of the LeNet conv layers (configs 2 and 3) in fp64 and fp32."""
     import torch
@@ -443,6 +489,7 @@ def main():
         rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
         rec["horizontal_fusion"] = horizontal_fusion_timing()
+        rec["sparse_conv"] = sparse_conv_timing()
         rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline()

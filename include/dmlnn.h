@@ -167,6 +167,22 @@ DMLNN_API int conv2d_forward_pool(dmlnn_dtype dtype, const void *X, const void *
                                   int pool_h, int pool_w, int pool_stride, int pool_pad,
                                   void *stream);
 
+/* ------------------------------------------------------- conv2d_forward_csr ----
+ * Paper: Section 3, "Sparse Operations" (the sparse-input / dense-filter conv2d
+ * operator, chosen by the number of non-zeros).  Same result as conv2d_forward
+ * with X given in CSR form: X is the N x (C*Hin*Win) matrix with row n holding
+ * the values vals[rowptr[n] .. rowptr[n+1]) at columns colidx[...] (in-row index
+ * c*Hin*Win + h*Win + w, strictly increasing within a row); rowptr has N+1
+ * entries with rowptr[0] = 0 and rowptr[N] = nnz.  All arrays live in device
+ * memory; row_index is a caller workspace of N*C*Hin + 1 int32 (overwritten).
+ * The kernel stages each input window from the CSR arrays (only non-zeros are
+ * read); entries that break the format are ignored rather than read or written
+ * out of bounds.  Below 5% density it uses the zero-fragment skip. */
+DMLNN_API int conv2d_forward_csr(dmlnn_dtype dtype, const int32_t *rowptr, const int32_t *colidx,
+                                 const void *vals, int nnz, int32_t *row_index, const void *W,
+                                 const void *b, void *out, int N, int C, int Hin, int Win, int F,
+                                 int Hf, int Wf, int stride, int pad, int relu, void *stream);
+
 /* ----------------------------------------------------- conv2d_forward_multi ----
  * Paper: Section "Future Work" (horizontal fusion for shared inputs: several
  * conv operators consuming the same input reuse one im2col intermediate).

@@ -284,6 +284,30 @@ int conv2d_forward_multi(dmlnn_dtype dtype, const void *X, const void *Wcat, con
     return launched(e, "conv2d_forward_multi");
 }
 
+int conv2d_forward_csr(dmlnn_dtype dtype, const int32_t *rowptr, const int32_t *colidx,
+                       const void *vals, int nnz, int32_t *row_index, const void *W,
+                       const void *b, void *out, int N, int C, int Hin, int Win, int F, int Hf,
+                       int Wf, int stride, int pad, int relu, void *stream)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_forward_csr: bad dtype %d", (int)dtype);
+    if (!rowptr || !row_index || !W || !out || (nnz > 0 && (!colidx || !vals)))
+        return fail(DMLNN_ERR_NULL,
+                    "conv2d_forward_csr: rowptr, row_index, W, out (and colidx, vals if nnz > 0) "
+                    "are required");
+    if (nnz < 0) return fail(DMLNN_ERR_ARG, "conv2d_forward_csr: bad nnz=%d", nnz);
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    if (nnz > (long long)N * C * Hin * Win)
+        return fail(DMLNN_ERR_ARG, "conv2d_forward_csr: nnz=%d exceeds the matrix size", nnz);
+    if (int r = device_check()) return r;
+    // nnz-driven choice: below 5% density whole MFMA fragments of the staged
+    // window are likely zero, so the ballot-skip kernel is used.
+    const int skip = zero_skip_mode() || (long long)nnz * 20 < (long long)N * C * Hin * Win;
+    return launched(dmlnn::launch_conv_forward_csr(dtype, rowptr, colidx, vals, nnz, row_index, W,
+                                                   b, out, d, relu, skip, (hipStream_t)stream),
+                    "conv2d_forward_csr");
+}
+
 int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int32_t *argmax,
                         const void *pooled, void *dX, int N, int C, int Hin, int Win, int Hf,
                         int Wf, int stride, int pad, void *stream)

@@ -67,10 +67,19 @@ struct IgemmArgs {
     int bank_off[kMaxBanks + 1];
     void *bank_out[kMaxBanks];
     int require_dma;  // 1: return hipErrorNotSupported instead of using the register path
+    // Sparse input (forward, register-staged kernel): X given in CSR; csr_row
+    // holds, for every image row (n, c, y), the position of its first non-zero
+    // (N*Cs*Sh + 1 entries, the last = nnz), csr_col / csr_val the CSR columns
+    // (c*Sh*Sw + y*Sw + x) and values.
+    int csr;  // 1: the input is the CSR arrays below (csr_col / csr_val may be
+              // null when there are no non-zeros)
+    const int32_t *csr_row;
+    const int32_t *csr_col;
+    const void *csr_val;
     unsigned long long magic_kck, magic_hw, magic_wf;
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool CSR = false>
 __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 {
     using MF = Mfma<T>;
@@ -199,7 +208,28 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
     // Fallback for chunks larger than the staging registers: load and store
     // directly (one memory round trip per row slot; correct for any size).
     auto stage_direct = [&](int c0) {
-        for (int r = wave; r < nrows; r += kThreads / kWave) {
+        if (CSR) {
+            // Each wave zeroes its window rows, then scatters the row's non-zeros
+            // (LDS writes of one wave land in issue order).  Columns outside the
+            // row are ignored, so malformed input cannot write outside LDS.
+            const T *val = reinterpret_cast<const T *>(a.csr_val);
+            for (int r = wave; r < nrows; r += kThreads / kWave) {
+                const int c = r / rows_need, t = r - c * rows_need;
+                const int cg = c0 + c, yv = ybase + t;
+                T *dst = s_src + r * a.Wpad;
+                for (int u = lane; u < a.Wpad; u += kWave) dst[u] = T(0);
+                if (cg < a.Cs && yv >= 0 && yv < a.Sh) {
+                    const size_t ri = ((size_t)n * a.Cs + cg) * a.Sh + yv;
+                    const int kb = a.csr_row[ri], ke = a.csr_row[ri + 1];
+                    const int base = (cg * a.Sh + yv) * a.Sw;
+                    for (int k = kb + lane; k < ke; k += kWave) {
+                        const int x = a.csr_col[k] - base;
+                        if (x >= 0 && x < a.Sw) dst[x + a.Pw] = val[k];
+                    }
+                }
+            }
+        }
+        for (int r = wave; !CSR && r < nrows; r += kThreads / kWave) {
             const int c = r / rows_need, t = r - c * rows_need;
             const int cg = c0 + c, yv = ybase + t;
             const int ys = yv / a.up;
@@ -288,8 +318,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 // element lies outside the image (or beyond the tensor) get an out-of-range
 // offset and write 0.  Each lane's byte offset within a chunk is the same for
 // every chunk and stays in a register; the chunk's channel offset is the scalar
-// soffset.  In the backward pass the relu mask source is copied alongside and
-// applied as B fragments are read.
+// soffset.  In the backward pass the relu mask source is copied into one LDS
+// window and folded into the chunk's source window before its MFMAs.
 constexpr int kMaxDmaS = 12;  // source-window DMA instructions per wave per chunk
 constexpr int kMaxDmaA = 20;  // filter-slice DMA instructions per wave per chunk
 constexpr size_t kLdsPerBlock = 80 * 1024;  // two blocks per CU (160 KiB)
@@ -754,6 +784,13 @@ hipError_t launch_nb(const IgemmArgs &a, const Plan &p, int nimg, int zero_skip,
 {
     dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
     hipError_t e;
+    if (!BWD && a.csr) {
+        auto k = zero_skip ? conv_igemm_kernel<T, NB, false, true, true>
+                           : conv_igemm_kernel<T, NB, false, false, true>;
+        if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
+        return hipGetLastError();
+    }
     if (zero_skip) {
         auto k = conv_igemm_kernel<T, NB, BWD, true>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
@@ -793,9 +830,10 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
 
     const size_t img_bytes = (size_t)Cs * a.Sh * a.Sw * sizeof(T);
     const size_t w_bytes = (size_t)M * Cs * a.HfWf * sizeof(T);
+    if (a.csr) a.pipelined = 0;  // sparse staging is the direct path only
     Plan pd = p;
     DmaLayout L;
-    if (make_dma_plan(sizeof(T), BWD, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
+    if (!a.csr && make_dma_plan(sizeof(T), BWD, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
                       L)) {
         IgemmArgs ad = a;
         ad.KC = pd.KC;
@@ -918,6 +956,74 @@ hipError_t launch_conv_forward_multi(int dtype, const void *X, const void *Wcat,
     const int M = a.bank_off[nbanks];
     if (dtype == 0) return launch_typed<double, false>(a, M, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
     return launch_typed<float, false>(a, M, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+}
+
+namespace {
+// row_index[i] for image row i = (n, c, y): the first position of CSR row n whose
+// column is >= c*Hin*Win + y*Win (binary search within the row's range, which is
+// clamped to [0, nnz], so any rowptr keeps every read in bounds).
+__global__ __launch_bounds__(256) void csr_row_index_kernel(const int32_t *rowptr,
+                                                            const int32_t *colidx, int nnz,
+                                                            int32_t *row_index, int N, int C,
+                                                            int Hin, int Win)
+{
+    const long long total = (long long)N * C * Hin;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i <= total;
+         i += (long long)gridDim.x * 256) {
+        if (i == total) {
+            row_index[i] = min(max(rowptr[N], 0), nnz);
+            continue;
+        }
+        const int n = (int)(i / ((long long)C * Hin));
+        const int cy = (int)(i - (long long)n * C * Hin);  // c*Hin + y
+        int lo = min(max(rowptr[n], 0), nnz);
+        int hi = min(max(rowptr[n + 1], lo), nnz);
+        const int key = cy * Win;
+        while (lo < hi) {
+            const int mid = lo + (hi - lo) / 2;
+            if (colidx[mid] < key)
+                lo = mid + 1;
+            else
+                hi = mid;
+        }
+        row_index[i] = lo;
+    }
+}
+}  // namespace
+
+hipError_t launch_conv_forward_csr(int dtype, const int32_t *rowptr, const int32_t *colidx,
+                                   const void *vals, int nnz, int32_t *row_index, const void *W,
+                                   const void *b, void *out, const ConvDims &d, int relu,
+                                   int zero_skip, hipStream_t s)
+{
+    const long long rows = (long long)d.N * d.C * d.Hin + 1;
+    long long g = (rows + 255) / 256;
+    if (g > 4096) g = 4096;
+    hipLaunchKernelGGL(csr_row_index_kernel, dim3((int)g), dim3(256), 0, s, rowptr, colidx, nnz,
+                       row_index, d.N, d.C, d.Hin, d.Win);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    IgemmArgs a = {};
+    a.src = nullptr;  // not read: the staging takes the CSR arrays
+    a.wgt = W;
+    a.bias = b;
+    a.out = out;
+    a.Sh = d.Hin;
+    a.Sw = d.Win;
+    a.up = 1;
+    a.Hf = d.Hf;
+    a.Wf = d.Wf;
+    a.S = d.stride;
+    a.Ph = d.pad;
+    a.Pw = d.pad;
+    a.relu = relu;
+    a.csr = 1;
+    a.csr_row = row_index;
+    a.csr_col = colidx;
+    a.csr_val = vals;
+    if (dtype == 0)
+        return launch_typed<double, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
+    return launch_typed<float, false>(a, d.F, d.C, d.Hout, d.Wout, d.N, zero_skip, s);
 }
 
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,

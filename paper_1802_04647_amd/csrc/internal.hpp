@@ -31,6 +31,12 @@ hipError_t launch_conv_forward_multi(int dtype, const void *X, const void *Wcat,
                                      const void *bcat, void *const *outs, const int *Fs,
                                      int nbanks, const ConvDims &d, int relu, int zero_skip,
                                      hipStream_t s);
+// Sparse-input forward: X as CSR (rowptr N+1, colidx/vals nnz); row_index is a
+// caller workspace of N*C*Hin + 1 int32.
+hipError_t launch_conv_forward_csr(int dtype, const int32_t *rowptr, const int32_t *colidx,
+                                   const void *vals, int nnz, int32_t *row_index, const void *W,
+                                   const void *b, void *out, const ConvDims &d, int relu,
+                                   int zero_skip, hipStream_t s);
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
                                      const void *out_fwd, void *dX, const ConvDims &d,
                                      int zero_skip, hipStream_t s);

@@ -68,6 +68,8 @@ def load():
         "softmax_fwd": (_i, [_i, _vp, _vp, _i, _i, _vp]),
         "conv2d_forward_pool": (_i, [_i] + [_vp] * 6 + [_i] * 14 + [_vp]),
         "conv2d_forward_multi": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 10 + [_vp]),
+        "conv2d_forward_csr": (_i, [_i, _vp, _vp, _vp, _i, _vp, _vp, _vp, _vp] + [_i] * 10
+                               + [_vp]),
         "max_pool2d_bwd_relu": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "sgd_update": (_i, [_i, _vp, _vp, ctypes.c_double, ctypes.c_longlong, _vp]),
         "sgd_nesterov_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
@@ -293,6 +295,32 @@ def conv2d_forward_pool(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, pool_h, pool_
         dt, _p(X), _p(W), _p(b), _p(out), _p(pooled), _p(argmax), N, C, Hin, Win, F, Hf, Wf,
         stride, pad, int(relu), pool_h, pool_w, pool_stride, pool_pad, _stream()))
     return out, pooled, argmax, Hp, Wp
+
+
+def conv2d_forward_csr(rowptr, colidx, vals, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True,
+                       out=None, row_index=None):
+    """conv2d forward of a CSR input (N x C*Hin*Win; int32 rowptr/colidx on the device)."""
+    dt = _dtype(vals, W, b, out)
+    N, F = rowptr.numel() - 1, W.shape[0]
+    nnz = colidx.numel()
+    if rowptr.dtype != torch.int32 or colidx.dtype != torch.int32:
+        raise TypeError("rowptr and colidx must be int32")
+    _need(vals, nnz, "vals")
+    _need(W, F * C * Hf * Wf, "W")
+    _need(b, F, "b")
+    Hout = conv2d_out_dim(Hin, Hf, stride, pad)
+    Wout = conv2d_out_dim(Win, Wf, stride, pad)
+    if out is None:
+        out = _empty((N, F * max(Hout, 0) * max(Wout, 0)), W)
+    if row_index is None:
+        row_index = torch.empty(N * C * Hin + 1, dtype=torch.int32, device=W.device)
+    _need(out, N * F * max(Hout, 0) * max(Wout, 0), "out")
+    _need(row_index, N * C * Hin + 1, "row_index")
+    _check("conv2d_forward_csr", load().conv2d_forward_csr(
+        dt, _p(rowptr), _p(colidx) if nnz else None, _p(vals) if nnz else None, nnz,
+        _p(row_index), _p(W), _p(b), _p(out), N, C, Hin, Win, F, Hf, Wf, stride, pad,
+        int(relu), _stream()))
+    return out
 
 
 def conv2d_forward_multi(X, Ws, bs, C, Hin, Win, Hf, Wf, stride, pad, relu=True, outs=None,

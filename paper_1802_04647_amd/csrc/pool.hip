@@ -52,44 +52,58 @@ __global__ __launch_bounds__(256) void max_pool_fwd_kernel(const T *__restrict__
     }
 }
 
+// One thread per input cell of a (n, c) plane: blockIdx.y walks the planes,
+// blockIdx.x * 256 + threadIdx.x the cells (32-bit index math per plane).
 template <typename T>
 __global__ __launch_bounds__(256) void max_pool_bwd_kernel(const T *__restrict__ dout,
                                                            const int32_t *__restrict__ argmax,
                                                            const T *__restrict__ pooled,
-                                                           T *__restrict__ dX, long long total,
+                                                           T *__restrict__ dX, long long planes,
                                                            int C, int Hin, int Win, int Hf,
                                                            int Wf, int S, int P, int Hout,
                                                            int Wout)
 {
-    for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total;
-         e += (long long)gridDim.x * 256) {
-        const int w = (int)(e % Win);
-        long long r = e / Win;
-        const int h = (int)(r % Hin);
-        r /= Hin;
-        const int c = (int)(r % C);
-        const long long n = r / C;
-        const int32_t me = c * Hin * Win + h * Win + w;
-        const size_t obase = (size_t)n * C * Hout * Wout + (size_t)c * Hout * Wout;
-        // outputs (oh, ow) whose window [oh*S-P, oh*S-P+Hf) contains h
-        int oh_lo = h + P - Hf + 1;
-        oh_lo = oh_lo <= 0 ? 0 : (oh_lo + S - 1) / S;
-        int oh_hi = (h + P) / S;
-        if (oh_hi > Hout - 1) oh_hi = Hout - 1;
-        int ow_lo = w + P - Wf + 1;
-        ow_lo = ow_lo <= 0 ? 0 : (ow_lo + S - 1) / S;
-        int ow_hi = (w + P) / S;
-        if (ow_hi > Wout - 1) ow_hi = Wout - 1;
-        T acc = T(0);
-        for (int oh = oh_lo; oh <= oh_hi; ++oh)
-            for (int ow = ow_lo; ow <= ow_hi; ++ow) {
-                const size_t o = obase + (size_t)oh * Wout + ow;
-                // with pooled given, the relu before the pool gates the route:
-                // the routed cell holds the pooled value, so its relu mask is
-                // pooled > 0
-                if (argmax[o] == me && (!pooled || pooled[o] > T(0))) acc += dout[o];
+    const int HW = Hin * Win;
+    const bool disjoint = S >= Hf && S >= Wf && P == 0;
+    for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
+        const int c = (int)(pl % C);
+        const size_t obase = (size_t)pl * Hout * Wout;
+        T *dXp = dX + (size_t)pl * HW;
+        for (int idx = blockIdx.x * 256 + threadIdx.x; idx < HW; idx += gridDim.x * 256) {
+            const int h = idx / Win, w = idx - (idx / Win) * Win;
+            const int32_t me = c * HW + idx;
+            if (disjoint) {
+                // Windows do not overlap: at most one window covers the cell.
+                const int oh = h / S, ow = w / S;
+                // (the three reads are independent, so they are issued together)
+                const bool in = oh < Hout && ow < Wout && h - oh * S < Hf && w - ow * S < Wf;
+                const size_t o = in ? obase + (size_t)oh * Wout + ow : obase;
+                const int32_t am = argmax[o];
+                const T d = dout[o];
+                const T pv = pooled ? pooled[o] : T(1);
+                dXp[idx] = (in && am == me && pv > T(0)) ? d : T(0);
+                continue;
             }
-        dX[e] = acc;
+            // outputs (oh, ow) whose window [oh*S-P, oh*S-P+Hf) contains h
+            int oh_lo = h + P - Hf + 1;
+            oh_lo = oh_lo <= 0 ? 0 : (oh_lo + S - 1) / S;
+            int oh_hi = (h + P) / S;
+            if (oh_hi > Hout - 1) oh_hi = Hout - 1;
+            int ow_lo = w + P - Wf + 1;
+            ow_lo = ow_lo <= 0 ? 0 : (ow_lo + S - 1) / S;
+            int ow_hi = (w + P) / S;
+            if (ow_hi > Wout - 1) ow_hi = Wout - 1;
+            T acc = T(0);
+            for (int oh = oh_lo; oh <= oh_hi; ++oh)
+                for (int ow = ow_lo; ow <= ow_hi; ++ow) {
+                    const size_t o = obase + (size_t)oh * Wout + ow;
+                    // with pooled given, the relu before the pool gates the route:
+                    // the routed cell holds the pooled value, so its relu mask is
+                    // pooled > 0
+                    if (argmax[o] == me && (!pooled || pooled[o] > T(0))) acc += dout[o];
+                }
+            dXp[idx] = acc;
+        }
     }
 }
 
@@ -124,18 +138,24 @@ hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argma
                                int Hf, int Wf, int stride, int pad, int Hout, int Wout,
                                hipStream_t s)
 {
-    const long long total = (long long)N * C * Hin * Win;
-    const int g = grid_for(total);
+    const long long planes = (long long)N * C;
+    const int HW = Hin * Win;
+    // About 16k blocks in all, each thread walking several cells and planes:
+    // tiny one-element blocks would leave the dispatcher as the bottleneck.
+    int gx = (HW + 1023) / 1024;
+    if (gx > 8) gx = 8;
+    long long gy = planes;
+    const long long cap = 16384 / gx;
+    if (gy > cap) gy = cap;
+    const dim3 grid(gx, (unsigned)gy);
     if (dtype == 0)
-        hipLaunchKernelGGL(max_pool_bwd_kernel<double>, dim3(g), dim3(256), 0, s,
+        hipLaunchKernelGGL(max_pool_bwd_kernel<double>, grid, dim3(256), 0, s,
                            (const double *)dout, argmax, (const double *)pooled, (double *)dX,
-                           total, C, Hin, Win, Hf, Wf,
-                           stride, pad, Hout, Wout);
+                           planes, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout);
     else
-        hipLaunchKernelGGL(max_pool_bwd_kernel<float>, dim3(g), dim3(256), 0, s,
-                           (const float *)dout, argmax, (const float *)pooled, (float *)dX, total,
-                           C, Hin, Win, Hf, Wf,
-                           stride, pad, Hout, Wout);
+        hipLaunchKernelGGL(max_pool_bwd_kernel<float>, grid, dim3(256), 0, s,
+                           (const float *)dout, argmax, (const float *)pooled, (float *)dX,
+                           planes, C, Hin, Win, Hf, Wf, stride, pad, Hout, Wout);
     return hipGetLastError();
 }
 

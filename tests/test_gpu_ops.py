@@ -18,6 +18,8 @@ POOLS = [  # (N, C, H, W, Hf, Wf, s, p)
     (2, 3, 7, 9, 3, 3, 2, 1),
     (2, 2, 6, 5, 2, 3, 1, 1),         # overlapping windows
     (1, 2, 9, 9, 3, 2, 3, 0),
+    (1, 2, 10, 11, 3, 3, 3, 0),       # trailing rows/columns no window covers
+    (2, 3, 8, 8, 2, 2, 3, 0),         # gaps between windows
 ]
 
 

@@ -135,7 +135,20 @@ def lenet_timing(steps=50, warmup=10):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3))
+    # the same step recorded once as a HIP graph and replayed
+    gtr = LeNetTrainer(params)
+    gtr.capture(Xd, Yd, warmup=2)
+    for _ in range(warmup):
+        gtr.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        gtr.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    gms = e0.elapsed_time(e1) / steps
+    return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3), graph_ms_per_step=gms,
+                graph_images_per_s=64.0 / (gms / 1e3))
 
 
 def _median_ms(fn, reps=20, warmup=3):
@@ -485,7 +498,9 @@ def main():
         lt = lenet_timing()
         rec["lenet_training"] = {"batch": 64, "dtype": "f64",
                                  "ms_per_step": round(lt["ms_per_step"], 4),
-                                 "images_per_s": round(lt["images_per_s"], 1)}
+                                 "images_per_s": round(lt["images_per_s"], 1),
+                                 "hip_graph_ms_per_step": round(lt["graph_ms_per_step"], 4),
+                                 "hip_graph_images_per_s": round(lt["graph_images_per_s"], 1)}
         rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
         rec["horizontal_fusion"] = horizontal_fusion_timing()

@@ -87,6 +87,36 @@ class LeNetTrainer:
         dmlnn.sgd_momentum_update(self.p_flat, self.g_flat, self.v_flat, self.lr, self.mu)
         return loss
 
+    # --- HIP graph form of the step ----------------------------------------
+    # The step is a fixed sequence of launches on fixed buffers, so it can be
+    # recorded once into a HIP graph and replayed: one submission instead of
+    # seventeen, and no host work between kernels.  The batch is read from
+    # static input buffers (copy a new batch into them before a replay).
+    def capture(self, X, Y, warmup: int = 1):
+        """Record one training step reading X, Y (copied into static buffers).
+        The warm-up steps run eagerly first (they update the parameters)."""
+        self.X_static = X.clone()
+        self.Y_static = Y.clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(warmup):  # kernel attributes and occupancy queries happen here
+                self.step(self.X_static, self.Y_static)
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.graph_loss = self.step(self.X_static, self.Y_static)
+        return self.graph
+
+    def replay(self, X=None, Y=None):
+        """One training step from the recorded graph (optionally on a new batch)."""
+        if X is not None:
+            self.X_static.copy_(X)
+        if Y is not None:
+            self.Y_static.copy_(Y)
+        self.graph.replay()
+        return self.graph_loss
+
 
 class LeNetScorer:
     """Forward-only batched scoring of the same network (the paper's parfor-style

@@ -67,6 +67,8 @@ struct IgemmArgs {
     int bank_off[kMaxBanks + 1];
     void *bank_out[kMaxBanks];
     int require_dma;  // 1: return hipErrorNotSupported instead of using the register path
+    int k4;           // LDS-DMA kernel with NB = 1: 0, or the row blocks (2 or 4) of the
+                      // four-way k split
     // Sparse input (forward, register-staged kernel): X given in CSR; csr_row
     // holds, for every image row (n, c, y), the position of its first non-zero
     // (N*Cs*Sh + 1 entries, the last = nnz), csr_col / csr_val the CSR columns
@@ -329,7 +331,7 @@ struct DmaLayout {
                                           // has 256 bytes of slack
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL, int K4 = 0>
 __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
@@ -364,6 +366,24 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < NB; ++y) acc[x][y] = MF::zero();
+    // K4 (NB = 1 tiles of small layers): every wave covers the whole 16*K4 x 32
+    // tile and the four waves split the k-steps (wave w takes steps 4w, 4w+16,
+    // ...); the partial tiles are added in wave order after the last chunk.
+    constexpr int R4 = K4 ? K4 : 1;
+    typename MF::acc_t acc4[R4][2];
+    int lb4[2];
+    if (K4) {
+#pragma unroll
+        for (int x = 0; x < R4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y) acc4[x][y] = MF::zero();
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int q = q0 + y * 16 + (lane & 15);
+            const int qy = q / a.Qw, qx = q - qy * a.Qw;
+            lb4[y] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+        }
+    }
 
     const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
     const unsigned img_bytes = (unsigned)(img * sizeof(T));
@@ -498,29 +518,90 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
                 acc[1][y] = MF::mma(fa1, bv, acc[1][y]);
             }
         };
-        // With ksplit, wave half wm takes the steps kk = 4*wm, 4*wm + 8, ...
-        const int kstep = KS ? 8 : 4;
-        int kk = KS ? 4 * wm : 0;
-        frag(kk, a0[0], a1[0], b0);
-        for (; kk + kstep < a.KCK; kk += 2 * kstep) {
-            frag(kk + kstep, a0[1], a1[1], b1);
-            mma_step(a0[0], a1[0], b0);
-            frag(kk + 2 * kstep, a0[0], a1[0], b0);
-            mma_step(a0[1], a1[1], b1);
-            if (!ZSKIP) {
-                // Issue order: a set's reads, then the other set's MFMAs.
-                __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+        if (!K4) {
+            // With ksplit, wave half wm takes the steps kk = 4*wm, 4*wm + 8, ...
+            const int kstep = KS ? 8 : 4;
+            int kk = KS ? 4 * wm : 0;
+            frag(kk, a0[0], a1[0], b0);
+            for (; kk + kstep < a.KCK; kk += 2 * kstep) {
+                frag(kk + kstep, a0[1], a1[1], b1);
+                mma_step(a0[0], a1[0], b0);
+                frag(kk + 2 * kstep, a0[0], a1[0], b0);
+                mma_step(a0[1], a1[1], b1);
+                if (!ZSKIP) {
+                    // Issue order: a set's reads, then the other set's MFMAs.
+                    __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, NB + 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+                }
             }
+            if (kk < a.KCK) mma_step(a0[0], a1[0], b0);
+        } else {
+            const T *ar = stage_a(st) + (lane & 15) * a.SA + (lane >> 4);
+            T fa[2][R4], fb[2][2];
+            auto frag4 = [&](int k, T (&A)[R4], T (&B)[2]) {
+#pragma unroll
+                for (int x = 0; x < R4; ++x) A[x] = ar[16 * x * a.SA + k];
+                const int ko = tap_off(k + (lane >> 4));
+#pragma unroll
+                for (int y = 0; y < 2; ++y) B[y] = s_src[ko + lb4[y]];
+            };
+            auto mma4 = [&](const T (&A)[R4], const T (&B)[2]) {
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    if (ZSKIP && wave_all_zero(B[y])) continue;
+#pragma unroll
+                    for (int x = 0; x < R4; ++x) acc4[x][y] = MF::mma(A[x], B[y], acc4[x][y]);
+                }
+            };
+            int kk = 4 * wave;
+            frag4(kk, fa[0], fb[0]);
+            for (; kk + 16 < a.KCK; kk += 32) {
+                frag4(kk + 16, fa[1], fb[1]);
+                mma4(fa[0], fb[0]);
+                frag4(kk + 32, fa[0], fb[0]);
+                mma4(fa[1], fb[1]);
+                if (!ZSKIP) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, R4 + 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2 * R4, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, R4 + 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2 * R4, 0);
+                }
+            }
+            if (kk < a.KCK) mma4(fa[0], fb[0]);
         }
-        if (kk < a.KCK) mma_step(a0[0], a1[0], b0);
         wait_dma();
         __syncthreads();
         st ^= 1;
     }
 
+    if (K4) {
+        // Partial tiles to LDS, then each wave sums (in wave order) the part of
+        // the tile the standard epilogue expects it to hold.
+        T *s_p = reinterpret_cast<T *>(smem);
+#pragma unroll
+        for (int x = 0; x < R4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    s_p[(wave * 64 + 16 * x + MF::row(lane, r)) * 32 + 16 * y + (lane & 15)] =
+                        acc4[x][y][r];
+        __syncthreads();
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ml = wm * 32 + 16 * x + MF::row(lane, r), col = wn * 16 + (lane & 15);
+                T v = T(0);
+                if (ml < 16 * R4)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) v += s_p[(w * 64 + ml) * 32 + col];
+                acc[x][0][r] = v;
+            }
+        __syncthreads();
+    }
     bool active = true;  // this wave holds final values of its rows
     if (KS) {
         // Waves wm = 1 hand their partial tiles to the waves wm = 0 of the same
@@ -748,35 +829,43 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
     return false;
 }
 
-template <typename T, int NB, bool BWD, bool KS, bool POOL>
+template <typename T, int NB, bool BWD, bool KS, bool POOL, int K4 = 0>
 hipError_t launch_dma_ks(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                          int nimg, int zero_skip, hipStream_t s)
 {
     dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
     hipError_t e;
     if (zero_skip) {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS, POOL>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS, POOL, K4>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     } else {
-        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS, POOL>;
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS, POOL, K4>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
     }
     return hipGetLastError();
 }
 
+template <typename T, int NB, bool BWD, bool POOL>
+hipError_t launch_dma_k4(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
+                         int nimg, int zero_skip, hipStream_t s)
+{
+    if (NB == 1 && a.k4 == 4)
+        return launch_dma_ks<T, NB, BWD, false, POOL, 4>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (NB == 1 && a.k4 == 2)
+        return launch_dma_ks<T, NB, BWD, false, POOL, 2>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
+    return launch_dma_ks<T, NB, BWD, false, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
+}
+
 template <typename T, int NB, bool BWD>
 hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                       int nimg, int zero_skip, hipStream_t s)
 {
-    if (!BWD && a.pool_out) {
-        if (a.ksplit)
-            return launch_dma_ks<T, NB, false, true, true>(a, p, L, w_bytes, nimg, zero_skip, s);
-        return launch_dma_ks<T, NB, false, false, true>(a, p, L, w_bytes, nimg, zero_skip, s);
-    }
-    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true, false>(a, p, L, w_bytes, nimg, zero_skip, s);
-    return launch_dma_ks<T, NB, BWD, false, false>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (!BWD && a.pool_out)
+        return launch_dma_k4<T, NB, false, true>(a, p, L, w_bytes, nimg, zero_skip, s);
+    return launch_dma_k4<T, NB, BWD, false>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
 
 template <typename T, int NB, bool BWD>
@@ -839,9 +928,17 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         ad.KC = pd.KC;
         ad.KCK = pd.KCK;
         ad.SA = pd.SA;
-        ad.ksplit = M <= 32;
+        // The smallest tiles (NB = 1: small layers with few blocks) split the
+        // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
+        // when a chunk has enough steps to share (16+) and enough rows (M > 16).
+        ad.k4 = (pd.NB == 1 && pd.KCK >= 64 && M > 16) ? (M <= 32 ? 2 : 4) : 0;
+        ad.ksplit = !ad.k4 && M <= 32;
         if (ad.ksplit) {  // the partial-tile hand-over reuses the stages
             const size_t red = sizeof(T) * (size_t)2 * 2 * pd.NB * 4 * kWave;
+            if (pd.lds < red) pd.lds = red;
+        }
+        if (ad.k4) {  // so do the four partial tiles
+            const size_t red = sizeof(T) * (size_t)4 * 64 * 32;
             if (pd.lds < red) pd.lds = red;
         }
         if (pool) {  // so does the pooling tile (32 rows x 32 NB)

@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--zero-skip-probe", action="store_true",
+                    help="only run the config 2 zero-skip measurement (for counter runs)")
     ap.add_argument("--only-f64", action="store_true",
                     help="skip the fp32, LeNet, other-config and other-kernel extras")
     return ap.parse_args()
@@ -151,8 +153,8 @@ def lenet_timing(steps=50, warmup=10):
                 graph_images_per_s=64.0 / (gms / 1e3))
 
 
-def _median_ms(fn, reps=20, warmup=3):
-    """Median over reps of HIP-event timings on the current stream."""
+def _median_ms(fn, reps=20, warmup=5, with_min=False):
+    """Median (and min) over reps of HIP-event timings on the current stream."""
     import torch
     for _ in range(warmup):
         fn()
@@ -165,7 +167,7 @@ def _median_ms(fn, reps=20, warmup=3):
         e1.record()
     torch.cuda.synchronize()
     ts = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
-    return ts[len(ts) // 2]
+    return (ts[len(ts) // 2], ts[0]) if with_min else ts[len(ts) // 2]
 
 
 def scoring_timing(M=4096):
@@ -259,6 +261,62 @@ def sparse_conv_timing():
     return res
 
 
+def _reach_counts(H, Hf, S, P, Hout):
+    """For each input row h: the number of output rows whose window covers h."""
+    import numpy as np
+    cnt = np.zeros(H, dtype=np.int64)
+    for oh in range(Hout):
+        for i in range(Hf):
+            h = oh * S + i - P
+            if 0 <= h < H:
+                cnt[h] += 1
+    return cnt
+
+
+def zero_skip_timing():
+    """Config 2 forward (LeNet conv1, ~80% i.i.d. zeros) and a structured-zero
+    supplement (the same draw with a 6-pixel zero border) with the zero-fragment
+    skip off and on: dense-equivalent GFLOP/s and the nnz-based algorithmic work
+    2*F*sum over non-zero inputs of the outputs each reaches."""
+    import numpy as np
+    import torch
+    from paper_1802_04647_amd import dmlnn
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    s = SHAPES["lenet_conv1"]
+    X0, W0, b0, _ = conv_layer_inputs("lenet_conv1")
+    Xs = X0.reshape(s.N, s.C, s.Hin, s.Win).copy()
+    Xs[:, :, :6, :] = 0.0
+    Xs[:, :, -6:, :] = 0.0
+    Xs[:, :, :, :6] = 0.0
+    Xs[:, :, :, -6:] = 0.0
+    rh = _reach_counts(s.Hin, s.Hf, s.stride, s.pad, s.Hout)
+    rw = _reach_counts(s.Win, s.Wf, s.stride, s.pad, s.Wout)
+    reach = np.outer(rh, rw)  # outputs per (h, w) for one filter
+    W, b = torch.from_numpy(W0).cuda(), torch.from_numpy(b0).cuda()
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=torch.float64, device="cuda")
+    dense_flops = s.flops_per_pass()
+    res = {}
+    for name, Xh in (("config2_iid_zeros", X0), ("config2_structured_zeros", Xs.reshape(s.N, -1))):
+        nz = (Xh.reshape(s.N, s.C, s.Hin, s.Win) != 0)
+        nnz_flops = 2.0 * s.F * float((nz * reach).sum())
+        X = torch.from_numpy(np.ascontiguousarray(Xh)).cuda()
+        row = {"zero_fraction": round(float(np.mean(Xh == 0)), 4),
+               "dense_gflop": round(dense_flops / 1e9, 4), "nnz_gflop": round(nnz_flops / 1e9, 4)}
+        for mode in (0, 1):
+            prev = dmlnn.set_zero_skip(mode)
+            ms, mn = _median_ms(lambda: dmlnn.conv2d_forward(X, W, b, *a, out=out), reps=20,
+                                warmup=5, with_min=True)
+            dmlnn.set_zero_skip(prev)
+            row["skip" if mode else "dense"] = {
+                "median_ms": round(ms, 4), "min_ms": round(mn, 4),
+                "dense_equiv_gflops": round(dense_flops / (ms / 1e3) / 1e9, 1),
+                "nnz_gflops": round(nnz_flops / (ms / 1e3) / 1e9, 1)}
+        res[name] = row
+    return res
+
+
 def conv_config_timing():
     """Per-pass GFLOP/s of the LeNet conv layers (configs 2 and 3) in fp64 and fp32."""
     import torch
@@ -294,10 +352,12 @@ def conv_config_timing():
             flops = s.flops_per_pass()
             res[name][dtn] = {}
             for pname, fn in fns.items():
-                ms = _median_ms(fn)
+                ms, mn = _median_ms(fn, with_min=True)
                 tf = flops / (ms / 1e3) / 1e12
-                res[name][dtn][pname] = {"ms": round(ms, 4), "tflops": round(tf, 3),
-                                         "pct_of_mfma_peak": round(100 * tf / peak, 2)}
+                res[name][dtn][pname] = {"ms": round(ms, 4), "min_ms": round(mn, 4),
+                                         "tflops": round(tf, 3),
+                                         "pct_of_mfma_peak": round(100 * tf / peak, 2),
+                                         "images_per_s": round(s.N / (ms / 1e3), 1)}
     return res
 
 
@@ -342,7 +402,8 @@ def aux_kernel_timing():
     ids = torch.empty((64, 64 * 49), dtype=torch.int32, device="cuda")
     hbm("max_pool2d_fwd_lenet", Xs.numel() * 8 + ps.numel() * 12,
         lambda: dmlnn.max_pool2d_fwd(Xs, 64, 14, 14, 2, 2, 2, 0, out=ps, argmax=ids),
-        "64 x 64 x 14x14 -> 7x7 (config 3), fp64")
+        "64 x 64 x 14x14 -> 7x7 (config 3), fp64; 8.8 MB, resident in the 256 MB MALL "
+        "across reps")
     # SGD-momentum over the LeNet parameter count (config 4)
     n = 1663370
     th = torch.randn(n, dtype=f64, device="cuda", generator=g)
@@ -449,6 +510,9 @@ def main():
         print("no GPU available", file=sys.stderr)
         sys.exit(1)
 
+    if args.zero_skip_probe:
+        print(json.dumps({"zero_skip": zero_skip_timing()}), flush=True)
+        return
     r = conv_step_timing("f64", args.steps, args.warmup)
     N, F3 = r["N"], 3 * r["flops_per_pass"]
     ms_step = r["wall_s"] * 1e3 / args.steps
@@ -505,6 +569,7 @@ def main():
         rec["conv_configs"] = conv_config_timing()
         rec["horizontal_fusion"] = horizontal_fusion_timing()
         rec["sparse_conv"] = sparse_conv_timing()
+        rec["zero_skip"] = zero_skip_timing()
         rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline()

@@ -325,6 +325,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 constexpr int kMaxDmaS = 12;  // source-window DMA instructions per wave per chunk
 constexpr int kMaxDmaA = 20;  // filter-slice DMA instructions per wave per chunk
 constexpr size_t kLdsPerBlock = 80 * 1024;  // two blocks per CU (160 KiB)
+constexpr size_t kLdsPerBlock32 = 53 * 1024;  // three blocks per CU (fp32)
 
 struct DmaLayout {
     int src_bytes, a_bytes, stage_bytes;  // per-stage regions, 256-byte multiples; a_bytes
@@ -332,7 +333,7 @@ struct DmaLayout {
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL, int K4 = 0>
-__global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
+__global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, sizeof(T) == 4 ? 3 : 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
     using MF = Mfma<T>;
@@ -808,6 +809,11 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
 {
     if (img_bytes >= 0x80000000ull || w_bytes >= 0x80000000ull) return false;
     const long long dpe = (long long)tsz / 4;
+    // The largest chunk that fits, unless a chunk at least half as large has no
+    // padded k-steps (KC*Hf*Wf a multiple of 4): then the largest such chunk.
+    int first = 0, exact = 0;
+    Plan pf = p, pe = p;
+    DmaLayout lf = {}, le = {};
     for (int kc = Cs < 16 ? Cs : 16; kc >= 1; --kc) {
         const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 1;
         const long long nis = ((long long)kc * rows_max * Wpad * dpe + kWave - 1) / kWave;
@@ -818,15 +824,29 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
         l.a_bytes = (int)nia * 256 + 256;  // + slack read by the last step's prefetch
         l.stage_bytes = l.src_bytes + l.a_bytes;
         const size_t total = 2 * (size_t)l.stage_bytes + (bwd ? (size_t)l.src_bytes : 0);
-        if (total > kLdsPerBlock) continue;
-        p.KC = kc;
-        p.KCK = kck;
-        p.SA = sa;
-        p.lds = total;
-        L = l;
-        return true;
+        // fp32 kernels fit three blocks per CU in registers; keep LDS to a third
+        if (total > (tsz == 4 ? kLdsPerBlock32 : kLdsPerBlock)) continue;
+        Plan q = p;
+        q.KC = kc;
+        q.KCK = kck;
+        q.SA = sa;
+        q.lds = total;
+        if (!first) {
+            first = kc;
+            pf = q;
+            lf = l;
+        }
+        if (kck == kc * HfWf && 2 * kc >= first) {
+            exact = kc;
+            pe = q;
+            le = l;
+            break;
+        }
     }
-    return false;
+    if (!first) return false;
+    p = exact ? pe : pf;
+    L = exact ? le : lf;
+    return true;
 }
 
 template <typename T, int NB, bool BWD, bool KS, bool POOL, int K4 = 0>
@@ -944,7 +964,8 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         if (pool) {  // so does the pooling tile (32 rows x 32 NB)
             const size_t pt = sizeof(T) * (size_t)32 * 32 * pd.NB;
             if (pd.lds < pt) pd.lds = pt;
-            if (pd.lds > kLdsPerBlock) return hipErrorNotSupported;
+            if (pd.lds > (sizeof(T) == 4 ? kLdsPerBlock32 : kLdsPerBlock))
+                return hipErrorNotSupported;
         }
         switch (pd.NB) {
         case 7: return launch_dma<T, 7, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);

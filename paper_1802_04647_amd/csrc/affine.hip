@@ -5,13 +5,10 @@
 //   forward  out = X W + b        (A = X,        B = W)
 //   dX = g W^T                    (A = g,        B = W viewed transposed)
 //   dW = X^T g                    (A = X viewed transposed, B = g)
-// where g = dout masked to out_fwd > 0 when a relu mask is given; the mask is
-// applied as the operand is loaded.  A block owns a 16 x 16 output tile and up
-// to 16 waves that split K (one MFMA per 4-deep k-step); their partial tiles
-// are added in wave order (deterministic).  Column sums of g (db) use a
-// separate fixed-order kernel.
-#include <type_traits>
-
+// where g = dout masked to out_fwd > 0 when a relu mask is given.  A block
+// owns a 16 x 16 output tile and up to 16 waves that split K (one MFMA per
+// 4-deep k-step); their partial tiles are added in wave order
+// (deterministic).  Column sums of g (db) use a separate fixed-order kernel.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -28,95 +25,193 @@ struct GemmArgs {
     void *C;                // C[i*ldc + j]
     long long sAm, sAk, sBk, sBn, ldc;
     int M, N, K, relu;
-    int kw_len;             // k per wave (a multiple of 4)
+    int kw_len;             // k per wave (a multiple of 16)
 };
 
-// A block owns a (16 TM) x 16 output tile (each B fragment feeds TM MFMAs, so B
-// is read once per 16 TM rows); its waves split K into contiguous ranges
-// of kw_len and read their MFMA fragments straight from global memory (the
-// products here have at most a few MB of operands, which stay in L2).  The
-// per-wave partial tiles are added in wave order (deterministic).  Rows and
-// columns past the matrix edge read a clamped (valid) row or column: they only
-// feed outputs that are not stored.  The main loop takes whole batches of kU
-// steps with no k test, so its loads issue back to back; the tail zeroes k
-// past the wave's range.  MA / MB: A / B carries a relu mask.
-template <typename T, bool MA, bool MB, int kTM>
-__global__ __launch_bounds__(kMaxKW * kWave) void gemm_kernel(GemmArgs g)
+// A block owns a 16 x 16 output tile; its waves split K into contiguous
+// ranges of kw_len (a multiple of 16) and read their MFMA fragments straight
+// from global memory (the products here have at most a few MB of operands,
+// which stay in L2).
+//
+// k is walked in groups of 16 (four MFMA k-steps).  Inside a group the k
+// order is permuted so that an operand stored with k contiguous (X for the
+// forward product, g and W for dX) is read with 16-byte vector loads: lane
+// quarter q holds k = 2q, 2q+1, 8+2q, 9+2q of the group in its four steps
+// (fp64; for fp32 k = 4q..4q+3).  Each step still covers four distinct k, the
+// four steps cover the group, and both operands use the same order, so the
+// products are unchanged.  A 16-row fragment then reads 64 contiguous bytes
+// per row per load instead of 32, which halves the L1 cache accesses that
+// bound these loads.  Operands with rows contiguous keep per-step loads.
+//
+// These products are small, so a wave's time is load latency: groups are
+// loaded two at a time, one batch ahead (two register sets), so one batch's
+// loads are in flight while the previous batch's MFMAs issue.  Rows and
+// columns past the matrix edge read a clamped (valid) row or column; they only
+// feed outputs that are not stored.  A partial last group (K not a multiple
+// of 16) reads clamped k and zeroes B past the range.  A relu mask is loaded
+// beside its operand and applied just before the MFMA.  The per-wave partial
+// tiles are added in wave order (deterministic).
+template <typename T>
+struct GemmFrag {
+    // position in the group of k-step u for lane quarter q
+    static __device__ __forceinline__ int kpos(int q, int u)
+    {
+        if (sizeof(T) == 8) return (u & 1) + 2 * q + 8 * (u >> 1);
+        return 4 * q + u;
+    }
+    // the four values of a k-contiguous row at group start p (16-byte aligned)
+    static __device__ __forceinline__ void vload(const T *p, int q, T (&v)[4])
+    {
+        if constexpr (sizeof(T) == 8) {
+            const double2 lo = *reinterpret_cast<const double2 *>(p + 2 * q);
+            const double2 hi = *reinterpret_cast<const double2 *>(p + 8 + 2 * q);
+            v[0] = lo.x;
+            v[1] = lo.y;
+            v[2] = hi.x;
+            v[3] = hi.y;
+        } else {
+            const float4 x = *reinterpret_cast<const float4 *>(p + 4 * q);
+            v[0] = x.x;
+            v[1] = x.y;
+            v[2] = x.z;
+            v[3] = x.w;
+        }
+    }
+};
+
+// Waves per block at most: the masked fp64 forms hold two register sets of
+// operands and masks, more than the 128 registers a 16-wave block leaves.
+template <typename T, bool MA, bool MB>
+constexpr int gemm_max_waves() { return (sizeof(T) == 8 && (MA || MB)) ? 8 : kMaxKW; }
+
+template <typename T, bool MA, bool MB, bool VA, bool VB>
+__global__ __launch_bounds__((gemm_max_waves<T, MA, MB>() * kWave)) void gemm_kernel(GemmArgs g)
 {
     using MF = Mfma<T>;
-    constexpr int kTI = 16 * kTM;
-    constexpr int kU = kTM == 1 ? 8 : 4;  // 4-deep k-steps loaded before their MFMAs
+    using FR = GemmFrag<T>;
     extern __shared__ __align__(16) unsigned char smem[];
-    T *s_red = reinterpret_cast<T *>(smem);  // [wave][kTI * kTJ]
+    T *s_red = reinterpret_cast<T *>(smem);  // [wave][16 * kTJ]
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
     const int nw = blockDim.x / kWave;
-    const int i0 = blockIdx.x * kTI, j0 = blockIdx.y * kTJ;
+    // Blocks are dealt to the 8 XCDs round-robin (block b to XCD b mod 8), and
+    // each XCD has its own L2.  Tile t = (ti, tj), ti fastest, is renumbered so
+    // that every XCD owns a contiguous run of tiles: the row tiles of a column
+    // strip then share one L2 copy of that strip of B (for the LeNet products
+    // B is a 12.8 MB weight matrix, larger than one L2).
+    const int ntile = gridDim.x * gridDim.y, bl = blockIdx.x + gridDim.x * blockIdx.y;
+    const int per = ntile / 8, rem = ntile % 8, xcd = bl % 8;
+    const int t = xcd * per + min(xcd, rem) + bl / 8;
+    const int i0 = (t % gridDim.x) * 16, j0 = (t / gridDim.x) * kTJ;
     const int kbeg = wave * g.kw_len, kend = min(g.K, kbeg + g.kw_len);
+    const int ngrp = kend > kbeg ? (kend - kbeg + 15) / 16 : 0;
+    const bool ragged = ((kend - kbeg) & 15) != 0;  // the last group is partial
     const T *A = reinterpret_cast<const T *>(g.A);
     const T *Am = reinterpret_cast<const T *>(g.Amask);
     const T *B = reinterpret_cast<const T *>(g.B);
     const T *Bm = reinterpret_cast<const T *>(g.Bmask);
-    const int li = lane & 15, lk = lane >> 4;
-    long long arow[kTM];
-#pragma unroll
-    for (int x = 0; x < kTM; ++x) arow[x] = (long long)min(i0 + 16 * x + li, g.M - 1) * g.sAm;
+    const int li = lane & 15, q = lane >> 4;
+    const long long arow = (long long)min(i0 + li, g.M - 1) * g.sAm;
     const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
 
-    auto ldA = [&](int x, int k) -> T {
-        const long long o = arow[x] + (long long)k * g.sAk;
-        const T v = A[o];
-        if (MA) return Am[o] > T(0) ? v : T(0);
-        return v;
+    struct Grp {
+        T a[4], b[4];
+        T am[4], bm[4];  // used only with a mask (MA / MB)
     };
-    auto ldB = [&](int k) -> T {
-        const long long o = (long long)k * g.sBk + bcol;
-        const T v = B[o];
-        if (MB) return Bm[o] > T(0) ? v : T(0);
-        return v;
-    };
-
-    typename MF::acc_t acc[kTM];
+    // one group of 16 k from k0; `part`: the wave's partial last group
+    auto load_grp = [&](int k0, bool part, Grp &f) {
+        if (part) {
 #pragma unroll
-    for (int x = 0; x < kTM; ++x) acc[x] = MF::zero();
-    int kk = kbeg;
-    for (; kk + 4 * kU <= kend; kk += 4 * kU) {
-        T a[kU][kTM], b[kU];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-#pragma unroll
-            for (int x = 0; x < kTM; ++x) a[u][x] = ldA(x, kk + 4 * u + lk);
-            b[u] = ldB(kk + 4 * u + lk);
+            for (int u = 0; u < 4; ++u) {
+                const int k = k0 + FR::kpos(q, u), kc = min(k, kend - 1);
+                const long long oa = arow + (long long)kc * g.sAk;
+                const long long ob = (long long)kc * g.sBk + bcol;
+                f.a[u] = A[oa];
+                if (MA) f.am[u] = Am[oa];
+                const T bv = B[ob];
+                f.b[u] = k < kend ? bv : T(0);
+                if (MB) f.bm[u] = Bm[ob];
+            }
+            return;
         }
+        if constexpr (VA) {
+            FR::vload(A + arow + k0, q, f.a);
+            if constexpr (MA) FR::vload(Am + arow + k0, q, f.am);
+        } else {
 #pragma unroll
-        for (int u = 0; u < kU; ++u)
+            for (int u = 0; u < 4; ++u) {
+                const long long oa = arow + (long long)(k0 + FR::kpos(q, u)) * g.sAk;
+                f.a[u] = A[oa];
+                if (MA) f.am[u] = Am[oa];
+            }
+        }
+        if constexpr (VB) {
+            FR::vload(B + bcol + k0, q, f.b);
+            if constexpr (MB) FR::vload(Bm + bcol + k0, q, f.bm);
+        } else {
 #pragma unroll
-            for (int x = 0; x < kTM; ++x) acc[x] = MF::mma(a[u][x], b[u], acc[x]);
+            for (int u = 0; u < 4; ++u) {
+                const long long ob = (long long)(k0 + FR::kpos(q, u)) * g.sBk + bcol;
+                f.b[u] = B[ob];
+                if (MB) f.bm[u] = Bm[ob];
+            }
+        }
+    };
+    typename MF::acc_t acc = MF::zero();
+    auto mma_grp = [&](const Grp &f) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const T av = MA ? (f.am[u] > T(0) ? f.a[u] : T(0)) : f.a[u];
+            const T bv = MB ? (f.bm[u] > T(0) ? f.b[u] : T(0)) : f.b[u];
+            acc = MF::mma(av, bv, acc);
+        }
+    };
+    // batch b = groups 2b and 2b + 1 (the second may not exist)
+    auto load_batch = [&](int b, Grp (&f)[2]) {
+        const int g0 = 2 * b;
+        load_grp(kbeg + 16 * g0, ragged && g0 == ngrp - 1, f[0]);
+        if (g0 + 1 < ngrp) load_grp(kbeg + 16 * g0 + 16, ragged && g0 + 1 == ngrp - 1, f[1]);
+    };
+    auto mma_batch = [&](int b, const Grp (&f)[2]) {
+        mma_grp(f[0]);
+        if (2 * b + 1 < ngrp) mma_grp(f[1]);
+    };
+    const int nbatch = (ngrp + 1) / 2;
+    Grp f0[2], f1[2];
+    if (nbatch > 0) load_batch(0, f0);
+    int i = 0;
+    for (; i + 1 < nbatch; i += 2) {
+        load_batch(i + 1, f1);
+        mma_batch(i, f0);
+        if (i + 2 < nbatch) load_batch(i + 2, f0);
+        mma_batch(i + 1, f1);
     }
-    for (; kk < kend; kk += 4) {
-        const int k = kk + lk;
-        const int kc = min(k, kend - 1);
-        T b = ldB(kc);
-        b = k < kend ? b : T(0);
-#pragma unroll
-        for (int x = 0; x < kTM; ++x) acc[x] = MF::mma(ldA(x, kc), b, acc[x]);
-    }
+    if (i < nbatch) mma_batch(i, f0);
 
-#pragma unroll
-    for (int x = 0; x < kTM; ++x)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            s_red[wave * kTI * kTJ + (16 * x + MF::row(lane, r)) * kTJ + li] = acc[x][r];
-    __syncthreads();
     T *C = reinterpret_cast<T *>(g.C);
     const T *bias = reinterpret_cast<const T *>(g.bias);
-    for (int e = tid; e < kTI * kTJ; e += blockDim.x) {
-        const int i = i0 + e / kTJ, j = j0 + e % kTJ;
-        if (i < g.M && j < g.N) {
+    if (nw == 1) {  // one wave: no partial tiles to add
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int ii = i0 + MF::row(lane, r), j = j0 + li;
+            if (ii < g.M && j < g.N) {
+                T v = acc[r];
+                if (bias) v += bias[j];
+                C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) s_red[wave * 16 * kTJ + MF::row(lane, r) * kTJ + li] = acc[r];
+    __syncthreads();
+    for (int e = tid; e < 16 * kTJ; e += blockDim.x) {
+        const int ii = i0 + e / kTJ, j = j0 + e % kTJ;
+        if (ii < g.M && j < g.N) {
             T v = s_red[e];
-            for (int w = 1; w < nw; ++w) v += s_red[w * kTI * kTJ + e];
+            for (int w = 1; w < nw; ++w) v += s_red[w * 16 * kTJ + e];
             if (bias) v += bias[j];
-            C[(long long)i * g.ldc + j] = relu_if(v, g.relu);
+            C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
         }
     }
 }
@@ -147,27 +242,42 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T *G, const T *mask, 
     }
 }
 
-// Waves per block: about 128 k each, at most 16 (a power of two).
+// An operand takes the vector loads when k is contiguous and every row start
+// is 16-byte aligned.
+template <typename T>
+bool vec_ok(const void *p, long long s_row, long long s_k)
+{
+    constexpr long long e = 16 / sizeof(T);  // elements per 16 bytes
+    return s_k == 1 && s_row % e == 0 && reinterpret_cast<uintptr_t>(p) % 16 == 0;
+}
+
+template <typename T, bool MA, bool MB>
+auto pick_gemm(bool va, bool vb)
+{
+    return va ? (vb ? gemm_kernel<T, MA, MB, true, true> : gemm_kernel<T, MA, MB, true, false>)
+              : (vb ? gemm_kernel<T, MA, MB, false, true> : gemm_kernel<T, MA, MB, false, false>);
+}
+
+// Waves per block: enough that each walks about 16 k-steps (two batches), at
+// most 16; the per-wave k range is a multiple of 16.
 template <typename T>
 hipError_t gemm(GemmArgs g, hipStream_t s)
 {
-    int nw = 1;
-    while (nw < kMaxKW && 2 * nw * 128 <= g.K) nw <<= 1;
-    g.kw_len = ((g.K + nw - 1) / nw + 3) / 4 * 4;
-    // 64-row tiles when that still leaves at least 128 blocks, else 16-row tiles
-    const bool tall = (long long)((g.M + 63) / 64) * ((g.N + kTJ - 1) / kTJ) >= 128;
-    const int kTI = tall ? 64 : 16;
-    const size_t lds = (size_t)nw * kTI * kTJ * sizeof(T);
-    auto pick = [&](auto tm) {
-        constexpr int TM = decltype(tm)::value;
-        return g.Amask ? (g.Bmask ? gemm_kernel<T, true, true, TM> : gemm_kernel<T, true, false, TM>)
-                       : (g.Bmask ? gemm_kernel<T, false, true, TM>
-                                  : gemm_kernel<T, false, false, TM>);
-    };
-    auto k = tall ? pick(std::integral_constant<int, 4>()) : pick(std::integral_constant<int, 1>());
+    if (g.Amask && g.Bmask) return hipErrorInvalidValue;  // one masked operand at most
+    const int grps = (g.K + 15) / 16;
+    const int max_w = g.Amask ? gemm_max_waves<T, true, false>()
+                              : (g.Bmask ? gemm_max_waves<T, false, true>() : kMaxKW);
+    int nw = (grps + 3) / 4;
+    nw = nw < 1 ? 1 : (nw > max_w ? max_w : nw);
+    g.kw_len = ((grps + nw - 1) / nw) * 16;
+    const bool va = vec_ok<T>(g.A, g.sAm, g.sAk) && (!g.Amask || vec_ok<T>(g.Amask, g.sAm, g.sAk));
+    const bool vb = vec_ok<T>(g.B, g.sBn, g.sBk) && (!g.Bmask || vec_ok<T>(g.Bmask, g.sBn, g.sBk));
+    const size_t lds = nw > 1 ? (size_t)nw * 16 * kTJ * sizeof(T) : 0;
+    auto k = g.Amask ? pick_gemm<T, true, false>(va, vb)
+                     : (g.Bmask ? pick_gemm<T, false, true>(va, vb) : pick_gemm<T, false, false>(va, vb));
     hipError_t e = allow_dynamic_lds(k, lds);
     if (e != hipSuccess) return e;
-    dim3 grid((g.M + kTI - 1) / kTI, (g.N + kTJ - 1) / kTJ);
+    dim3 grid((g.M + 15) / 16, (g.N + kTJ - 1) / kTJ);
     hipLaunchKernelGGL(k, grid, dim3(nw * kWave), lds, s, g);
     return hipGetLastError();
 }

@@ -64,6 +64,18 @@ __device__ __forceinline__ int div_magic(int n, unsigned long long magic)
     return (int)(((unsigned long long)(unsigned)n * magic) >> 32);
 }
 
+// floor(n / d) for 0 <= n < 2^22 and 1 <= d < 2^22, with rcp = 1.0f / d.  The
+// float product n * rcp is within a relative 2^-22 of n / d (rcp and the
+// product each round once), i.e. within 1 of it, so its truncation is off by
+// at most one either way and one correction step makes it exact.
+__device__ __forceinline__ int div_small(int n, int d, float rcp)
+{
+    int q = (int)((float)n * rcp);
+    const int r = n - q * d;
+    q += (r >= d) - (r < 0);
+    return q;
+}
+
 inline unsigned long long host_magic(int d)
 {
     return (0x100000000ull + (unsigned long long)d - 1ull) / (unsigned long long)d;

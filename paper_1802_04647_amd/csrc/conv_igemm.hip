@@ -79,6 +79,7 @@ struct IgemmArgs {
     const int32_t *csr_col;
     const void *csr_val;
     unsigned long long magic_kck, magic_hw, magic_wf;
+    unsigned long long magic_wpad, magic_sa, magic_qw;  // LDS-DMA kernel set-up
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP, bool CSR = false>
@@ -323,7 +324,14 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 // soffset.  In the backward pass the relu mask source is copied into one LDS
 // window and folded into the chunk's source window before its MFMAs.
 constexpr int kMaxDmaS = 12;  // source-window DMA instructions per wave per chunk
-constexpr int kMaxDmaA = 20;  // filter-slice DMA instructions per wave per chunk
+// Filter-slice DMA instructions per wave per chunk.  (Twice as many offset
+// registers for the one- and two-column-block tiles, which would allow larger
+// chunks, measured slower on the LeNet layers: the longer unrolled set-up and
+// issue code cost more than the saved barriers.)
+constexpr int dma_a_max(int) { return 20; }
+// Rows of the staged filter slice: layers with M <= 32 take the k-split (or
+// four-way) forms, whose waves only read rows 0..31.
+__host__ __device__ constexpr int dma_a_rows(int M) { return M <= 32 ? 32 : kBM; }
 constexpr size_t kLdsPerBlock = 80 * 1024;  // two blocks per CU (160 KiB)
 constexpr size_t kLdsPerBlock32 = 53 * 1024;  // three blocks per CU (fp32)
 
@@ -354,12 +362,21 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     const int CHn = rows_need * a.Wpad;
     const int KCv = a.KC * a.HfWf;
 
+    // Set-up index math avoids runtime integer division (a long VALU sequence
+    // each; the offsets below take dozens): the divisors are launch constants
+    // with host magic numbers, or the block's row count through a float
+    // reciprocal.  A pixel u < 32 NB past the tile's first column splits as
+    // (qx0 + u) / Qw with both operands below 2^16 (the plan bounds Qw).
+    const int qx0 = q0 - qy0 * a.Qw;
+    auto pix_off = [&](int u) {
+        const int v = qx0 + u, dy = div_magic(v, a.magic_qw);
+        return dy * a.S * a.Wpad + (v - dy * a.Qw) * a.S;
+    };
     int lbase[NB];
 #pragma unroll
     for (int y = 0; y < NB; ++y) {
-        int q = q0 + (wn * NB + y) * 16 + (lane & 15);
-        int qy = q / a.Qw, qx = q - qy * a.Qw;
-        lbase[y] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+        const int u = (wn * NB + y) * 16 + (lane & 15);
+        lbase[y] = (q0 + u < qend) ? pix_off(u) : 0;
     }
 
     typename MF::acc_t acc[2][NB];
@@ -380,9 +397,8 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
             for (int y = 0; y < 2; ++y) acc4[x][y] = MF::zero();
 #pragma unroll
         for (int y = 0; y < 2; ++y) {
-            const int q = q0 + y * 16 + (lane & 15);
-            const int qy = q / a.Qw, qx = q - qy * a.Qw;
-            lb4[y] = (q < qend) ? (qy - qy0) * a.S * a.Wpad + qx * a.S : 0;
+            const int u = y * 16 + (lane & 15);
+            lb4[y] = (q0 + u < qend) ? pix_off(u) : 0;
         }
     }
 
@@ -398,20 +414,30 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     // Per-lane byte offsets inside a chunk (channel c0 excluded), or kDmaZero.
     const int Ds = a.KC * CHn * dpe;
     const int NIs = (Ds + kWave - 1) / kWave;
-    const int Da = kBM * a.SA * dpe;
+    constexpr int kMaxDmaA = dma_a_max(NB);
+    const int Da = dma_a_rows(a.M) * a.SA * dpe;
     const int NIa = (Da + kWave - 1) / kWave;
     int vs_off[kMaxDmaS], va_off[kMaxDmaA];
+    // Window element e (< 12 * 4 * 64) -> (row r, column x) by the magic of
+    // Wpad, r -> (channel c, row t) through the reciprocal of rows_need.
+    const float rcp_rows = 1.0f / (float)rows_need;
 #pragma unroll
     for (int j = 0; j < kMaxDmaS; ++j) {
         const int ii = wave + 4 * j, d = ii * kWave + lane;
         int off = kDmaZero;
         if (ii < NIs && d < Ds) {
             const int e = d / dpe, h = d - e * dpe;
-            const int r = e / a.Wpad, x = e - r * a.Wpad;
-            const int c = r / rows_need, t = r - c * rows_need;
+            const int r = div_magic(e, a.magic_wpad), x = e - r * a.Wpad;
+            const int c = div_small(r, rows_need, rcp_rows), t = r - c * rows_need;
             const int yv = ybase + t, xv = x - a.Pw;
-            const int ys = yv / a.up, xs = xv / a.up;
-            if (yv >= 0 && ys * a.up == yv && ys < a.Sh && xv >= 0 && xs * a.up == xv && xs < a.Sw)
+            bool in = yv >= 0 && xv >= 0;
+            int ys = yv, xs = xv;
+            if (a.up != 1) {  // backward_data of a strided layer: up-sampled source
+                ys = max(yv, 0) / a.up;
+                xs = max(xv, 0) / a.up;
+                in = in && ys * a.up == yv && xs * a.up == xv;
+            }
+            if (in && ys < a.Sh && xs < a.Sw)
                 off = (int)((((size_t)c * a.Sh + ys) * a.Sw + xs) * sizeof(T)) + 4 * h;
         }
         vs_off[j] = off;
@@ -422,14 +448,14 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         int off = kDmaZero;
         if (ii < NIa && d < Da) {
             const int e = d / dpe, h = d - e * dpe;
-            const int m = e / a.SA, kk = e - m * a.SA;
+            const int m = div_magic(e, a.magic_sa), kk = e - m * a.SA;
             const int mg = m0 + m;
             if (mg < a.M && kk < KCv) {
                 size_t el;
                 if (!BWD) {
                     el = (size_t)mg * a.Cs * a.HfWf + kk;
                 } else {
-                    const int c = kk / a.HfWf, t = kk - c * a.HfWf;
+                    const int c = div_magic(kk, a.magic_hw), t = kk - c * a.HfWf;
                     el = ((size_t)c * a.M + mg) * a.HfWf + (a.HfWf - 1 - t);
                 }
                 off = (int)(el * sizeof(T)) + 4 * h;
@@ -804,9 +830,10 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
 // per-block LDS share.  False when the problem needs the register-staged path
 // (very wide rows, very large filters, or tensors of 2 GiB and more, whose byte
 // offsets would reach the out-of-range marker).
-bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpad,
+bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, int Wpad,
                    size_t img_bytes, size_t w_bytes, Plan &p, DmaLayout &L)
 {
+    const int max_a = dma_a_max(p.NB), rows_a = dma_a_rows(M);
     if (img_bytes >= 0x80000000ull || w_bytes >= 0x80000000ull) return false;
     const long long dpe = (long long)tsz / 4;
     // The largest chunk that fits, unless a chunk at least half as large has no
@@ -817,8 +844,8 @@ bool make_dma_plan(size_t tsz, bool bwd, int Cs, int HfWf, int rows_max, int Wpa
     for (int kc = Cs < 16 ? Cs : 16; kc >= 1; --kc) {
         const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 1;
         const long long nis = ((long long)kc * rows_max * Wpad * dpe + kWave - 1) / kWave;
-        const long long nia = ((long long)kBM * sa * dpe + kWave - 1) / kWave;
-        if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > kMaxDmaA) continue;
+        const long long nia = ((long long)rows_a * sa * dpe + kWave - 1) / kWave;
+        if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > max_a) continue;
         DmaLayout l;
         l.src_bytes = (int)nis * 256;
         l.a_bytes = (int)nia * 256 + 256;  // + slack read by the last step's prefetch
@@ -871,10 +898,12 @@ template <typename T, int NB, bool BWD, bool POOL>
 hipError_t launch_dma_k4(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                          int nimg, int zero_skip, hipStream_t s)
 {
-    if (NB == 1 && a.k4 == 4)
-        return launch_dma_ks<T, NB, BWD, false, POOL, 4>(a, p, L, w_bytes, nimg, zero_skip, s);
-    if (NB == 1 && a.k4 == 2)
-        return launch_dma_ks<T, NB, BWD, false, POOL, 2>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if constexpr (NB == 1) {
+        if (a.k4 == 4)
+            return launch_dma_ks<T, NB, BWD, false, POOL, 4>(a, p, L, w_bytes, nimg, zero_skip, s);
+        if (a.k4 == 2)
+            return launch_dma_ks<T, NB, BWD, false, POOL, 2>(a, p, L, w_bytes, nimg, zero_skip, s);
+    }
     if (a.ksplit) return launch_dma_ks<T, NB, BWD, true, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
     return launch_dma_ks<T, NB, BWD, false, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
@@ -942,12 +971,15 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     if (a.csr) a.pipelined = 0;  // sparse staging is the direct path only
     Plan pd = p;
     DmaLayout L;
-    if (!a.csr && make_dma_plan(sizeof(T), BWD, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
+    if (!a.csr && make_dma_plan(sizeof(T), BWD, M, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
                       L)) {
         IgemmArgs ad = a;
         ad.KC = pd.KC;
         ad.KCK = pd.KCK;
         ad.SA = pd.SA;
+        ad.magic_wpad = host_magic(pd.Wpad);
+        ad.magic_sa = host_magic(pd.SA);
+        ad.magic_qw = host_magic(Qw);
         // The smallest tiles (NB = 1: small layers with few blocks) split the
         // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
         // when a chunk has enough steps to share (16+) and enough rows (M > 16).

@@ -59,7 +59,8 @@ def test_bias_add_relu_parity(dt):
     assert_close(host(Xd), oracle.bias_add_relu(X, b, C, HW, relu=True), dt, "in place")
 
 
-AFFINE = [(64, 3136, 512), (64, 512, 10), (5, 7, 3), (33, 70, 65), (1, 1, 1)]
+AFFINE = [(64, 3136, 512), (64, 512, 10), (5, 7, 3), (33, 70, 65), (1, 1, 1), (70, 1000, 33),
+          (17, 4099, 20), (3, 130, 600)]
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])

@@ -22,6 +22,8 @@
 // source rows its pixels touch, zero-padded, and (b) the 64 x KC*Hf*Wf slice of
 // A, both in LDS.  A per-chunk table maps k -> LDS offset of tap (c,i,j); each
 // lane adds the offset of its own pixel.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -747,6 +749,170 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     }
 }
 
+// Layers with at most four output rows (forward with F <= 4, backward_data
+// with C <= 4): a matrix-core tile is at least 16 rows, so nearly all of its
+// work would be padding.  Here the products run on the vector ALU.  A block
+// covers 64 consecutive pixels of one image (a lane per pixel) with four waves
+// that split the source channels (wave w takes channels w, w+4, ... of each
+// chunk); their partial sums are added in wave order at the end.  Per chunk
+// of KC channels the block stages the window rows its pixels read (the masked
+// dout in the backward pass) and the chunk's filter values in LDS; a lane then
+// walks its channels' taps, the Wf taps of a window row unrolled so their LDS
+// reads overlap.  Filter values are read by all lanes at one address (an LDS
+// broadcast).
+constexpr int kSmallM = 4;
+constexpr int kSmallPix = 64;
+constexpr int kSmallWaves = 4;
+constexpr int kSmallMaxWf = 7;
+constexpr int kSmallStage = 8;  // window elements each thread loads before storing
+constexpr size_t kSmallLds = 32 * 1024;
+
+// WF: the filter width when it is 3 or 5 (taps fully unrolled), else 0 (any
+// width up to kSmallMaxWf).  MM: 1 when M = 1, else 4 (filter rows past M are
+// staged as zeros, so no row test is needed).
+template <typename T, bool BWD, int WF, int MM>
+__global__ __launch_bounds__(kSmallPix * kSmallWaves) void conv_small_m_kernel(IgemmArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int n = blockIdx.y;
+    const int q0 = blockIdx.x * kSmallPix, qend = min(q0 + kSmallPix, a.Q);
+    const int qy0 = q0 / a.Qw;
+    const int rows = ((qend - 1) / a.Qw - qy0) * a.S + a.Hf;
+    const int ybase = qy0 * a.S - a.Ph;
+    const int CHn = rows * a.Wpad;
+    T *s_win = reinterpret_cast<T *>(smem);  // [KC][rows][Wpad]
+    T *s_w = s_win + (size_t)a.KC * a.CH;    // [KC][MM][Hf*Wf]; CH = the largest rows * Wpad
+    const int q = q0 + lane;
+    const bool act = q < qend;
+    int lb = 0;
+    if (act) {
+        const int qy = q / a.Qw, qx = q - qy * a.Qw;
+        lb = (qy - qy0) * a.S * a.Wpad + qx * a.S;
+    }
+    const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
+    const T *src = reinterpret_cast<const T *>(a.src) + (size_t)n * img;
+    const T *msk = (BWD && a.mask) ? reinterpret_cast<const T *>(a.mask) + (size_t)n * img : nullptr;
+    const T *W = reinterpret_cast<const T *>(a.wgt);
+    const int MW = MM * a.HfWf;
+    const float rcp_ch = 1.0f / (float)CHn, rcp_wpad = 1.0f / (float)a.Wpad;
+    const float rcp_up = 1.0f / (float)a.up;
+    const T *mskp = msk ? msk : src;  // loaded either way; used only with a mask
+    T acc[MM];
+#pragma unroll
+    for (int m = 0; m < MM; ++m) acc[m] = T(0);
+
+    for (int c0 = 0; c0 < a.Cs; c0 += a.KC) {
+        const int kc = min(a.KC, a.Cs - c0);
+        __syncthreads();  // the previous chunk's readers are done
+        // Window element e = (c, t, x) of the chunk.  Each thread issues eight
+        // loads before using any: cells outside the source read element 0 of
+        // the image (a valid address) and are zeroed afterwards, so no branch
+        // splits the loads (a load under a divergent branch is waited for at
+        // the branch's end).
+        const int tot = kc * CHn;
+        for (int base = 0; base < tot; base += kSmallStage * kSmallPix * kSmallWaves) {
+            T v[kSmallStage], mv[kSmallStage];
+            bool ok[kSmallStage];
+#pragma unroll
+            for (int u = 0; u < kSmallStage; ++u) {
+                const int e = min(base + u * kSmallPix * kSmallWaves + tid, tot - 1);
+                const int c = div_small(e, CHn, rcp_ch), rem = e - c * CHn;
+                const int t = div_small(rem, a.Wpad, rcp_wpad), x = rem - t * a.Wpad;
+                const int yv = ybase + t, xv = x - a.Pw;
+                const int ys = div_small(max(yv, 0), a.up, rcp_up);
+                const int xs = div_small(max(xv, 0), a.up, rcp_up);
+                const bool in = yv >= 0 && xv >= 0 && ys * a.up == yv && xs * a.up == xv &&
+                                ys < a.Sh && xs < a.Sw;
+                const size_t o = in ? ((size_t)(c0 + c) * a.Sh + ys) * a.Sw + xs : 0;
+                ok[u] = in;
+                v[u] = src[o];
+                mv[u] = mskp[o];
+            }
+#pragma unroll
+            for (int u = 0; u < kSmallStage; ++u) {
+                const int e = base + u * kSmallPix * kSmallWaves + tid;
+                if (e < tot) s_win[e] = (ok[u] && (!msk || mv[u] > T(0))) ? v[u] : T(0);
+            }
+        }
+        for (int e = tid; e < kc * MW; e += kSmallPix * kSmallWaves) {
+            const int c = e / MW, r = e - c * MW;
+            const int m = r / a.HfWf, tp = r - m * a.HfWf;
+            const size_t el = BWD ? ((size_t)(c0 + c) * a.M + m) * a.HfWf + (a.HfWf - 1 - tp)
+                                  : ((size_t)m * a.Cs + (c0 + c)) * a.HfWf + tp;
+            s_w[e] = m < a.M ? W[el] : T(0);
+        }
+        __syncthreads();
+        if (act) {
+            for (int c = wave; c < kc; c += kSmallWaves) {
+                const T *wrow = s_win + c * CHn + lb;
+                const T *wc = s_w + c * MW;
+                for (int i = 0; i < a.Hf; ++i) {
+                    if constexpr (WF > 0) {
+                        // a window row's taps: all LDS reads first, then the FMAs
+                        T v[WF], w[MM][WF];
+#pragma unroll
+                        for (int j = 0; j < WF; ++j) v[j] = wrow[i * a.Wpad + j];
+#pragma unroll
+                        for (int m = 0; m < MM; ++m)
+#pragma unroll
+                            for (int j = 0; j < WF; ++j) w[m][j] = wc[m * a.HfWf + i * WF + j];
+#pragma unroll
+                        for (int j = 0; j < WF; ++j)
+#pragma unroll
+                            for (int m = 0; m < MM; ++m) acc[m] += w[m][j] * v[j];
+                    } else {
+                        for (int j = 0; j < a.Wf; ++j) {
+                            const T v = wrow[i * a.Wpad + j];
+#pragma unroll
+                            for (int m = 0; m < MM; ++m) acc[m] += wc[m * a.HfWf + i * a.Wf + j] * v;
+                        }
+                    }
+                }
+            }
+        }
+    }
+    // partial sums of the four channel groups, added in wave order
+    __syncthreads();
+    T *s_red = reinterpret_cast<T *>(smem);  // [wave][M][64]
+#pragma unroll
+    for (int m = 0; m < MM; ++m)
+        if (m < a.M) s_red[(wave * kSmallM + m) * kSmallPix + lane] = acc[m];
+    __syncthreads();
+    T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
+    const T *bias = reinterpret_cast<const T *>(a.bias);
+    for (int e = tid; e < a.M * kSmallPix; e += kSmallPix * kSmallWaves) {
+        const int m = e / kSmallPix, u = e - m * kSmallPix;
+        if (q0 + u >= qend) continue;
+        T v = s_red[m * kSmallPix + u];
+#pragma unroll
+        for (int w = 1; w < kSmallWaves; ++w) v += s_red[(w * kSmallM + m) * kSmallPix + u];
+        if (!BWD) v = relu_if(v + (bias ? bias[m] : T(0)), a.relu);
+        out[(size_t)m * a.Q + q0 + u] = v;
+    }
+}
+
+// Channel chunk of the small-M kernel: the largest whose window and filter
+// values fit kSmallLds; 0 when not even one channel fits.
+int small_m_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, int &CH,
+                 int &Wpad)
+{
+    Wpad = (Qw - 1) * S + Wf;
+    int rows_max = 0;
+    for (int q0 = 0; q0 < Q; q0 += kSmallPix) {
+        const int qe = (q0 + kSmallPix < Q ? q0 + kSmallPix : Q) - 1;
+        const int r = (qe / Qw - q0 / Qw) * S + Hf;
+        rows_max = r > rows_max ? r : rows_max;
+    }
+    CH = rows_max * Wpad;
+    if (Wf > kSmallMaxWf) return 0;
+    const int MM = M == 1 ? 1 : kSmallM;
+    const size_t per_c = tsz * ((size_t)CH + (size_t)MM * Hf * Wf);
+    size_t kc = kSmallLds / per_c;
+    if (kc > (size_t)Cs) kc = Cs;
+    return (int)kc;
+}
+
 // Host-side tile selection ----------------------------------------------------
 
 struct Plan {
@@ -952,6 +1118,33 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.Q = Qh * Qw;
     a.HfWf = a.Hf * a.Wf;
     const bool pool = !BWD && a.pool_out;
+    if (M <= kSmallM && !pool && !a.csr && a.nbanks <= 1 && !a.require_dma) {
+        int CH, Wpad;
+        const int kc = small_m_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, CH, Wpad);
+        if (kc >= 1) {
+            a.KC = kc;
+            a.CH = CH;
+            a.Wpad = Wpad;
+            auto pick = [&](auto mm) {
+                constexpr int MM = decltype(mm)::value;
+                return a.Wf == 3 ? conv_small_m_kernel<T, BWD, 3, MM>
+                                 : (a.Wf == 5 ? conv_small_m_kernel<T, BWD, 5, MM>
+                                              : conv_small_m_kernel<T, BWD, 0, MM>);
+            };
+            auto k = M == 1 ? pick(std::integral_constant<int, 1>())
+                            : pick(std::integral_constant<int, kSmallM>());
+            const int MM = M == 1 ? 1 : kSmallM;
+            // the chunk buffers, or the final reduction ([4 waves][4 rows][64 pixels])
+            size_t lds = sizeof(T) * ((size_t)kc * CH + (size_t)kc * MM * a.HfWf);
+            const size_t red = sizeof(T) * kSmallWaves * kSmallM * kSmallPix;
+            if (lds < red) lds = red;
+            hipError_t e = allow_dynamic_lds(k, lds);
+            if (e != hipSuccess) return e;
+            dim3 grid((a.Q + kSmallPix - 1) / kSmallPix, nimg);
+            hipLaunchKernelGGL(k, grid, dim3(kSmallPix * kSmallWaves), lds, s, a);
+            return hipGetLastError();
+        }
+    }
     if (!make_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, nimg, p, pool ? Qw * a.PS : 0))
         return pool ? hipErrorNotSupported : hipErrorInvalidValue;
     a.tiles_per_img = p.tiles_per_img;

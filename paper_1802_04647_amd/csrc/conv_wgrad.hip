@@ -29,7 +29,7 @@ constexpr size_t kLdsBudget = 72 * 1024;
 // Upper bound on resident blocks (256 CUs x 4 blocks) used to size the workspace
 // without a device; the launch uses the measured occupancy, up to this bound.
 constexpr int kMaxResident = 1024;
-constexpr int kMinTiles = 4;  // fewest pixel tiles a split reduces
+constexpr int kMinTiles = 2;  // fewest pixel tiles a split reduces
 constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
 constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
 

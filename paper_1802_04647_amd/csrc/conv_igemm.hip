@@ -1008,7 +1008,9 @@ bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, 
     Plan pf = p, pe = p;
     DmaLayout lf = {}, le = {};
     for (int kc = Cs < 16 ? Cs : 16; kc >= 1; --kc) {
-        const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 1;
+        // row stride of the A slice: 2 mod 4 elements, so the 32 lanes of a half-wave
+        // (16 rows x 2 k) hit distinct banks (an odd stride conflicts)
+        const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 2;
         const long long nis = ((long long)kc * rows_max * Wpad * dpe + kWave - 1) / kWave;
         const long long nia = ((long long)rows_a * sa * dpe + kWave - 1) / kWave;
         if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > max_a) continue;

@@ -584,7 +584,7 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
         p.rows_max = d.Hf;
         p.Wpad = (rq - 1) * d.stride + d.Wf;
         p.CH = p.rows_max * p.Wpad;
-        p.SG = rq + 1;
+        p.SG = rq + 2;
         p.lds = wlds(tsz, p.SG, nch_alloc, p.CH, rq);
         if (p.lds > 160 * 1024) return false;
         p.pipelined = kBM * p.RQ <= kThreads * kMG && (long long)nch_alloc * p.CH <= kThreads * kMX;
@@ -607,7 +607,7 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
         int rows_max = aligned ? (rq / d.Wout - 1) * d.stride + d.Hf
                                : ((d.Wout + rq - 2) / d.Wout) * d.stride + d.Hf;
         int CH = rows_max * p.Wpad;
-        int SG = rq + 1;
+        int SG = rq + 2;  // 2 mod 4: the g-tile fragment reads are free of bank conflicts
         size_t lds = wlds(tsz, SG, nch_alloc, CH, rq);
         if (lds <= kLdsBudget || rq <= 4) {
             p.RQ = rq;
@@ -656,7 +656,7 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.nkr = (K + p.KR - 1) / p.KR;
     p.nft = (d.F + kBM - 1) / kBM;
     p.RQ = (d.Wout + 3) / 4 * 4;
-    p.SG = p.RQ + 1;
+    p.SG = p.RQ + 2;
     p.spr = 0;
     p.rows_max = d.Hf;
     p.Wpad = (d.Wout - 1) * d.stride + d.Wf;

@@ -145,8 +145,36 @@ template <typename Kernel>
 inline hipError_t allow_dynamic_lds(Kernel kernel, size_t bytes)
 {
     if (bytes <= 64 * 1024) return hipSuccess;
-    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    // The attribute persists per device and kernel: set it once per (device,
+    // kernel) for the largest size asked so far (a per-thread cache; the small
+    // LeNet-sized launches otherwise pay the call every time).
+    struct Entry {
+        int dev;
+        const void *k;
+        size_t bytes;
+    };
+    thread_local Entry cache[32];
+    thread_local int used = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+    const void *k = reinterpret_cast<const void *>(kernel);
+    int slot = -1;
+    for (int i = 0; i < used; ++i)
+        if (cache[i].dev == dev && cache[i].k == k) {
+            if (cache[i].bytes >= bytes) return hipSuccess;
+            slot = i;
+            break;
+        }
+    const hipError_t e =
+        hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    if (slot < 0) {
+        slot = used < 32 ? used++ : 0;
+        cache[slot].dev = dev;
+        cache[slot].k = k;
+    }
+    cache[slot].bytes = bytes;
+    return hipSuccess;
 }
 
 // Resident blocks of `kernel` per CU for `lds` bytes of dynamic LDS, and the CU
@@ -154,13 +182,27 @@ inline hipError_t allow_dynamic_lds(Kernel kernel, size_t bytes)
 template <typename Kernel>
 inline int resident_slots(Kernel kernel, int threads, size_t lds)
 {
+    struct Entry {
+        int dev, threads, slots;
+        const void *k;
+        size_t lds;
+    };
+    thread_local Entry cache[32];
+    thread_local int used = 0, next = 0;
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
+    const void *k = reinterpret_cast<const void *>(kernel);
+    for (int i = 0; i < used; ++i)
+        if (cache[i].dev == dev && cache[i].k == k && cache[i].threads == threads &&
+            cache[i].lds == lds)
+            return cache[i].slots;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, lds) != hipSuccess)
         return 0;
-    return cus * per_cu;
+    Entry &c = cache[used < 32 ? used++ : (next++ & 31)];
+    c = Entry{dev, threads, cus * per_cu, k, lds};
+    return c.slots;
 }
 
 }  // namespace dmlnn

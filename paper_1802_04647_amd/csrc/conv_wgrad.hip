@@ -309,7 +309,17 @@ __global__ __launch_bounds__(256) void conv_wgrad_reduce(const T *ws, T *dW, T *
     if (e < total) {
         const T *base = e < FK ? ws + e : ws + (size_t)splits * FK + (e - FK);
         const size_t stride = e < FK ? (size_t)FK : (size_t)F;
-        for (int sp = ph; sp < splits; sp += 16) sum += (double)base[(size_t)sp * stride];
+        // eight loads in flight, then added in split order (a chain of dependent
+        // loads would wait a full memory latency per split)
+        int sp = ph;
+        for (; sp + 7 * 16 < splits; sp += 8 * 16) {
+            T v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = base[(size_t)(sp + 16 * u) * stride];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) sum += (double)v[u];
+        }
+        for (; sp < splits; sp += 16) sum += (double)base[(size_t)sp * stride];
     }
     s_part[ph][el] = sum;
     __syncthreads();

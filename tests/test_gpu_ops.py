@@ -89,6 +89,33 @@ def test_affine_parity(shape, dt):
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_affine_misaligned_operands_bitwise(dt):
+    # Operands whose rows are not 16-byte aligned take per-element loads instead
+    # of vector loads; both read k in the same order, so the results are equal.
+    N, D, M = 20, 96, 40
+    g = rng(44)
+    X = rounded(g.standard_normal((N, D)), dt)
+    W = rounded(g.standard_normal((D, M)), dt)
+    dout = rounded(g.standard_normal((N, M)), dt)
+    tdt = torch.float64 if dt == "f64" else torch.float32
+
+    def shifted(a):  # a copy of a that starts one element past an aligned allocation
+        buf = torch.zeros(a.size + 1, dtype=tdt, device="cuda")
+        v = buf[1:].view(a.shape)
+        v.copy_(torch.from_numpy(a).to(tdt))
+        return v
+
+    zb = dev(np.zeros(M), dt)
+    out_a = dmlnn.affine_fwd(dev(X, dt), dev(W, dt), zb, relu=False)
+    out_m = dmlnn.affine_fwd(shifted(X), shifted(W), zb, relu=False)
+    assert torch.equal(out_a, out_m)
+    assert_close(host(out_a), oracle.affine_fwd(X, W, np.zeros(M), relu=False), dt, "affine out")
+    dX_a, dW_a, _ = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), None)
+    dX_m, dW_m, _ = dmlnn.affine_bwd(shifted(dout), shifted(X), shifted(W), None)
+    assert torch.equal(dX_a, dX_m) and torch.equal(dW_a, dW_m)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
 @pytest.mark.parametrize("NK", [(64, 10), (7, 3), (5, 130), (1, 1)], ids=str)
 def test_softmax_xent_parity(NK, dt):
     N, K = NK

@@ -216,6 +216,120 @@ __global__ __launch_bounds__((gemm_max_waves<T, MA, MB>() * kWave)) void gemm_ke
     }
 }
 
+// Products with a moderate K and many columns (the LeNet dX = g W^T: 64 x 3136
+// from K = 512): the 16 x K strip of A (masked) is staged in LDS once per
+// block, and the block's four waves each stream their own 16 columns of B
+// over the whole K.  Splitting K across waves instead (above) makes every
+// 16-column tile re-read A and its mask from L2: for dX that is 100 MB of
+// 32-byte row pieces, and the L1 throughput on those pieces bounds the time.
+// k is walked in the same permuted 16-groups as above (A from LDS at the
+// permuted positions, B with 16-byte loads when k-contiguous), four groups
+// per batch, loaded one batch ahead.  No wave splits K, so no partial tiles.
+constexpr int kLdsAWaves = 4;
+constexpr int kLdsAMaxK = 1024;
+
+template <typename T, bool MA, bool VB>
+__global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs g)
+{
+    using MF = Mfma<T>;
+    using FR = GemmFrag<T>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_a = reinterpret_cast<T *>(smem);  // [16][SK], k past K zero
+
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int ntile = gridDim.x * gridDim.y, bl = blockIdx.x + gridDim.x * blockIdx.y;
+    const int per = ntile / 8, rem = ntile % 8, xcd = bl % 8;
+    const int t = xcd * per + min(xcd, rem) + bl / 8;
+    const int i0 = (t % gridDim.x) * 16;
+    const int j0 = (t / gridDim.x) * (16 * kLdsAWaves) + 16 * wave;
+    const int K16 = (g.K + 15) / 16 * 16;
+    const int SK = K16 + 2;  // 2 mod 4
+    const T *A = reinterpret_cast<const T *>(g.A);
+    const T *Am = reinterpret_cast<const T *>(g.Amask);
+    const T *B = reinterpret_cast<const T *>(g.B);
+
+    // Stage A: element (r, k) at s_a[r * SK + k].  With k contiguous in memory
+    // consecutive threads take consecutive k, else consecutive rows.  Eight
+    // branch-free loads per thread before any store (clamped rows and k).
+    const bool kfast = g.sAk == 1;
+    const int tot = 16 * K16;
+    for (int base = 0; base < tot; base += 8 * kLdsAWaves * kWave) {
+        T v[8], mv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = min(base + u * kLdsAWaves * kWave + tid, tot - 1);
+            const int r = kfast ? e / K16 : e % 16, k = kfast ? e % K16 : e / 16;
+            const long long o = (long long)min(i0 + r, g.M - 1) * g.sAm +
+                                (long long)min(k, g.K - 1) * g.sAk;
+            v[u] = A[o];
+            mv[u] = MA ? Am[o] : T(1);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = base + u * kLdsAWaves * kWave + tid;
+            if (e < tot) {
+                const int r = kfast ? e / K16 : e % 16, k = kfast ? e % K16 : e / 16;
+                s_a[r * SK + k] = (k < g.K && mv[u] > T(0)) ? v[u] : T(0);
+            }
+        }
+    }
+    __syncthreads();
+
+    const int li = lane & 15, q = lane >> 4;
+    const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
+    const T *arow = s_a + li * SK;
+    constexpr int kG = 4;  // groups per batch
+    const int ngrp = K16 / 16, nbatch = (ngrp + kG - 1) / kG;
+    auto load_b = [&](int b, T (&f)[kG][4]) {
+#pragma unroll
+        for (int gg = 0; gg < kG; ++gg) {
+            const int k0 = min(b * kG + gg, ngrp - 1) * 16;
+            if (VB && k0 + 16 <= g.K) {
+                FR::vload(B + bcol + k0, q, f[gg]);
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int k = k0 + FR::kpos(q, u);
+                    const T bv = B[(long long)min(k, g.K - 1) * g.sBk + bcol];
+                    f[gg][u] = k < g.K ? bv : T(0);
+                }
+            }
+        }
+    };
+    typename MF::acc_t acc = MF::zero();
+    auto mma_b = [&](int b, const T (&f)[kG][4]) {
+#pragma unroll
+        for (int gg = 0; gg < kG; ++gg) {
+            if (b * kG + gg >= ngrp) break;
+            const int k0 = (b * kG + gg) * 16;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc = MF::mma(arow[k0 + FR::kpos(q, u)], f[gg][u], acc);
+        }
+    };
+    T f0[kG][4], f1[kG][4];
+    load_b(0, f0);
+    int b = 0;
+    for (; b + 1 < nbatch; b += 2) {
+        load_b(b + 1, f1);
+        mma_b(b, f0);
+        if (b + 2 < nbatch) load_b(b + 2, f0);
+        mma_b(b + 1, f1);
+    }
+    if (b < nbatch) mma_b(b, f0);
+
+    T *C = reinterpret_cast<T *>(g.C);
+    const T *bias = reinterpret_cast<const T *>(g.bias);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int ii = i0 + MF::row(lane, r), j = j0 + li;
+        if (ii < g.M && j < g.N) {
+            T v = acc[r];
+            if (bias) v += bias[j];
+            C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
+        }
+    }
+}
+
 // db[j] = sum_i g[i, j], g masked by out_fwd > 0 if given.  A block covers 16
 // columns with 16 row phases each: thread (j, ph) sums rows ph, ph+16, ... in
 // order, and the 16 phase sums are added in phase order (deterministic).
@@ -264,6 +378,19 @@ template <typename T>
 hipError_t gemm(GemmArgs g, hipStream_t s)
 {
     if (g.Amask && g.Bmask) return hipErrorInvalidValue;  // one masked operand at most
+    // A strip in LDS: K up to 1024, no mask on B, and enough 16 x 64 tiles
+    const long long tiles64 = (long long)((g.M + 15) / 16) * ((g.N + 63) / 64);
+    if (!g.Bmask && g.K <= kLdsAMaxK && g.K >= 64 && tiles64 >= 128) {
+        const bool vb = vec_ok<T>(g.B, g.sBn, g.sBk);
+        auto k = g.Amask ? (vb ? gemm_lds_a_kernel<T, true, true> : gemm_lds_a_kernel<T, true, false>)
+                         : (vb ? gemm_lds_a_kernel<T, false, true> : gemm_lds_a_kernel<T, false, false>);
+        const size_t lds = sizeof(T) * 16 * ((size_t)(g.K + 15) / 16 * 16 + 2);
+        hipError_t e = allow_dynamic_lds(k, lds);
+        if (e != hipSuccess) return e;
+        dim3 grid((g.M + 15) / 16, (g.N + 63) / 64);
+        hipLaunchKernelGGL(k, grid, dim3(kLdsAWaves * kWave), lds, s, g);
+        return hipGetLastError();
+    }
     const int grps = (g.K + 15) / 16;
     const int max_w = g.Amask ? gemm_max_waves<T, true, false>()
                               : (g.Bmask ? gemm_max_waves<T, false, true>() : kMaxKW);

@@ -60,7 +60,7 @@ def test_bias_add_relu_parity(dt):
 
 
 AFFINE = [(64, 3136, 512), (64, 512, 10), (5, 7, 3), (33, 70, 65), (1, 1, 1), (70, 1000, 33),
-          (17, 4099, 20), (3, 130, 600)]
+          (17, 4099, 20), (3, 130, 600), (48, 300, 3000), (130, 1000, 1100)]
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])

@@ -171,6 +171,64 @@ def test_conv_parity_resnet_full_batch_sampled(dt):
     assert np.isfinite(dX).all() and np.isfinite(dW).all()
 
 
+def test_conv_parity_over_4gib_fp64():
+    """A batch whose input, output and gradients each exceed 4 GiB (2700 images of
+    the ResNet-shaped layer, fp64): the images past the 4 GiB mark take the same
+    kernels, so every offset there must be computed in 64 bits.  Only the last
+    four images are non-zero; sampled outputs of those images, and sampled
+    filter-gradient entries (sums over all 2700 images), against the oracle."""
+    s0 = SHAPES["resnet_conv"]
+    N = 2700
+    s = ConvShape(N, s0.C, s0.Hin, s0.Win, s0.F, s0.Hf, s0.Wf, s0.stride, s0.pad)
+    a = _args(s)
+    Ho, Wo = s.Hout, s.Wout
+    assert N * s.C * s.Hin * s.Win * 8 > 2 ** 32
+    g = np.random.Generator(np.random.PCG64(4096))
+    tail = 4
+    X = np.zeros((N, s.C * s.Hin * s.Win))
+    X[-tail:] = np.maximum(g.standard_normal((tail, X.shape[1])), 0.0)
+    W = g.standard_normal((s.F, s.C * s.Hf * s.Wf)) * np.sqrt(2.0 / (s.C * s.Hf * s.Wf))
+    b = g.standard_normal(s.F) * 0.1
+    dout = np.zeros((N, s.F * Ho * Wo))
+    dout[-tail:] = g.standard_normal((tail, dout.shape[1]))
+    mask = np.zeros_like(dout)
+    mask[-tail:] = np.maximum(g.standard_normal((tail, dout.shape[1])), 0.0)
+    print(f"\n[gpu] conv over 4 GiB: {s} f64", flush=True)
+    Xd, Wd, bd = dev(X, "f64"), dev(W, "f64"), dev(b, "f64")
+    outd, _, _ = dmlnn.conv2d_forward(Xd, Wd, bd, *a, relu=True)
+    doutd, maskd = dev(dout, "f64"), dev(mask, "f64")
+    dW, db = dmlnn.conv2d_backward_filter(Xd, doutd, maskd, *a, s.F)
+    dXd = dmlnn.conv2d_backward_data(Wd, doutd, maskd, *a)
+    torch.cuda.synchronize()
+    tol = TOL["f64"]
+    n_lo = N - tail
+    idx = g.integers(0, [tail, s.F, Ho, Wo], size=(200, 4))
+    idx[:, 0] += n_lo
+    ref = np.array([max(oracle.conv2d_forward_pre_elem(X, W, b, *a, *e), 0.0) for e in idx])
+    got = torch.stack([outd[e[0], (e[1] * Ho + e[2]) * Wo + e[3]] for e in idx]).cpu().numpy()
+    assert np.max(np.abs(got - ref)) <= tol * np.max(np.abs(ref))
+    # an image before the non-zero tail: relu(b) exactly
+    assert torch.equal(outd[n_lo - 1].view(s.F, -1),
+                       torch.relu(bd).view(s.F, 1).expand(s.F, Ho * Wo))
+    idx = g.integers(0, [tail, s.C, s.Hin, s.Win], size=(200, 4))
+    idx[:, 0] += n_lo
+    refx = np.array([oracle.conv2d_backward_data_elem(W, dout, mask, s.C, s.Hin, s.Win, s.F,
+                                                      s.Hf, s.Wf, s.stride, s.pad, *e)
+                     for e in idx])
+    gotx = torch.stack([dXd[e[0], (e[1] * s.Hin + e[2]) * s.Win + e[3]] for e in idx]).cpu().numpy()
+    assert np.max(np.abs(gotx - refx)) <= tol * np.max(np.abs(refx))
+    sel = g.integers(0, [s.F, s.C, s.Hf, s.Wf], size=(8, 4))
+    refw = np.array([oracle.conv2d_backward_filter_elem(X, dout, mask, s.N, s.C, s.Hin, s.Win,
+                                                        s.F, s.Hf, s.Wf, s.stride, s.pad, *e)
+                     for e in sel])
+    dWh = host(dW).reshape(s.F, s.C, s.Hf, s.Wf)
+    gotw = dWh[sel[:, 0], sel[:, 1], sel[:, 2], sel[:, 3]]
+    assert np.max(np.abs(gotw - refw)) <= tol * np.max(np.abs(refw))
+    refb = np.array([oracle.conv2d_backward_bias_elem(dout, mask, s.N, s.F, Ho, Wo, f)
+                     for f in range(s.F)])
+    assert_close(host(db), refb, "f64", "db")
+
+
 def test_zero_skip_matches_dense_bitwise():
     s = SHAPES["lenet_conv1"]
     X0, W0, b0, dout0 = conv_layer_inputs("lenet_conv1")

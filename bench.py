@@ -41,6 +41,8 @@ def parse():
                     help="only run the config 2 zero-skip measurement (for counter runs)")
     ap.add_argument("--only-f64", action="store_true",
                     help="skip the fp32, LeNet, other-config and other-kernel extras")
+    ap.add_argument("--only-lenet", action="store_true",
+                    help="only time the LeNet training step (for kernel-trace runs)")
     return ap.parse_args()
 
 
@@ -512,6 +514,10 @@ def main():
 
     if args.zero_skip_probe:
         print(json.dumps({"zero_skip": zero_skip_timing()}), flush=True)
+        return
+    if args.only_lenet:
+        lt = lenet_timing()
+        print(json.dumps({"lenet_training": {k: round(v, 4) for k, v in lt.items()}}), flush=True)
         return
     r = conv_step_timing("f64", args.steps, args.warmup)
     N, F3 = r["N"], 3 * r["flops_per_pass"]

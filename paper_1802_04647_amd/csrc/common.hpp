@@ -137,6 +137,14 @@ __device__ __forceinline__ void dma_dword(i32x4 rsrc, void *lds_base, int voffse
     llvm_amdgcn_raw_buffer_load_lds(rsrc, (lds_void *)lds_base, 4, voffset, soffset, 0, 0);
 }
 
+// The same with 16 bytes per lane: lane i's four dwords land at lds_base + 16 i.
+// The source needs only 4-byte alignment, and the range test is per dword (a
+// lane straddling the end of the range loads its dwords below it, zeros above).
+__device__ __forceinline__ void dma_x4(i32x4 rsrc, void *lds_base, int voffset, int soffset)
+{
+    llvm_amdgcn_raw_buffer_load_lds(rsrc, (lds_void *)lds_base, 16, voffset, soffset, 0, 0);
+}
+
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Kernels asking for more than 64 KiB of dynamic LDS must opt in (gfx950 has

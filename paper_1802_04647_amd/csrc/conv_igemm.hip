@@ -325,6 +325,12 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 // every chunk and stays in a register; the chunk's channel offset is the scalar
 // soffset.  In the backward pass the relu mask source is copied into one LDS
 // window and folded into the chunk's source window before its MFMAs.
+// The fp64 forward pass moves the filter slice 16 bytes per lane when a chunk
+// holds an even number of taps: a slice row is a contiguous run of the filter
+// row, each lane's element pair lies inside it, and the four-times-larger
+// instructions let a chunk take more channels (LeNet conv2: 2 instead of 1).
+// The backward pass reads the filter flipped and channel-major, so its pairs
+// are not contiguous and it keeps the 4-byte form.
 constexpr int kMaxDmaS = 12;  // source-window DMA instructions per wave per chunk
 // Filter-slice DMA instructions per wave per chunk.  (Twice as many offset
 // registers for the one- and two-column-block tiles, which would allow larger
@@ -340,6 +346,9 @@ constexpr size_t kLdsPerBlock32 = 53 * 1024;  // three blocks per CU (fp32)
 struct DmaLayout {
     int src_bytes, a_bytes, stage_bytes;  // per-stage regions, 256-byte multiples; a_bytes
                                           // has 256 bytes of slack
+    int a_vec;  // 1: the filter slice moves 16 bytes per lane (fp64 forward, chunks of
+                // an even number of taps: every pair of elements is contiguous in the
+                // filter, and no pair mixes a tap with a zero column)
 };
 
 template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL, int K4 = 0>
@@ -417,7 +426,9 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
     const int Ds = a.KC * CHn * dpe;
     const int NIs = (Ds + kWave - 1) / kWave;
     constexpr int kMaxDmaA = dma_a_max(NB);
-    const int Da = dma_a_rows(a.M) * a.SA * dpe;
+    const bool avec = sizeof(T) == 8 && !BWD && L.a_vec;
+    // filter-slice DMA units (dwords, or pairs of elements) and instructions
+    const int Da = avec ? dma_a_rows(a.M) * a.SA / 2 : dma_a_rows(a.M) * a.SA * dpe;
     const int NIa = (Da + kWave - 1) / kWave;
     int vs_off[kMaxDmaS], va_off[kMaxDmaA];
     // Window element e (< 12 * 4 * 64) -> (row r, column x) by the magic of
@@ -449,7 +460,7 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         const int ii = wave + 4 * j, d = ii * kWave + lane;
         int off = kDmaZero;
         if (ii < NIa && d < Da) {
-            const int e = d / dpe, h = d - e * dpe;
+            const int e = avec ? 2 * d : d / dpe, h = avec ? 0 : d - e * dpe;
             const int m = div_magic(e, a.magic_sa), kk = e - m * a.SA;
             const int mg = m0 + m;
             if (mg < a.M && kk < KCv) {
@@ -488,10 +499,18 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
                 if (has_mask) dma_dword(rs_msk, pm + ii * 256, vs_off[j], so_src);
             }
         }
+        if (avec) {
 #pragma unroll
-        for (int j = 0; j < kMaxDmaA; ++j) {
-            const int ii = wave + 4 * j;
-            if (ii < NIa) dma_dword(rs_w, pa + ii * 256, va_off[j], so_w);
+            for (int j = 0; j < kMaxDmaA; ++j) {
+                const int ii = wave + 4 * j;
+                if (ii < NIa) dma_x4(rs_w, pa + ii * 1024, va_off[j], so_w);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kMaxDmaA; ++j) {
+                const int ii = wave + 4 * j;
+                if (ii < NIa) dma_dword(rs_w, pa + ii * 256, va_off[j], so_w);
+            }
         }
     };
 
@@ -1011,12 +1030,16 @@ bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, 
         // row stride of the A slice: 2 mod 4 elements, so the 32 lanes of a half-wave
         // (16 rows x 2 k) hit distinct banks (an odd stride conflicts)
         const int kck = ((kc * HfWf + 3) / 4) * 4, sa = kck + 2;
+        // fp64 rows of sa = 2 mod 4 elements start 16-byte aligned in LDS
+        const bool vec = tsz == 8 && !bwd && (kc * HfWf) % 2 == 0;
         const long long nis = ((long long)kc * rows_max * Wpad * dpe + kWave - 1) / kWave;
-        const long long nia = ((long long)rows_a * sa * dpe + kWave - 1) / kWave;
+        const long long nia = vec ? ((long long)rows_a * sa / 2 + kWave - 1) / kWave
+                                  : ((long long)rows_a * sa * dpe + kWave - 1) / kWave;
         if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > max_a) continue;
         DmaLayout l;
         l.src_bytes = (int)nis * 256;
-        l.a_bytes = (int)nia * 256 + 256;  // + slack read by the last step's prefetch
+        l.a_bytes = (int)nia * (vec ? 1024 : 256) + 256;  // + slack read by the last step's prefetch
+        l.a_vec = vec;
         l.stage_bytes = l.src_bytes + l.a_bytes;
         const size_t total = 2 * (size_t)l.stage_bytes + (bwd ? (size_t)l.src_bytes : 0);
         // fp32 kernels fit three blocks per CU in registers; keep LDS to a third

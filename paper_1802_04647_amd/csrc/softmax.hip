@@ -46,42 +46,76 @@ __global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, co
     const int rpw = kWave / sw, seg = lane / sw, sl = lane - seg * sw;
     const T invN = T(1) / T(N);
     T total = T(0);
-    for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
-        const int n = r0 + seg;
-        const bool ok = n < N;
-        const T *s = S + (size_t)n * K;
-        const T *y = Y + (size_t)n * K;
-        T m = -INFINITY;
-        if (ok)
-            for (int k = sl; k < K; k += sw) m = s[k] > m ? s[k] : m;
-        m = seg_max(m, sw);
-        T se = T(0), ys = T(0);
-        if (ok)
-            for (int k = sl; k < K; k += sw) {
-                se += exp(s[k] - m);
-                ys += y[k];
+    if (K <= sw) {
+        // At most one column per lane: s and y are loaded once, into registers,
+        // and each exponential is taken once (the same values and reduction
+        // order as the general loop below).
+        for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
+            const int n = r0 + seg;
+            const bool ok = n < N && sl < K;
+            const size_t o = ok ? (size_t)n * K + sl : 0;
+            const T s0 = S[o], y0 = Y[o];
+            const T sk = ok ? s0 : T(-INFINITY), yk = ok ? y0 : T(0);
+            const T m = seg_max(sk, sw);
+            const T e = ok ? exp(sk - m) : T(0);
+            const T se = seg_sum(e, sw), ys = seg_sum(yk, sw);
+            const T lse = m + log(se);
+            const T rl = seg_sum(ok ? -(yk * (sk - lse)) : T(0), sw);
+            if (ok) {
+                const T p = e / se;
+                if (P) P[o] = p;
+                dS[o] = (p * ys - yk) * invN;
             }
-        se = seg_sum(se, sw);
-        ys = seg_sum(ys, sw);
-        const T lse = m + log(se);
-        T rl = T(0);
-        if (ok)
-            for (int k = sl; k < K; k += sw) {
-                const T sk = s[k], yk = y[k];
-                const T p = exp(sk - m) / se;
-                if (P) P[(size_t)n * K + k] = p;
-                dS[(size_t)n * K + k] = (p * ys - yk) * invN;
-                rl -= yk * (sk - lse);
-            }
-        rl = seg_sum(rl, sw);
-        if (ok) total += rl;
+            if (n < N) total += rl;
+        }
+    } else {
+        for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
+            const int n = r0 + seg;
+            const bool ok = n < N;
+            const T *s = S + (size_t)n * K;
+            const T *y = Y + (size_t)n * K;
+            T m = -INFINITY;
+            if (ok)
+                for (int k = sl; k < K; k += sw) m = s[k] > m ? s[k] : m;
+            m = seg_max(m, sw);
+            T se = T(0), ys = T(0);
+            if (ok)
+                for (int k = sl; k < K; k += sw) {
+                    se += exp(s[k] - m);
+                    ys += y[k];
+                }
+            se = seg_sum(se, sw);
+            ys = seg_sum(ys, sw);
+            const T lse = m + log(se);
+            T rl = T(0);
+            if (ok)
+                for (int k = sl; k < K; k += sw) {
+                    const T sk = s[k], yk = y[k];
+                    const T p = exp(sk - m) / se;
+                    if (P) P[(size_t)n * K + k] = p;
+                    dS[(size_t)n * K + k] = (p * ys - yk) * invN;
+                    rl -= yk * (sk - lse);
+                }
+            rl = seg_sum(rl, sw);
+            if (ok) total += rl;
+        }
     }
     s_part[threadIdx.x] = total;
     __syncthreads();
     if (threadIdx.x == 0) {
+        // segment i (wave i / rpw, segment i % rpw) keeps its sum at s_part[i * sw];
+        // the sums are added in segment order, read sixteen at a time so the
+        // LDS reads overlap instead of each waiting for the previous add
+        const int nseg = kSmWaves * rpw;
         T t = T(0);
-        for (int w = 0; w < kSmWaves; ++w)
-            for (int g = 0; g < rpw; ++g) t += s_part[w * kWave + g * sw];
+        for (int i0 = 0; i0 < nseg; i0 += 16) {
+            T v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) v[u] = s_part[min(i0 + u, nseg - 1) * sw];
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (i0 + u < nseg) t += v[u];
+        }
         *loss = t * invN;
     }
 }
@@ -93,6 +127,20 @@ __global__ __launch_bounds__(kSmThreads) void softmax_kernel(const T *S, T *P, i
     const int lane = lane_id(), wave = wave_id();
     const int rpw = kWave / sw, seg = lane / sw, sl = lane - seg * sw;
     const int wave_g = blockIdx.x * kSmWaves + wave, nwaves = gridDim.x * kSmWaves;
+    if (K <= sw) {  // one column per lane at most, as in softmax_xent_kernel
+        for (int r0 = wave_g * rpw; r0 < N; r0 += nwaves * rpw) {
+            const int n = r0 + seg;
+            const bool ok = n < N && sl < K;
+            const size_t o = ok ? (size_t)n * K + sl : 0;
+            const T s0 = S[o];
+            const T sk = ok ? s0 : T(-INFINITY);
+            const T m = seg_max(sk, sw);
+            const T e = ok ? exp(sk - m) : T(0);
+            const T se = seg_sum(e, sw);
+            if (ok) P[o] = e / se;
+        }
+        return;
+    }
     for (int r0 = wave_g * rpw; r0 < N; r0 += nwaves * rpw) {
         const int n = r0 + seg;
         const bool ok = n < N;

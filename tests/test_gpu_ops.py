@@ -60,7 +60,9 @@ def test_bias_add_relu_parity(dt):
 
 
 AFFINE = [(64, 3136, 512), (64, 512, 10), (5, 7, 3), (33, 70, 65), (1, 1, 1), (70, 1000, 33),
-          (17, 4099, 20), (3, 130, 600), (48, 300, 3000), (130, 1000, 1100)]
+          (17, 4099, 20), (3, 130, 600), (48, 300, 3000), (130, 1000, 1100),
+          (33, 700, 1300),   # dW with K = 33 over many tiles, ragged edges
+          (1000, 101, 900)]  # forward with K = 101 (a partial 16-group) over many tiles
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])

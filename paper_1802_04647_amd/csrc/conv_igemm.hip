@@ -1200,8 +1200,10 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         ad.magic_qw = host_magic(Qw);
         // The smallest tiles (NB = 1: small layers with few blocks) split the
         // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
-        // when a chunk has enough steps to share (16+) and enough rows (M > 16).
-        ad.k4 = (pd.NB == 1 && pd.KCK >= 64 && M > 16) ? (M <= 32 ? 2 : 4) : 0;
+        // when a chunk has enough steps to share (12+) and enough rows (M > 16).
+        // (LeNet conv2 forward, 13 steps a chunk: 64 -> 60 us against the 2 x 2
+        // wave form.)
+        ad.k4 = (pd.NB == 1 && pd.KCK >= 48 && M > 16) ? (M <= 32 ? 2 : 4) : 0;
         ad.ksplit = !ad.k4 && M <= 32;
         if (ad.ksplit) {  // the partial-tile hand-over reuses the stages
             const size_t red = sizeof(T) * (size_t)2 * 2 * pd.NB * 4 * kWave;

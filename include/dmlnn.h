@@ -218,8 +218,10 @@ DMLNN_API int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const 
                int N, int D, int M, int relu, void *stream);
 
 /* g = dout (masked to out_fwd > 0 when out_fwd != NULL);
- *   dX = g W^T (N x D, may be NULL), dW = X^T g (D x M), db = column sums of g
- *   (1 x M, may be NULL). */
+ *   dX = g W^T (N x D), dW = X^T g (D x M), db = column sums of g (1 x M).
+ * Each output may be NULL (not computed), but not all three: the products are
+ * independent, so a caller may compute them in separate calls on separate
+ * streams.  DMLNN_ERR_NULL when dout, X or W is NULL or no output is given. */
 DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W,
                const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M,
                void *stream);

@@ -453,7 +453,7 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
         e = dtype == 0 ? gemm<double>(g, s) : gemm<float>(g, s);
         if (e != hipSuccess) return e;
     }
-    {  // dW[d, m] = sum_n X[n, d] g[n, m]
+    if (dW) {  // dW[d, m] = sum_n X[n, d] g[n, m]
         GemmArgs g = {};
         g.A = X;
         g.sAm = 1;

@@ -376,7 +376,8 @@ int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W
                const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M, void *stream)
 {
     if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_bwd: bad dtype %d", (int)dtype);
-    if (!dout || !X || !W || !dW) return fail(DMLNN_ERR_NULL, "affine_bwd: dout, X, W, dW are required");
+    if (!dout || !X || !W) return fail(DMLNN_ERR_NULL, "affine_bwd: dout, X and W are required");
+    if (!dX && !dW && !db) return fail(DMLNN_ERR_NULL, "affine_bwd: no output (dX, dW, db all NULL)");
     if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M))
         return fail(DMLNN_ERR_ARG, "affine_bwd: bad sizes N=%d D=%d M=%d", N, D, M);
     if (int r = device_check()) return r;

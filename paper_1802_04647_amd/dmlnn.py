@@ -387,14 +387,15 @@ def affine_fwd(X, W, b, relu=False, out=None):
     return out
 
 
-def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW=None, db=None):
-    """Returns [dX, dW, db] (dX / db None when not wanted)."""
+def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW=None, db=None,
+               want_dW=True):
+    """Returns [dX, dW, db] (each None when not wanted)."""
     dt = _dtype(dout, X, W, out_fwd, dX, dW, db)
     N, D = X.shape
     M = W.shape[1]
     if dX is None and want_dX:
         dX = _empty((N, D), X)
-    if dW is None:
+    if dW is None and want_dW:
         dW = _empty((D, M), X)
     if db is None and want_db:
         db = _empty((M,), X)

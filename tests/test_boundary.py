@@ -91,6 +91,10 @@ def test_other_validation(lib):
     assert lib.max_pool2d_bwd(1, FAKE, FAKE, FAKE, 1, 1, 4, 4, 2, 2, 0, 0, None) == ERR_ARG
     assert lib.affine_fwd(0, FAKE, FAKE, None, FAKE, 0, 3, 4, 0, None) == ERR_ARG
     assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, None, None, None, 2, 3, 4, None) == ERR_NULL
+    assert lib.affine_bwd(0, None, FAKE, FAKE, None, FAKE, FAKE, None, 2, 3, 4, None) == ERR_NULL
+    # any one output alone is a valid request (it passes argument validation)
+    for outs in ((FAKE, None, None), (None, FAKE, None), (None, None, FAKE)):
+        assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, *outs, 2, 3, 4, None) not in (ERR_NULL, ERR_ARG)
     assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None) == ERR_NULL
     assert lib.sgd_momentum_update(0, FAKE, FAKE, FAKE, 0.1, 0.9, 0, None) == ERR_ARG
     assert lib.count_nonzero(3, FAKE, 10, FAKE, None) == ERR_DTYPE

@@ -88,6 +88,13 @@ def test_affine_parity(shape, dt):
     _, dW2, _ = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), None, want_dX=False,
                                  want_db=False)
     assert_close(host(dW2), oracle.affine_bwd(dout, X, W, None)[1], dt, "affine dW only")
+    # each output computed alone (separate calls) equals the joint call
+    mask = rounded(oracle.affine_fwd(X, W, b, relu=True), dt)
+    args = (dev(dout, dt), dev(X, dt), dev(W, dt), dev(mask, dt))
+    dXj, dWj, dbj = dmlnn.affine_bwd(*args)
+    dXs, _, _ = dmlnn.affine_bwd(*args, want_dW=False, want_db=False)
+    _, _, dbs = dmlnn.affine_bwd(*args, want_dX=False, want_dW=False)
+    assert dWj is not None and torch.equal(dXs, dXj) and torch.equal(dbs, dbj)
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])

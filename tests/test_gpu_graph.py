@@ -1,7 +1,9 @@
 """The LeNet training step recorded as a HIP graph and replayed: every replay
 must equal the eager step bitwise (same kernels, same order, deterministic
 reductions), with eager work and synchronisations between the replays and a
-new batch copied into the static inputs halfway."""
+new batch copied into the static inputs halfway.  The eager step runs its
+weight gradients on a second stream and the graph holds the single-stream form,
+so this also checks that the two forms agree bitwise."""
 import numpy as np
 import pytest
 import torch

@@ -224,8 +224,12 @@ __global__ __launch_bounds__((gemm_max_waves<T, MA, MB>() * kWave)) void gemm_ke
 // 32-byte row pieces, and the L1 throughput on those pieces bounds the time.
 // k is walked in the same permuted 16-groups as above (A from LDS at the
 // permuted positions, B with 16-byte loads when k-contiguous), four groups
-// per batch, loaded one batch ahead.  No wave splits K, so no partial tiles.
-constexpr int kLdsAWaves = 4;
+// per batch, loaded one batch ahead.  Each column block has two waves, one
+// per half of the k groups, so twice as many B loads are in flight per CU
+// (the product has too few tiles for more than one block per CU); the second
+// half's partial tile is added to the first's through LDS (fixed order).
+constexpr int kLdsACols = 4;                 // 16-column blocks per block
+constexpr int kLdsAWaves = 2 * kLdsACols;    // two k halves each
 constexpr int kLdsAMaxK = 1024;
 
 template <typename T, bool MA, bool VB>
@@ -241,7 +245,8 @@ __global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs
     const int per = ntile / 8, rem = ntile % 8, xcd = bl % 8;
     const int t = xcd * per + min(xcd, rem) + bl / 8;
     const int i0 = (t % gridDim.x) * 16;
-    const int j0 = (t / gridDim.x) * (16 * kLdsAWaves) + 16 * wave;
+    const int cb = wave % kLdsACols, kh = wave / kLdsACols;  // column block, k half
+    const int j0 = (t / gridDim.x) * (16 * kLdsACols) + 16 * cb;
     const int K16 = (g.K + 15) / 16 * 16;
     const int SK = K16 + 2;  // 2 mod 4
     const T *A = reinterpret_cast<const T *>(g.A);
@@ -279,11 +284,14 @@ __global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs
     const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
     const T *arow = s_a + li * SK;
     constexpr int kG = 4;  // groups per batch
-    const int ngrp = K16 / 16, nbatch = (ngrp + kG - 1) / kG;
+    // this wave's groups: [g_lo, g_hi) of the K16 / 16
+    const int ngrp_all = K16 / 16, nh = (ngrp_all + 1) / 2;
+    const int g_lo = kh ? nh : 0, g_hi = kh ? ngrp_all : nh;
+    const int ngrp = g_hi - g_lo, nbatch = (ngrp + kG - 1) / kG;
     auto load_b = [&](int b, T (&f)[kG][4]) {
 #pragma unroll
         for (int gg = 0; gg < kG; ++gg) {
-            const int k0 = min(b * kG + gg, ngrp - 1) * 16;
+            const int k0 = (g_lo + min(b * kG + gg, max(ngrp - 1, 0))) * 16;
             if (VB && k0 + 16 <= g.K) {
                 FR::vload(B + bcol + k0, q, f[gg]);
             } else {
@@ -301,13 +309,13 @@ __global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs
 #pragma unroll
         for (int gg = 0; gg < kG; ++gg) {
             if (b * kG + gg >= ngrp) break;
-            const int k0 = (b * kG + gg) * 16;
+            const int k0 = (g_lo + b * kG + gg) * 16;
 #pragma unroll
             for (int u = 0; u < 4; ++u) acc = MF::mma(arow[k0 + FR::kpos(q, u)], f[gg][u], acc);
         }
     };
     T f0[kG][4], f1[kG][4];
-    load_b(0, f0);
+    if (nbatch > 0) load_b(0, f0);
     int b = 0;
     for (; b + 1 < nbatch; b += 2) {
         load_b(b + 1, f1);
@@ -316,6 +324,16 @@ __global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs
         mma_b(b + 1, f1);
     }
     if (b < nbatch) mma_b(b, f0);
+
+    // the second k half hands its partial tile to the first (past the A strip)
+    T *s_red = s_a + 16 * SK;  // [kLdsACols][4][64]
+    if (kh == 1)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s_red[(cb * 4 + r) * kWave + lane] = acc[r];
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] += s_red[(cb * 4 + r) * kWave + lane];
 
     T *C = reinterpret_cast<T *>(g.C);
     const T *bias = reinterpret_cast<const T *>(g.bias);
@@ -384,10 +402,11 @@ hipError_t gemm(GemmArgs g, hipStream_t s)
         const bool vb = vec_ok<T>(g.B, g.sBn, g.sBk);
         auto k = g.Amask ? (vb ? gemm_lds_a_kernel<T, true, true> : gemm_lds_a_kernel<T, true, false>)
                          : (vb ? gemm_lds_a_kernel<T, false, true> : gemm_lds_a_kernel<T, false, false>);
-        const size_t lds = sizeof(T) * 16 * ((size_t)(g.K + 15) / 16 * 16 + 2);
+        const size_t lds = sizeof(T) * (16 * ((size_t)(g.K + 15) / 16 * 16 + 2) +
+                                         (size_t)kLdsACols * 4 * kWave);
         hipError_t e = allow_dynamic_lds(k, lds);
         if (e != hipSuccess) return e;
-        dim3 grid((g.M + 15) / 16, (g.N + 63) / 64);
+        dim3 grid((g.M + 15) / 16, (g.N + 16 * kLdsACols - 1) / (16 * kLdsACols));
         hipLaunchKernelGGL(k, grid, dim3(kLdsAWaves * kWave), lds, s, g);
         return hipGetLastError();
     }

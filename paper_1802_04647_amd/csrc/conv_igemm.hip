@@ -22,6 +22,7 @@
 // source rows its pixels touch, zero-padded, and (b) the 64 x KC*Hf*Wf slice of
 // A, both in LDS.  A per-chunk table maps k -> LDS offset of tap (c,i,j); each
 // lane adds the offset of its own pixel.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -932,6 +933,244 @@ int small_m_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S
     return (int)kc;
 }
 
+// ---------------------------------------------------------------------------
+// Filter-resident forward for small images with a moderate K (LeNet conv2: 64
+// images of 14x14, K = 800).  There the 64-row tiles above re-stage the whole
+// filter from L2 for every 32 pixels; here a block owns 16 filters of one
+// image and keeps their whole 16 x K slice in LDS, loaded once, while the
+// image's padded source window streams through in channel chunks (LDS DMA,
+// double-buffered, exactly as above).  Each of the four waves takes every
+// fourth 16-pixel tile of the image (at most four: Q <= 256), so a wave issues
+// up to four independent MFMAs per k-step from one filter fragment.  The
+// slice is stored chunk by chunk, each chunk's taps padded to a multiple of 4
+// (zeros), so a chunk's k-steps read it at a fixed offset.  The epilogue adds
+// the bias, applies relu and stores, or pools (the whole image is in the block:
+// every pooled window lies inside it).
+constexpr int kResRows = 16;
+constexpr int kResNT = 4;       // 16-pixel tiles per wave at most
+constexpr int kResThreads = 512;  // eight waves: four tile groups x two k halves
+constexpr int kResMaxDma = 12;  // source-window DMA instructions per wave per chunk
+
+template <typename T, bool POOL>
+__global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))) void conv_resident_kernel(IgemmArgs a, int lds_a_bytes, int stage_bytes)
+{
+    using MF = Mfma<T>;
+    constexpr int dpe = sizeof(T) / 4;
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_a = reinterpret_cast<T *>(smem);  // [16][SA]
+    unsigned char *stages = smem + lds_a_bytes;
+    auto stage_src = [&](int st) { return reinterpret_cast<T *>(stages + st * stage_bytes); };
+
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int tg = wave & 3, kh = wave >> 2;  // tile group, k half
+    const int n = blockIdx.x, m0 = blockIdx.y * kResRows;
+    const int KCv = a.KC * a.HfWf;
+    const int nchunk = (a.Cs + a.KC - 1) / a.KC;
+    const int Kw = a.Cs * a.HfWf;  // filter row length
+    const int Awid = nchunk * a.KCK;
+
+    // Source window of a chunk: [KC][Hpad][Wpad], row t / column x of the
+    // padded image (input row t - Ph, column x - Pw), zeros outside.  Per-lane
+    // DMA offsets are chunk-invariant; the chunk's channel offset is soffset.
+    const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
+    const i32x4 rs_src = buffer_rsrc(reinterpret_cast<const T *>(a.src) + (size_t)n * img,
+                                     (unsigned)(img * sizeof(T)));
+    const int Ds = a.KC * a.CH * dpe;
+    const int NIs = (Ds + kWave - 1) / kWave;
+    const float rcp_ch = 1.0f / (float)a.CH, rcp_wpad = 1.0f / (float)a.Wpad;
+    int vs_off[kResMaxDma];
+#pragma unroll
+    for (int j = 0; j < kResMaxDma; ++j) {
+        const int ii = wave + 8 * j, d = ii * kWave + lane;
+        int off = kDmaZero;
+        if (ii < NIs && d < Ds) {
+            const int e = d / dpe, h = d - e * dpe;
+            const int c = div_small(e, a.CH, rcp_ch), r = e - c * a.CH;
+            const int t = div_small(r, a.Wpad, rcp_wpad), x = r - t * a.Wpad;
+            const int y = t - a.Ph, xs = x - a.Pw;
+            if (y >= 0 && y < a.Sh && xs >= 0 && xs < a.Sw)
+                off = (int)((((size_t)c * a.Sh + y) * a.Sw + xs) * sizeof(T)) + 4 * h;
+        }
+        vs_off[j] = off;
+    }
+    auto issue = [&](int st, int c0) {
+        unsigned char *ps = reinterpret_cast<unsigned char *>(stage_src(st));
+        const int so = (int)((size_t)c0 * a.Sh * a.Sw * sizeof(T));
+#pragma unroll
+        for (int j = 0; j < kResMaxDma; ++j) {
+            const int ii = wave + 8 * j;
+            if (ii < NIs) dma_dword(rs_src, ps + ii * 256, vs_off[j], so);
+        }
+    };
+    issue(0, 0);
+
+    // The filter slice, once: slot ch * KCK + kl of row r holds
+    // W[m0 + r][ch * KC * HfWf + kl] for kl < KC * HfWf inside the filter row,
+    // else 0.  Thirty-two branch-free loads per thread in flight before the
+    // stores (one round trip for the LeNet slice, 16 x 800).
+    const T *W = reinterpret_cast<const T *>(a.wgt);
+    const int tot_a = kResRows * Awid;
+    const float rcp_aw = 1.0f / (float)Awid, rcp_kck = 1.0f / (float)a.KCK;
+    constexpr int kAB = 32;
+    for (int base = 0; base < tot_a; base += kAB * kResThreads) {
+        T v[kAB];
+#pragma unroll
+        for (int u = 0; u < kAB; ++u) {
+            const int e = min(base + u * kResThreads + tid, tot_a - 1);
+            const int r = div_small(e, Awid, rcp_aw), sl = e - r * Awid;
+            const int ch = div_small(sl, a.KCK, rcp_kck), kl = sl - ch * a.KCK;
+            const int k = ch * KCv + kl;
+            v[u] = W[(size_t)min(m0 + r, a.M - 1) * Kw + min(k, Kw - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < kAB; ++u) {
+            const int e = base + u * kResThreads + tid;
+            if (e < tot_a) {
+                const int r = div_small(e, Awid, rcp_aw), sl = e - r * Awid;
+                const int ch = div_small(sl, a.KCK, rcp_kck), kl = sl - ch * a.KCK;
+                const int k = ch * KCv + kl;
+                s_a[r * a.SA + sl] = (m0 + r < a.M && kl < KCv && k < Kw) ? v[u] : T(0);
+            }
+        }
+    }
+
+    // Window offset of this lane's pixel in each of the wave's tiles (0 past Q:
+    // a valid address whose results are not stored).
+    int pb[kResNT];
+#pragma unroll
+    for (int tt = 0; tt < kResNT; ++tt) {
+        const int q = (tg + 4 * tt) * 16 + (lane & 15);
+        const int oy = div_magic(q, a.magic_qw), ox = q - oy * a.Qw;
+        pb[tt] = q < a.Q ? oy * a.S * a.Wpad + ox * a.S : 0;
+    }
+    typename MF::acc_t acc[kResNT];
+#pragma unroll
+    for (int tt = 0; tt < kResNT; ++tt) acc[tt] = MF::zero();
+    wait_dma();
+    __syncthreads();
+
+    // Steps past the chunk's last tap read tap KCv - 1 (finite) against a zero
+    // filter column.  The prefetch after a chunk's last step reads past its
+    // slots, inside LDS (the slice is followed by the stages), unused.
+    auto tap_off = [&](int k) {
+        const int kc = min(k, KCv - 1);
+        const int c = div_magic(kc, a.magic_hw), t = kc - c * a.HfWf;
+        const int i = div_magic(t, a.magic_wf), j = t - i * a.Wf;
+        return c * a.CH + i * a.Wpad + j;
+    };
+    for (int ch = 0; ch < nchunk; ++ch) {
+        const int st = ch & 1;
+        if (ch + 1 < nchunk) issue(st ^ 1, (ch + 1) * a.KC);
+        const T *s_src = stage_src(st);
+        const T *arow = s_a + (lane & 15) * a.SA + ch * a.KCK + (lane >> 4);
+        T fa0, fa1, fb0[kResNT], fb1[kResNT];
+        auto frag = [&](int kk, T &fa, T (&fb)[kResNT]) {
+            fa = arow[kk];
+            const int ko = tap_off(kk + (lane >> 4));
+#pragma unroll
+            for (int tt = 0; tt < kResNT; ++tt) fb[tt] = s_src[ko + pb[tt]];
+        };
+        auto mma_step = [&](T fa, const T (&fb)[kResNT]) {
+#pragma unroll
+            for (int tt = 0; tt < kResNT; ++tt) acc[tt] = MF::mma(fa, fb[tt], acc[tt]);
+        };
+        // k half kh takes the steps 4 kh, 4 kh + 8, ...
+        int kk = 4 * kh;
+        frag(kk, fa0, fb0);
+        for (; kk + 8 < a.KCK; kk += 16) {
+            frag(kk + 8, fa1, fb1);
+            mma_step(fa0, fb0);
+            frag(kk + 16, fa0, fb0);
+            mma_step(fa1, fb1);
+            __builtin_amdgcn_sched_group_barrier(0x100, kResNT + 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, kResNT, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, kResNT + 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, kResNT, 0);
+        }
+        if (kk < a.KCK) mma_step(fa0, fb0);
+        wait_dma();
+        __syncthreads();
+    }
+
+    // The second k half hands its partial tiles to the first (the stages are
+    // free after the last barrier); the first adds them (fixed order).
+    {
+        T *s_red = reinterpret_cast<T *>(stages);  // [4 tile groups][kResNT][4][64]
+        if (kh == 1)
+#pragma unroll
+            for (int tt = 0; tt < kResNT; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane] = acc[tt][r];
+        __syncthreads();
+        if (kh == 0)
+#pragma unroll
+            for (int tt = 0; tt < kResNT; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[tt][r] += s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane];
+        __syncthreads();
+    }
+    // Epilogue (first k half): bias and relu, then the conv output and/or the pool.
+    const T *bias = reinterpret_cast<const T *>(a.bias);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int m = m0 + MF::row(lane, r);
+        const T bm = (bias && m < a.M) ? bias[m] : T(0);
+#pragma unroll
+        for (int tt = 0; tt < kResNT; ++tt) acc[tt][r] = relu_if(acc[tt][r] + bm, a.relu);
+    }
+    if (a.out && kh == 0) {
+        T *out = reinterpret_cast<T *>(a.out) + (size_t)n * a.M * a.Q;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = m0 + MF::row(lane, r);
+#pragma unroll
+            for (int tt = 0; tt < kResNT; ++tt) {
+                const int q = (tg + 4 * tt) * 16 + (lane & 15);
+                if (m < a.M && q < a.Q) out[(size_t)m * a.Q + q] = acc[tt][r];
+            }
+        }
+    }
+    if (POOL) {
+        // the 16 x Q tile to LDS (the stages are free after the last barrier),
+        // then every thread scans windows: first maximum wins (strict >)
+        T *s_t = reinterpret_cast<T *>(stages);
+        if (kh == 0)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int tt = 0; tt < kResNT; ++tt) {
+                    const int q = (tg + 4 * tt) * 16 + (lane & 15);
+                    if (q < a.Q) s_t[MF::row(lane, r) * a.Q + q] = acc[tt][r];
+                }
+        __syncthreads();
+        const int npool = a.Hp * a.Wp;
+        T *pout = reinterpret_cast<T *>(a.pool_out) + (size_t)n * a.M * npool;
+        int32_t *pidx = a.pool_idx + (size_t)n * a.M * npool;
+        for (int e = tid; e < kResRows * npool; e += kResThreads) {
+            const int rr = e / npool, pe = e - rr * npool;
+            const int m = m0 + rr;
+            if (m >= a.M) continue;
+            const int py = pe / a.Wp, px = pe - py * a.Wp;
+            T best = T(0);
+            int bidx = -1;
+            for (int i = 0; i < a.PH; ++i) {
+                const int yy = py * a.PS + i;
+                for (int j = 0; j < a.PW; ++j) {
+                    const int xx = px * a.PS + j;
+                    const T v = s_t[rr * a.Q + yy * a.Qw + xx];
+                    if (bidx < 0 || v > best) {
+                        best = v;
+                        bidx = yy * a.Qw + xx;
+                    }
+                }
+            }
+            const size_t o = (size_t)m * npool + pe;
+            pout[o] = best;
+            pidx[o] = m * a.Q + bidx;
+        }
+    }
+}
+
 // Host-side tile selection ----------------------------------------------------
 
 struct Plan {
@@ -1132,6 +1371,57 @@ hipError_t launch_nb(const IgemmArgs &a, const Plan &p, int nimg, int zero_skip,
     return hipGetLastError();
 }
 
+// Plan of the filter-resident forward, or false when it does not apply: at
+// most 256 output pixels, enough blocks (images x 16-filter groups) to fill
+// the CUs, and a 16-row filter slice that leaves room in LDS for two source
+// chunks.  The chunk is the largest whose DMA fits the offset registers,
+// preferring one without padded k-steps.
+struct ResPlan {
+    int KC, KCK, SA, Wpad, CH, lds_a, stage;
+    size_t lds;
+};
+
+bool res_plan(size_t tsz, int M, int Cs, int Qh, int Qw, int Hf, int Wf, int S, int nimg,
+              bool pool, ResPlan &r)
+{
+    const int Q = Qh * Qw, HfWf = Hf * Wf;
+    if (Q > kResNT * 4 * 16) return false;
+    if ((long long)nimg * ((M + kResRows - 1) / kResRows) < 128) return false;
+    r.Wpad = (Qw - 1) * S + Wf;
+    r.CH = ((Qh - 1) * S + Hf) * r.Wpad;
+    const long long dpe = (long long)tsz / 4;
+    int first = 0;
+    for (int kc = Cs < 16 ? Cs : 16; kc >= 1; --kc) {
+        const int kcv = kc * HfWf, kck = (kcv + 3) / 4 * 4;
+        const int nchunk = (Cs + kc - 1) / kc;
+        const long long nis = ((long long)kc * r.CH * dpe + kWave - 1) / kWave;
+        if ((nis + 7) / 8 > kResMaxDma) continue;
+        const long long sa = (long long)nchunk * kck + 2;  // 2 mod 4
+        // + slack for the prefetch after a chunk's last step
+        const long long lds_a = (kResRows * sa * (long long)tsz + 64 * (long long)tsz + 255) / 256 * 256;
+        long long stage = nis * 256;
+        // the stages also hold the k-half reduction and the pooling tile
+        const long long need = std::max((long long)4 * kResNT * 4 * kWave,
+                                        pool ? (long long)kResRows * Q : 0LL) * (long long)tsz;
+        if (2 * stage < need) stage = (need / 2 + 255) / 256 * 256;
+        const long long total = lds_a + 2 * stage;
+        if (total > 160 * 1024) continue;
+        // the largest chunk that fits, unless one at least half as large has no
+        // padded k-steps: then the largest such
+        const bool exact = kck == kcv;
+        if (first && !(exact && 2 * kc >= first)) continue;
+        r.KC = kc;
+        r.KCK = kck;
+        r.SA = (int)sa;
+        r.lds_a = (int)lds_a;
+        r.stage = (int)stage;
+        r.lds = (size_t)total;
+        if (!first) first = kc;
+        if (exact) break;
+    }
+    return first > 0;
+}
+
 template <typename T, bool BWD>
 hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, int zero_skip,
                         hipStream_t s)
@@ -1167,6 +1457,28 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
             if (e != hipSuccess) return e;
             dim3 grid((a.Q + kSmallPix - 1) / kSmallPix, nimg);
             hipLaunchKernelGGL(k, grid, dim3(kSmallPix * kSmallWaves), lds, s, a);
+            return hipGetLastError();
+        }
+    }
+    // The filter-resident forward, fp64 only (in fp32 the 64-row tiles measured
+    // faster on LeNet conv2: 40 against 43 us).
+    if constexpr (!BWD && sizeof(T) == 8) {
+        ResPlan rp;
+        if (!a.csr && a.nbanks <= 1 && !zero_skip && M >= kResRows &&
+            res_plan(sizeof(T), M, Cs, Qh, Qw, a.Hf, a.Wf, a.S, nimg, pool, rp)) {
+            a.KC = rp.KC;
+            a.KCK = rp.KCK;
+            a.SA = rp.SA;
+            a.Wpad = rp.Wpad;
+            a.CH = rp.CH;
+            a.magic_hw = host_magic(a.HfWf);
+            a.magic_wf = host_magic(a.Wf);
+            a.magic_qw = host_magic(Qw);
+            auto k = pool ? conv_resident_kernel<T, true> : conv_resident_kernel<T, false>;
+            hipError_t e = allow_dynamic_lds(k, rp.lds);
+            if (e != hipSuccess) return e;
+            dim3 grid(nimg, (M + kResRows - 1) / kResRows);
+            hipLaunchKernelGGL(k, grid, dim3(kResThreads), rp.lds, s, a, rp.lds_a, rp.stage);
             return hipGetLastError();
         }
     }

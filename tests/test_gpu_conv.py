@@ -46,6 +46,8 @@ CASES = [
     ConvShape(1, 4, 70, 3, 2, 5, 3, 1, 2),      # narrow tall image: tiles span many rows
     ConvShape(1, 2, 12, 12, 100, 3, 3, 1, 1),   # backward_data over 100 channels in chunks
     ConvShape(1, 2, 9, 9, 4, 8, 8, 1, 3),       # filter wider than 7: matrix-core path
+    ConvShape(32, 5, 9, 9, 64, 3, 3, 1, 1),     # forward: filter-resident kernel (ragged chunk)
+    ConvShape(16, 7, 10, 10, 130, 3, 3, 1, 1),  # forward: filter-resident, ragged filter group
 ]
 
 

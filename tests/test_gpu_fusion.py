@@ -22,6 +22,10 @@ CASES = [
     (ConvShape(2, 3, 15, 13, 5, 3, 3, 1, 1), 3, 3, 3),     # windows leave trailing rows/cols
     (ConvShape(2, 4, 10, 20, 6, 3, 3, 1, 1), 2, 3, 3),     # gaps between windows
     (ConvShape(1, 5, 17, 9, 3, 3, 3, 2, 1), 1, 1, 1),      # 1x1 pool (identity)
+    # filter-resident forward (images x 16-filter groups >= 128, <= 256 pixels)
+    (ConvShape(64, 32, 14, 14, 64, 5, 5, 1, 2), 2, 2, 2),  # LeNet conv2 + pool2, batch 64
+    (ConvShape(43, 17, 16, 16, 40, 3, 3, 1, 0), 2, 2, 2),  # ragged chunk and filter group
+    (ConvShape(128, 3, 7, 6, 20, 3, 3, 2, 1), 2, 2, 2),    # stride 2, 20 filters
 ]
 
 

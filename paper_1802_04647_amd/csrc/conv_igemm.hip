@@ -939,17 +939,22 @@ int small_m_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S
 // filter from L2 for every 32 pixels; here a block owns 16 filters of one
 // image and keeps their whole 16 x K slice in LDS, loaded once, while the
 // image's padded source window streams through in channel chunks (LDS DMA,
-// double-buffered, exactly as above).  Each of the four waves takes every
-// fourth 16-pixel tile of the image (at most four: Q <= 256), so a wave issues
-// up to four independent MFMAs per k-step from one filter fragment.  The
+// double-buffered, exactly as above).  The waves form four tile groups (group
+// g takes every fourth 16-pixel tile of the image from tile g, at most four:
+// Q <= 256), so a wave issues up to four independent MFMAs per k-step from one
+// filter fragment, times kResKs k ranges (alternate k-steps; the partial tiles
+// are added in range order at the end): with one block per CU (the slice and
+// the two chunks take most of its LDS) that keeps four waves per SIMD.  The
 // slice is stored chunk by chunk, each chunk's taps padded to a multiple of 4
 // (zeros), so a chunk's k-steps read it at a fixed offset.  The epilogue adds
 // the bias, applies relu and stores, or pools (the whole image is in the block:
 // every pooled window lies inside it).
 constexpr int kResRows = 16;
 constexpr int kResNT = 4;       // 16-pixel tiles per wave at most
-constexpr int kResThreads = 512;  // eight waves: four tile groups x two k halves
-constexpr int kResMaxDma = 12;  // source-window DMA instructions per wave per chunk
+constexpr int kResKs = 4;                      // k ranges (alternate k-steps)
+constexpr int kResWaves = 4 * kResKs;          // four tile groups x kResKs
+constexpr int kResThreads = kResWaves * kWave;
+constexpr int kResMaxDma = 6;  // source-window DMA instructions per wave per chunk
 
 template <typename T, bool POOL>
 __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))) void conv_resident_kernel(IgemmArgs a, int lds_a_bytes, int stage_bytes)
@@ -962,7 +967,7 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
     auto stage_src = [&](int st) { return reinterpret_cast<T *>(stages + st * stage_bytes); };
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-    const int tg = wave & 3, kh = wave >> 2;  // tile group, k half
+    const int tg = wave & 3, kh = wave >> 2;  // tile group, k range
     const int n = blockIdx.x, m0 = blockIdx.y * kResRows;
     const int KCv = a.KC * a.HfWf;
     const int nchunk = (a.Cs + a.KC - 1) / a.KC;
@@ -981,7 +986,7 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
     int vs_off[kResMaxDma];
 #pragma unroll
     for (int j = 0; j < kResMaxDma; ++j) {
-        const int ii = wave + 8 * j, d = ii * kWave + lane;
+        const int ii = wave + kResWaves * j, d = ii * kWave + lane;
         int off = kDmaZero;
         if (ii < NIs && d < Ds) {
             const int e = d / dpe, h = d - e * dpe;
@@ -998,7 +1003,7 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
         const int so = (int)((size_t)c0 * a.Sh * a.Sw * sizeof(T));
 #pragma unroll
         for (int j = 0; j < kResMaxDma; ++j) {
-            const int ii = wave + 8 * j;
+            const int ii = wave + kResWaves * j;
             if (ii < NIs) dma_dword(rs_src, ps + ii * 256, vs_off[j], so);
         }
     };
@@ -1011,7 +1016,7 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
     const T *W = reinterpret_cast<const T *>(a.wgt);
     const int tot_a = kResRows * Awid;
     const float rcp_aw = 1.0f / (float)Awid, rcp_kck = 1.0f / (float)a.KCK;
-    constexpr int kAB = 32;
+    constexpr int kAB = 16;
     for (int base = 0; base < tot_a; base += kAB * kResThreads) {
         T v[kAB];
 #pragma unroll
@@ -1074,13 +1079,14 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
             for (int tt = 0; tt < kResNT; ++tt) acc[tt] = MF::mma(fa, fb[tt], acc[tt]);
         };
-        // k half kh takes the steps 4 kh, 4 kh + 8, ...
+        // k range kh takes the steps 4 kh, 4 kh + KST, ...
+        constexpr int KST = 4 * kResKs;
         int kk = 4 * kh;
         frag(kk, fa0, fb0);
-        for (; kk + 8 < a.KCK; kk += 16) {
-            frag(kk + 8, fa1, fb1);
+        for (; kk + KST < a.KCK; kk += 2 * KST) {
+            frag(kk + KST, fa1, fb1);
             mma_step(fa0, fb0);
-            frag(kk + 16, fa0, fb0);
+            frag(kk + 2 * KST, fa0, fb0);
             mma_step(fa1, fb1);
             __builtin_amdgcn_sched_group_barrier(0x100, kResNT + 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, kResNT, 0);
@@ -1092,24 +1098,29 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
         __syncthreads();
     }
 
-    // The second k half hands its partial tiles to the first (the stages are
-    // free after the last barrier); the first adds them (fixed order).
+    // The other k ranges hand their partial tiles to the first, one range at a
+    // time through the stages (free after the last barrier); the first adds
+    // them in range order.
     {
         T *s_red = reinterpret_cast<T *>(stages);  // [4 tile groups][kResNT][4][64]
-        if (kh == 1)
+        for (int h = 1; h < kResKs; ++h) {  // the other ranges, in order
+            if (kh == h)
 #pragma unroll
-            for (int tt = 0; tt < kResNT; ++tt)
+                for (int tt = 0; tt < kResNT; ++tt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane] = acc[tt][r];
-        __syncthreads();
-        if (kh == 0)
+                    for (int r = 0; r < 4; ++r)
+                        s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane] = acc[tt][r];
+            __syncthreads();
+            if (kh == 0)
 #pragma unroll
-            for (int tt = 0; tt < kResNT; ++tt)
+                for (int tt = 0; tt < kResNT; ++tt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[tt][r] += s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane];
-        __syncthreads();
+                    for (int r = 0; r < 4; ++r)
+                        acc[tt][r] += s_red[((tg * kResNT + tt) * 4 + r) * kWave + lane];
+            __syncthreads();
+        }
     }
-    // Epilogue (first k half): bias and relu, then the conv output and/or the pool.
+    // Epilogue (first k range): bias and relu, then the conv output and/or the pool.
     const T *bias = reinterpret_cast<const T *>(a.bias);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -1395,7 +1406,7 @@ bool res_plan(size_t tsz, int M, int Cs, int Qh, int Qw, int Hf, int Wf, int S, 
         const int kcv = kc * HfWf, kck = (kcv + 3) / 4 * 4;
         const int nchunk = (Cs + kc - 1) / kc;
         const long long nis = ((long long)kc * r.CH * dpe + kWave - 1) / kWave;
-        if ((nis + 7) / 8 > kResMaxDma) continue;
+        if ((nis + kResWaves - 1) / kResWaves > kResMaxDma) continue;
         const long long sa = (long long)nchunk * kck + 2;  // 2 mod 4
         // + slack for the prefetch after a chunk's last step
         const long long lds_a = (kResRows * sa * (long long)tsz + 64 * (long long)tsz + 255) / 256 * 256;

@@ -967,7 +967,10 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
     auto stage_src = [&](int st) { return reinterpret_cast<T *>(stages + st * stage_bytes); };
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-    const int tg = wave & 3, kh = wave >> 2;  // tile group, k range
+    // tile group and k range: the waves of one SIMD (wave mod 4) hold the four
+    // tile groups, so a group with one tile more than the others does not load
+    // one SIMD alone
+    const int kh = wave & 3, tg = wave >> 2;
     const int n = blockIdx.x, m0 = blockIdx.y * kResRows;
     const int KCv = a.KC * a.HfWf;
     const int nchunk = (a.Cs + a.KC - 1) / a.KC;
@@ -1048,6 +1051,10 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
         const int oy = div_magic(q, a.magic_qw), ox = q - oy * a.Qw;
         pb[tt] = q < a.Q ? oy * a.S * a.Wpad + ox * a.S : 0;
     }
+    // tiles of this group that hold pixels (wave-uniform): the others skip
+    // their fragment reads and MFMAs
+    const int ntile = (a.Q + 15) / 16;
+    const int nt = ntile > tg ? min(kResNT, (ntile - tg + 3) / 4) : 0;
     typename MF::acc_t acc[kResNT];
 #pragma unroll
     for (int tt = 0; tt < kResNT; ++tt) acc[tt] = MF::zero();
@@ -1073,11 +1080,13 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
             fa = arow[kk];
             const int ko = tap_off(kk + (lane >> 4));
 #pragma unroll
-            for (int tt = 0; tt < kResNT; ++tt) fb[tt] = s_src[ko + pb[tt]];
+            for (int tt = 0; tt < kResNT; ++tt)
+                if (tt < nt) fb[tt] = s_src[ko + pb[tt]];
         };
         auto mma_step = [&](T fa, const T (&fb)[kResNT]) {
 #pragma unroll
-            for (int tt = 0; tt < kResNT; ++tt) acc[tt] = MF::mma(fa, fb[tt], acc[tt]);
+            for (int tt = 0; tt < kResNT; ++tt)
+                if (tt < nt) acc[tt] = MF::mma(fa, fb[tt], acc[tt]);
         };
         // k range kh takes the steps 4 kh, 4 kh + KST, ...
         constexpr int KST = 4 * kResKs;

@@ -89,6 +89,23 @@ def test_conv_parity_small(s, dt):
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("s", [ConvShape(64, 32, 14, 14, 64, 5, 5, 1, 2),
+                               ConvShape(128, 20, 6, 6, 16, 3, 3, 1, 1),
+                               ConvShape(64, 40, 8, 8, 24, 5, 5, 1, 2)], ids=str)
+def test_backward_data_without_mask(s, dt):
+    """backward_data with no relu mask (as in the LeNet step, whose pool backward
+    folds the mask in): LeNet conv2 at batch 64, a ragged 32-row tile, and a
+    ragged last channel chunk."""
+    X0, W0, b0, dout0 = random_conv_case(101, s, zero_frac=0.3)
+    W, dout = (rounded(v, dt) for v in (W0, dout0))
+    a = _args(s)
+    print(f"\n[gpu] backward_data {s} {dt}", flush=True)
+    dX = dmlnn.conv2d_backward_data(dev(W, dt), dev(dout, dt), None, *a)
+    torch.cuda.synchronize()
+    assert_close(host(dX), oracle.conv2d_backward_data(W, dout, None, *a), dt, "dX")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
 @pytest.mark.parametrize("name", ["conv_small", "lenet_conv1", "lenet_conv2"])
 def test_conv_parity_workloads(name, dt):
     s = SHAPES[name]

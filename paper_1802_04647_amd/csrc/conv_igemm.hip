@@ -970,7 +970,7 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
     // tile group and k range: the waves of one SIMD (wave mod 4) hold the four
     // tile groups, so a group with one tile more than the others does not load
     // one SIMD alone
-    const int kh = wave & 3, tg = wave >> 2;
+    const int kh = wave % kResKs, tg = wave / kResKs;
     const int n = blockIdx.x, m0 = blockIdx.y * kResRows;
     const int KCv = a.KC * a.HfWf;
     const int nchunk = (a.Cs + a.KC - 1) / a.KC;
@@ -1014,8 +1014,8 @@ __global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2))
 
     // The filter slice, once: slot ch * KCK + kl of row r holds
     // W[m0 + r][ch * KC * HfWf + kl] for kl < KC * HfWf inside the filter row,
-    // else 0.  Thirty-two branch-free loads per thread in flight before the
-    // stores (one round trip for the LeNet slice, 16 x 800).
+    // else 0.  Sixteen branch-free loads per thread in flight before the
+    // stores (one round trip for the LeNet slice, 16 x 800, over 1024 threads).
     const T *W = reinterpret_cast<const T *>(a.wgt);
     const int tot_a = kResRows * Awid;
     const float rcp_aw = 1.0f / (float)Awid, rcp_kck = 1.0f / (float)a.KCK;

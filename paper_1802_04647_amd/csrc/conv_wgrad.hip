@@ -436,16 +436,21 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             vx[it] = v;
         }
     };
+    // New row r goes to slot (s0 + r) mod Hf, s0 = (oh*S + Hf - nr) mod Hf (the
+    // same for the whole block); r < nr <= Hf, so the wrap is one subtraction of
+    // Hf rows, taken from the offset rem = r*Wpad + u within the channel's rows.
+    // This phase sits between the two barriers with the matrix pipe idle, so it
+    // avoids per-element division and modulo.
     auto store_x = [&](int oh) {
         const int tid = opaque(threadIdx.x);
+        const int s0 = (oh * a.S + a.Hf - nr) % a.Hf;
+        const int base = s0 * a.Wpad, wrap = (a.Hf - s0) * a.Wpad, ring = a.Hf * a.Wpad;
 #pragma unroll
         for (int it = 0; it < kRX; ++it) {
             const int e = tid + kRingThreads * it;
             if (e < nch * nrw) {
                 const int c = div_magic(e, a.magic_ch), rem = e - c * nrw;
-                const int r = div_magic(rem, a.magic_wpad), u = rem - r * a.Wpad;
-                const int yr = oh * a.S + a.Hf - nr + r;
-                s_x[c * a.CH + (yr % a.Hf) * a.Wpad + u] = vx[it];
+                s_x[c * a.CH + base + rem - (rem >= wrap ? ring : 0)] = vx[it];
             }
         }
     };
@@ -474,8 +479,12 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         }
     }
     const int lq = lane >> 4;
+    // (image, output row) of the current tile, advanced by one row per tile
+    // (no 64-bit division per tile)
+    int cn = (int)(t_begin / a.Hout), coh = (int)(t_begin - (long long)cn * a.Hout);
     for (long long tt = t_begin; tt < t_end; ++tt) {
-        const int n = (int)(tt / a.Hout), oh = (int)(tt - (long long)n * a.Hout);
+        const int n = cn, oh = coh;
+        const int n1 = oh + 1 < a.Hout ? n : n + 1, oh1 = oh + 1 < a.Hout ? oh + 1 : 0;
         // LDS offset of column k = (c, i, j) of this lane's blocks: filter row i
         // of this tile sits in slot (oh*S + i) mod Hf.
         const int rot = (oh * a.S) % a.Hf;
@@ -511,8 +520,6 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         }
 
         if (tt + 1 < t_end) {
-            const long long t1 = tt + 1;
-            const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
             __syncthreads();
             store_g();
             if (oh1 != 0)
@@ -521,12 +528,13 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
                 stage_x_full(n1, oh1);
             __syncthreads();
             if (tt + 2 < t_end) {
-                const long long t2 = tt + 2;
-                const int n2 = (int)(t2 / a.Hout), oh2 = (int)(t2 - (long long)n2 * a.Hout);
+                const int n2 = oh1 + 1 < a.Hout ? n1 : n1 + 1, oh2 = oh1 + 1 < a.Hout ? oh1 + 1 : 0;
                 load_g(n2, oh2);
                 if (oh2 != 0) load_x(n2, oh2);
             }
         }
+        cn = n1;
+        coh = oh1;
     }
 
     T *wsp = reinterpret_cast<T *>(a.ws) + (size_t)split * a.F * a.K;

@@ -455,13 +455,19 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         }
     };
     // All Hf rows of tile oh, straight from global memory (first tile of an image).
+    // Element e is row rw = e / Wpad of the window (channel c = rw / Hf, filter
+    // row t), column u; row t goes to slot (oh*S + t) mod Hf = rot0 + t, less Hf
+    // once it reaches Hf.  Magic and reciprocal divisions (e < 2^16, rw < 2^22):
+    // this runs between the barriers with the matrix pipe idle.
     auto stage_x_full = [&](int n, int oh) {
         const int tot = nch * a.CH;
+        const int rot0 = (oh * a.S) % a.Hf;
+        const float rcp_hf = 1.0f / (float)a.Hf;
         for (int e = tid; e < tot; e += kRingThreads) {
-            const int c = e / a.CH, rem = e - c * a.CH;
-            const int t = rem / a.Wpad, u = rem - t * a.Wpad;
-            const int yr = oh * a.S + t;
-            s_x[c * a.CH + (yr % a.Hf) * a.Wpad + u] = x_at(n, c, yr, u);
+            const int rw = div_magic(e, a.magic_wpad), u = e - rw * a.Wpad;
+            const int c = div_small(rw, a.Hf, rcp_hf), t = rw - c * a.Hf;
+            const int sl = rot0 + t - (rot0 + t >= a.Hf ? a.Hf : 0);
+            s_x[c * a.CH + sl * a.Wpad + u] = x_at(n, c, oh * a.S + t, u);
         }
     };
 

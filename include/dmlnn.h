@@ -11,8 +11,8 @@
  *   - Section 3, "Builtin NN Functions": conv2d and pooling, and their backward
  *     functions, are builtins.
  *   - Section 2 (NN library and its softmax-classifier listing): layers with
- *     init/forward/backward; affine = X %*% W + b; softmax; cross-entropy;
- *     SGD (and SGD with momentum among the optimizers).
+ *     init/forward/backward; affine (X W plus a bias row); softmax;
+ *     cross-entropy; SGD (and SGD with momentum among the optimizers).
  *
  * Conventions shared by every entry point
  *   - Tensor pointers are DEVICE pointers to contiguous row-major buffers that
@@ -122,9 +122,72 @@ DMLNN_API int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void 
  * returns the previous mode, or -1 for an invalid mode. */
 DMLNN_API int dmlnn_set_zero_skip(int mode);
 
+/* ------------------------------------------------------------ conv2d_plan ----
+ * Which kernel a conv2d pass would run for these sizes, and its tiling: a
+ * host-only query (no device access, launches nothing) for profiling and tests.
+ * The choice depends only on the arguments, as in the call itself (for
+ * backward_filter, `splits` is the most reduction splits a launch may use;
+ * the launch takes fewer when the device holds fewer blocks at once).
+ * pass: DMLNN_PASS_FORWARD (conv2d_forward), DMLNN_PASS_BACKWARD_FILTER,
+ * DMLNN_PASS_BACKWARD_DATA.  zero_skip: the zero-skip mode the call would run
+ * under (0 or 1).  Returns DMLNN_OK and fills *plan, or an error status
+ * (DMLNN_ERR_ARG also when no tiling fits). */
+typedef enum {
+    DMLNN_PASS_FORWARD = 0,
+    DMLNN_PASS_BACKWARD_FILTER = 1,
+    DMLNN_PASS_BACKWARD_DATA = 2
+} dmlnn_conv_pass;
+
+typedef enum {
+    DMLNN_KERNEL_IGEMM_DMA = 1,      /* implicit GEMM, matrix cores, LDS-DMA staging     */
+    DMLNN_KERNEL_IGEMM_REG = 2,      /* implicit GEMM, matrix cores, register staging    */
+    DMLNN_KERNEL_SMALL_M = 3,        /* vector-ALU kernel for at most four output rows    */
+    DMLNN_KERNEL_RESIDENT = 4,       /* filter-resident forward for small images (fp64)   */
+    DMLNN_KERNEL_WGRAD_RING = 5,     /* backward_filter: row ring over the whole k range  */
+    DMLNN_KERNEL_WGRAD_TILES = 6     /* backward_filter: (filter tile, k range) blocks    */
+} dmlnn_conv_kernel;
+
+typedef struct {
+    int kernel;        /* dmlnn_conv_kernel */
+    int zero_skip;     /* 1: the kernel's zero-skip instantiation runs (the small-M and
+                          resident kernels have none: 0 there under either mode) */
+    int tile_m;        /* GEMM rows of a block tile (filters; channels for backward_data) */
+    int tile_pixels;   /* output pixels of a block tile (backward_filter: of a pixel tile) */
+    int blocks;        /* blocks of the main launch (backward_filter: per split) */
+    int chunk;         /* source channels staged per chunk (backward_filter: the k
+                          columns one block covers) */
+    int k_split;       /* wave groups of a block that split the k-steps (1, 2 or 4) */
+    int splits;        /* backward_filter: the most reduction splits; else 0 */
+    int window_width;  /* staged input-window row length, elements */
+    int window_rows;   /* staged input-window rows per channel */
+    size_t lds_bytes;  /* dynamic LDS per block */
+    size_t workspace_bytes; /* backward_filter: conv2d_backward_filter_workspace_size; else 0 */
+} dmlnn_conv_plan;
+
+DMLNN_API int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F,
+                          int Hf, int Wf, int stride, int pad, int zero_skip,
+                          dmlnn_conv_plan *plan);
+
+/* nnz-driven operator choice for a dense operand (paper, Section 3 "Sparse
+ * Operations": the number of non-zeros kept for every intermediate selects
+ * among the physical conv2d operators).  Given the number of non-zeros of the
+ * operand a pass stages — X for DMLNN_PASS_FORWARD and
+ * DMLNN_PASS_BACKWARD_FILTER, the gradient dout for DMLNN_PASS_BACKWARD_DATA —
+ * for instance read back from count_nonzero, returns the zero-skip mode worth
+ * setting with dmlnn_set_zero_skip: 1 when the pass's kernel has a skip form
+ * and, with the zeros spread independently at that density, at least 5% of its
+ * 64-value input fragments are expected to be all zero ((1 - density)^64 >=
+ * 0.05, i.e. density <= 4.6%); else 0.  Structured zeros (zero borders, dead
+ * channels) skip more than this estimate: a caller that knows its data may set
+ * mode 1 directly (results are identical either way).  Host only.  Returns -1
+ * when an argument is invalid (nnz outside [0, element count]). */
+DMLNN_API int conv2d_zero_skip_choice(dmlnn_dtype dtype, int pass, long long nnz, int N, int C,
+                                      int Hin, int Win, int F, int Hf, int Wf, int stride,
+                                      int pad);
+
 /* --------------------------------------------------------- bias_add_relu ----
  * Paper: Section 3, "Tensor Representation" (broadcasting of vectors over
- * matrices) and the affine listing (X %*% W + b).
+ * matrices) and the affine layer of Section 2 (a bias row added to X W).
  *   out[n, c*HW + q] = relu ? max(X[n,c*HW+q] + b[c], 0) : X[n,c*HW+q] + b[c]
  * X and out are N x (C*HW); b has C entries or is NULL.  out may equal X
  * (in place). */
@@ -211,8 +274,8 @@ DMLNN_API int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int
                                   int Hf, int Wf, int stride, int pad, void *stream);
 
 /* ----------------------------------------------------------------- affine ----
- * Paper: Section 2 listing (scores = X %*% W + b; backward returns
- * [dX, dW, db]).  X is N x D, W is D x M, b is 1 x M, out is N x M.
+ * Paper: Section 2 (the affine layer of the softmax-classifier example: the
+ * product X W plus a bias row; its backward returns dX, dW, db in that order).  X is N x D, W is D x M, b is 1 x M, out is N x M.
  *   out = X W + b, then max(., 0) if relu.  b may be NULL. */
 DMLNN_API int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
                int N, int D, int M, int relu, void *stream);
@@ -227,8 +290,9 @@ DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, con
                void *stream);
 
 /* ----------------------------------------------------------- softmax_xent ----
- * Paper: Section 2 listing (probs = softmax(scores); cross-entropy backward;
- * softmax backward), fused.  Per row: p = exp(s - max s) / sum exp(s - max s);
+ * Paper: Section 2 (the softmax-classifier example chains the softmax
+ * forward, the cross-entropy backward and the softmax backward); one fused
+ * pass with the same result.  Per row: p = exp(s - max s) / sum exp(s - max s);
  *   loss    = -(1/N) sum_{n,k} Y[n,k] * log p[n,k]   (one device scalar)
  *   dscores = (p * sum_k Y[n,k] - Y) / N
  * scores, Y, probs, dscores are N x K; probs may be NULL; loss points to one
@@ -237,8 +301,8 @@ DMLNN_API int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y,
                  void *dscores, void *loss, int N, int K, void *stream);
 
 /* ------------------------------------------------------------- softmax_fwd ----
- * Paper: Section 2 listing (probs = softmax::forward(scores)), used alone for
- * forward-only scoring.  Row-wise, max-shifted:
+ * Paper: Section 2 (the softmax layer's forward), used alone for forward-only
+ * scoring.  Row-wise, max-shifted:
  *   probs[n,k] = exp(scores[n,k] - max_k scores[n,:]) / sum_k exp(...)
  * scores and probs are N x K (probs may not alias scores). */
 DMLNN_API int softmax_fwd(dmlnn_dtype dtype, const void *scores, void *probs, int N, int K,
@@ -246,7 +310,7 @@ DMLNN_API int softmax_fwd(dmlnn_dtype dtype, const void *scores, void *probs, in
 
 /* ---------------------------------------------------- sgd_momentum_update ----
  * Paper: Section 2 (SGD with momentum is one of the NN library's optimizers;
- * the listing's plain SGD is W - lr*dW, the case mu = 0).
+ * the example's plain gradient step is the case mu = 0).
  *   v <- mu*v - lr*grad;  theta <- theta + v     (elementwise, in place)
  * theta, grad and v hold n elements. */
 DMLNN_API int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *grad, void *v,
@@ -263,7 +327,7 @@ DMLNN_API int sgd_momentum_update(dmlnn_dtype dtype, void *theta, const void *gr
  * buffer and DMLNN_ERR_ARG for n outside [1, INT_MAX] or a hyper-parameter
  * outside its stated range; nothing is launched then. */
 
-/* Plain SGD (the paper's softmax-classifier listing: W = W - lr*dW):
+/* Plain SGD (the gradient step of the paper's softmax-classifier example):
  *   theta <- theta - lr*grad */
 DMLNN_API int sgd_update(dmlnn_dtype dtype, void *theta, const void *grad, double lr,
                          long long n, void *stream);

@@ -229,7 +229,7 @@ void oracle_conv2d_backward_data(const double *W, const double *dout, const doub
 
 /* ------------------------------------------------------------------------- */
 /* bias_add (+relu): broadcasting a vector over a matrix (Section 3 "Tensor   */
-/* Representation"; the affine listing adds b to X %*% W).                   */
+/* Representation"; Section 2's affine layer adds a bias row to X W).       */
 /* out[n, c*HW + q] = relu?(X[n, c*HW + q] + b[c]);  b may be NULL.            */
 /* ------------------------------------------------------------------------- */
 void oracle_bias_add_relu(const double *X, const double *b, double *out,
@@ -302,8 +302,9 @@ void oracle_max_pool2d_bwd(const double *dout, const int32_t *argmax, double *dX
 }
 
 /* ------------------------------------------------------------------------- */
-/* affine (Section 2 listing: scores = X %*% W + b; backward returns           */
-/* [dX, dW, db]).  X is N x D, W is D x M, b is 1 x M.                         */
+/* affine (Section 2: the affine layer is X W plus a bias row; its backward   */
+/* returns the gradients of X, W and b in that order).  X is N x D, W is      */
+/* D x M, b is 1 x M.                                                          */
 /* ------------------------------------------------------------------------- */
 void oracle_affine_fwd(const double *X, const double *W, const double *b, double *out,
                        int N, int D, int M, int do_relu)
@@ -354,8 +355,8 @@ void oracle_affine_bwd(const double *dout, const double *X, const double *W,
 }
 
 /* ------------------------------------------------------------------------- */
-/* softmax + cross-entropy (Section 2 listing: probs = softmax(scores);        */
-/* dprobs = cross_entropy_loss backward(probs, y); dscores = softmax backward. */
+/* softmax + cross-entropy (Section 2: the classifier example chains the     */
+/* softmax forward, the cross-entropy backward and the softmax backward).      */
 /* Readings: the loss is the mean over the N rows; log-sum-exp is shifted by   */
 /* the row maximum.                                                            */
 /* ------------------------------------------------------------------------- */
@@ -434,8 +435,9 @@ void oracle_softmax_backward(const double *dP, const double *P, double *dS, int 
 }
 
 /* ------------------------------------------------------------------------- */
-/* SGD with momentum (Section 2 names it among the optimizers; the listing's   */
-/* plain update is W - lr*dW).  Reading: v <- mu*v - lr*g;  theta <- theta + v */
+/* SGD with momentum (Section 2 names it among the optimizers; the example's  */
+/* plain gradient step is the case mu = 0).                                    */
+/* Reading: v <- mu*v - lr*g;  theta <- theta + v                              */
 /* ------------------------------------------------------------------------- */
 void oracle_sgd_momentum_update(double *theta, const double *grad, double *v,
                                 double lr, double mu, long long n)

@@ -1,5 +1,7 @@
-// affine forward/backward (paper, Section 2 listing: scores = X %*% W + b and
-// [dX, dW, db] = affine::backward(...)) on the gfx950 matrix cores.
+// affine forward/backward (paper, Section 2: the affine layer is the matrix
+// product of the inputs with the weights plus a broadcast bias row, and its
+// backward returns the input, weight and bias gradients in that order) on the
+// gfx950 matrix cores.
 //
 // One strided GEMM kernel serves all three products:
 //   forward  out = X W + b        (A = X,        B = W)

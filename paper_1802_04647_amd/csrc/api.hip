@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 
@@ -187,6 +188,56 @@ int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void *dout, con
     return launched(dmlnn::launch_conv_backward_data(dtype, W, dout, out_fwd, dX, d,
                                                      zero_skip_mode(), (hipStream_t)stream),
                     "conv2d_backward_data");
+}
+
+int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                int stride, int pad, int zero_skip, dmlnn_conv_plan *plan)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_plan: bad dtype %d", (int)dtype);
+    if (!plan) return fail(DMLNN_ERR_NULL, "conv2d_plan: plan is required");
+    if (pass < DMLNN_PASS_FORWARD || pass > DMLNN_PASS_BACKWARD_DATA)
+        return fail(DMLNN_ERR_ARG, "conv2d_plan: bad pass %d", pass);
+    if (zero_skip != 0 && zero_skip != 1)
+        return fail(DMLNN_ERR_ARG, "conv2d_plan: zero_skip must be 0 or 1");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    dmlnn::ConvPlanInfo info;
+    if (dmlnn::conv_plan_info(dtype, pass, d, zero_skip, info) != hipSuccess)
+        return fail(DMLNN_ERR_ARG, "conv2d_plan: no tiling fits these sizes");
+    memset(plan, 0, sizeof(*plan));
+    plan->kernel = info.kernel;
+    plan->zero_skip = zero_skip && info.kernel != dmlnn::kConvSmallM &&
+                      info.kernel != dmlnn::kConvResident;
+    plan->tile_m = info.tile_m;
+    plan->tile_pixels = info.tile_pixels;
+    plan->blocks = info.blocks;
+    plan->chunk = info.chunk;
+    plan->k_split = info.k_split;
+    plan->splits = info.splits;
+    plan->window_width = info.window_width;
+    plan->window_rows = info.window_rows;
+    plan->lds_bytes = info.lds;
+    plan->workspace_bytes =
+        pass == DMLNN_PASS_BACKWARD_FILTER ? dmlnn::conv_wgrad_workspace_bytes(dtype, d) : 0;
+    g_err[0] = '\0';
+    return DMLNN_OK;
+}
+
+int conv2d_zero_skip_choice(dmlnn_dtype dtype, int pass, long long nnz, int N, int C, int Hin,
+                            int Win, int F, int Hf, int Wf, int stride, int pad)
+{
+    if (!dtype_ok(dtype) || pass < DMLNN_PASS_FORWARD || pass > DMLNN_PASS_BACKWARD_DATA) return -1;
+    dmlnn::ConvDims d;
+    if (conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return -1;
+    const long long n = pass == DMLNN_PASS_BACKWARD_DATA ? (long long)N * F * d.Hout * d.Wout
+                                                         : (long long)N * C * Hin * Win;
+    if (nnz < 0 || nnz > n) return -1;
+    dmlnn::ConvPlanInfo info;
+    if (dmlnn::conv_plan_info(dtype, pass, d, 1, info) != hipSuccess) return -1;
+    if (info.kernel == dmlnn::kConvSmallM) return 0;  // no skip form
+    // expected share of all-zero 64-value fragments under independent zeros
+    const double density = (double)nnz / (double)n;
+    return pow(1.0 - density, 64.0) >= 0.05 ? 1 : 0;
 }
 
 int bias_add_relu(dmlnn_dtype dtype, const void *X, const void *b, void *out, int N, int C, int HW,

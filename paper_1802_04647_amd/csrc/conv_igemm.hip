@@ -216,8 +216,11 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
     auto stage_direct = [&](int c0) {
         if (CSR) {
             // Each wave zeroes its window rows, then scatters the row's non-zeros
-            // (LDS writes of one wave land in issue order).  Columns outside the
-            // row are ignored, so malformed input cannot write outside LDS.
+            // (LDS writes of one wave land in issue order).  A staged row holds
+            // window columns [0, Wpad), i.e. input columns [-Pw, Wpad - Pw): with a
+            // stride above 1 the last input columns can lie past the last window
+            // (they feed no output) and are skipped, as are columns outside the
+            // image row, so no input, well-formed or not, writes outside the row.
             const T *val = reinterpret_cast<const T *>(a.csr_val);
             for (int r = wave; r < nrows; r += kThreads / kWave) {
                 const int c = r / rows_need, t = r - c * rows_need;
@@ -228,9 +231,10 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
                     const size_t ri = ((size_t)n * a.Cs + cg) * a.Sh + yv;
                     const int kb = a.csr_row[ri], ke = a.csr_row[ri + 1];
                     const int base = (cg * a.Sh + yv) * a.Sw;
+                    const int xlim = min(a.Sw, a.Wpad - a.Pw);
                     for (int k = kb + lane; k < ke; k += kWave) {
                         const int x = a.csr_col[k] - base;
-                        if (x >= 0 && x < a.Sw) dst[x + a.Pw] = val[k];
+                        if (x >= 0 && x < xlim) dst[x + a.Pw] = val[k];
                     }
                 }
             }
@@ -1401,11 +1405,14 @@ struct ResPlan {
     size_t lds;
 };
 
-bool res_plan(size_t tsz, int M, int Cs, int Qh, int Qw, int Hf, int Wf, int S, int nimg,
-              bool pool, ResPlan &r)
+bool res_plan(size_t tsz, int M, int Cs, int Sh, int Sw, int Qh, int Qw, int Hf, int Wf, int S,
+              int nimg, bool pool, ResPlan &r)
 {
     const int Q = Qh * Qw, HfWf = Hf * Wf;
     if (Q > kResNT * 4 * 16) return false;
+    // the per-image buffer range and the chunk's soffset are 32-bit byte offsets
+    // that must stay below the out-of-range marker
+    if ((size_t)Cs * Sh * Sw * tsz >= 0x80000000ull) return false;
     if ((long long)nimg * ((M + kResRows - 1) / kResRows) < 128) return false;
     r.Wpad = (Qw - 1) * S + Wf;
     r.CH = ((Qh - 1) * S + Hf) * r.Wpad;
@@ -1442,50 +1449,134 @@ bool res_plan(size_t tsz, int M, int Cs, int Qh, int Qw, int Hf, int Wf, int S, 
     return first > 0;
 }
 
+// Geometry of one forward / backward_data launch (the GEMM view: M output rows,
+// Cs source channels of Sh x Sw, Qh x Qw output pixels) and the fused forms it
+// carries, as the kernel choice sees them.
+struct ConvGeo {
+    int M, Cs, Sh, Sw, Qh, Qw, Hf, Wf, S, nimg;
+    bool pool;
+    int PS;
+    int csr, nbanks, require_dma, zero_skip;
+};
+
+// The kernel family a launch takes and its tiling.
+struct ConvChoice {
+    int kernel;   // ConvKernel
+    Plan p, pd;   // tiling (register-staged kernel; pd: the LDS-DMA kernel's)
+    DmaLayout L;  // LDS-DMA staging layout
+    ResPlan rp;   // filter-resident forward
+    int small_kc, small_CH, small_Wpad, small_MM;  // small-M kernel
+    int k4, ksplit;                               // LDS-DMA in-block k split
+    size_t lds;   // dynamic LDS per block
+};
+
+// Kernel selection for a forward or backward_data pass, host only (no device
+// access): the small-M vector kernel for at most four output rows, the
+// filter-resident forward for small fp64 images, else the LDS-DMA implicit
+// GEMM, else the register-staged one.  hipErrorNotSupported when a fused form
+// (pool epilogue, filter banks) needs the LDS-DMA kernel and the shape does
+// not fit it; hipErrorInvalidValue when no tiling fits.
+hipError_t choose_conv(size_t tsz, bool bwd, const ConvGeo &g, ConvChoice &c)
+{
+    c = ConvChoice{};
+    const int HfWf = g.Hf * g.Wf, Q = g.Qh * g.Qw;
+    if (g.M <= kSmallM && !g.pool && !g.csr && g.nbanks <= 1 && !g.require_dma) {
+        const int kc = small_m_plan(tsz, g.M, g.Cs, g.Qw, Q, g.Hf, g.Wf, g.S, c.small_CH,
+                                    c.small_Wpad);
+        if (kc >= 1) {
+            c.kernel = kConvSmallM;
+            c.small_kc = kc;
+            c.small_MM = g.M == 1 ? 1 : kSmallM;
+            // the chunk buffers, or the final reduction ([4 waves][4 rows][64 pixels])
+            c.lds = tsz * ((size_t)kc * c.small_CH + (size_t)kc * c.small_MM * HfWf);
+            const size_t red = tsz * kSmallWaves * kSmallM * kSmallPix;
+            if (c.lds < red) c.lds = red;
+            return hipSuccess;
+        }
+    }
+    // The filter-resident forward, fp64 only (in fp32 the 64-row tiles measured
+    // faster on LeNet conv2: 40 against 43 us); it has no zero-skip form.
+    if (!bwd && tsz == 8 && !g.csr && g.nbanks <= 1 && !g.zero_skip && g.M >= kResRows &&
+        res_plan(tsz, g.M, g.Cs, g.Sh, g.Sw, g.Qh, g.Qw, g.Hf, g.Wf, g.S, g.nimg, g.pool, c.rp)) {
+        c.kernel = kConvResident;
+        c.lds = c.rp.lds;
+        return hipSuccess;
+    }
+    if (!make_plan(tsz, g.M, g.Cs, g.Qw, Q, g.Hf, g.Wf, g.S, g.nimg, c.p,
+                   g.pool ? g.Qw * g.PS : 0))
+        return g.pool ? hipErrorNotSupported : hipErrorInvalidValue;
+    const size_t img_bytes = (size_t)g.Cs * g.Sh * g.Sw * tsz;
+    const size_t w_bytes = (size_t)g.M * g.Cs * HfWf * tsz;
+    if (g.csr) c.p.pipelined = 0;  // sparse staging is the direct path only
+    c.pd = c.p;
+    if (!g.csr && make_dma_plan(tsz, bwd, g.M, g.Cs, HfWf, c.p.CH / c.p.Wpad, c.p.Wpad,
+                                img_bytes, w_bytes, c.pd, c.L)) {
+        c.kernel = kConvDma;
+        // The smallest tiles (NB = 1: small layers with few blocks) split the
+        // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
+        // when a chunk has enough steps to share (12+) and enough rows (M > 16).
+        // (LeNet conv2 forward, 13 steps a chunk: 64 -> 60 us against the 2 x 2
+        // wave form.)
+        c.k4 = (c.pd.NB == 1 && c.pd.KCK >= 48 && g.M > 16) ? (g.M <= 32 ? 2 : 4) : 0;
+        c.ksplit = !c.k4 && g.M <= 32;
+        if (c.ksplit) {  // the partial-tile hand-over reuses the stages
+            const size_t red = tsz * (size_t)2 * 2 * c.pd.NB * 4 * kWave;
+            if (c.pd.lds < red) c.pd.lds = red;
+        }
+        if (c.k4) {  // so do the four partial tiles
+            const size_t red = tsz * (size_t)4 * 64 * 32;
+            if (c.pd.lds < red) c.pd.lds = red;
+        }
+        if (g.pool) {  // so does the pooling tile (32 rows x 32 NB)
+            const size_t pt = tsz * (size_t)32 * 32 * c.pd.NB;
+            if (c.pd.lds < pt) c.pd.lds = pt;
+            if (c.pd.lds > (tsz == 4 ? kLdsPerBlock32 : kLdsPerBlock)) return hipErrorNotSupported;
+        }
+        c.lds = c.pd.lds;
+        return hipSuccess;
+    }
+    if (g.pool || g.require_dma) return hipErrorNotSupported;  // fused epilogues: LDS-DMA only
+    c.kernel = kConvReg;
+    c.lds = c.p.lds;
+    return hipSuccess;
+}
+
 template <typename T, bool BWD>
 hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, int zero_skip,
                         hipStream_t s)
 {
-    Plan p;
     a.M = M;
     a.Cs = Cs;
     a.Qw = Qw;
     a.Q = Qh * Qw;
     a.HfWf = a.Hf * a.Wf;
     const bool pool = !BWD && a.pool_out;
-    if (M <= kSmallM && !pool && !a.csr && a.nbanks <= 1 && !a.require_dma) {
-        int CH, Wpad;
-        const int kc = small_m_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, CH, Wpad);
-        if (kc >= 1) {
-            a.KC = kc;
-            a.CH = CH;
-            a.Wpad = Wpad;
-            auto pick = [&](auto mm) {
-                constexpr int MM = decltype(mm)::value;
-                return a.Wf == 3 ? conv_small_m_kernel<T, BWD, 3, MM>
-                                 : (a.Wf == 5 ? conv_small_m_kernel<T, BWD, 5, MM>
-                                              : conv_small_m_kernel<T, BWD, 0, MM>);
-            };
-            auto k = M == 1 ? pick(std::integral_constant<int, 1>())
-                            : pick(std::integral_constant<int, kSmallM>());
-            const int MM = M == 1 ? 1 : kSmallM;
-            // the chunk buffers, or the final reduction ([4 waves][4 rows][64 pixels])
-            size_t lds = sizeof(T) * ((size_t)kc * CH + (size_t)kc * MM * a.HfWf);
-            const size_t red = sizeof(T) * kSmallWaves * kSmallM * kSmallPix;
-            if (lds < red) lds = red;
-            hipError_t e = allow_dynamic_lds(k, lds);
-            if (e != hipSuccess) return e;
-            dim3 grid((a.Q + kSmallPix - 1) / kSmallPix, nimg);
-            hipLaunchKernelGGL(k, grid, dim3(kSmallPix * kSmallWaves), lds, s, a);
-            return hipGetLastError();
-        }
+    ConvGeo g = {M, Cs, a.Sh, a.Sw, Qh, Qw, a.Hf, a.Wf, a.S, nimg, pool, a.PS, a.csr,
+                 a.nbanks, a.require_dma, zero_skip};
+    ConvChoice c;
+    const hipError_t ce = choose_conv(sizeof(T), BWD, g, c);
+    if (ce != hipSuccess) return ce;
+    if (c.kernel == kConvSmallM) {
+        a.KC = c.small_kc;
+        a.CH = c.small_CH;
+        a.Wpad = c.small_Wpad;
+        auto pick = [&](auto mm) {
+            constexpr int MM = decltype(mm)::value;
+            return a.Wf == 3 ? conv_small_m_kernel<T, BWD, 3, MM>
+                             : (a.Wf == 5 ? conv_small_m_kernel<T, BWD, 5, MM>
+                                          : conv_small_m_kernel<T, BWD, 0, MM>);
+        };
+        auto k = M == 1 ? pick(std::integral_constant<int, 1>())
+                        : pick(std::integral_constant<int, kSmallM>());
+        hipError_t e = allow_dynamic_lds(k, c.lds);
+        if (e != hipSuccess) return e;
+        dim3 grid((a.Q + kSmallPix - 1) / kSmallPix, nimg);
+        hipLaunchKernelGGL(k, grid, dim3(kSmallPix * kSmallWaves), c.lds, s, a);
+        return hipGetLastError();
     }
-    // The filter-resident forward, fp64 only (in fp32 the 64-row tiles measured
-    // faster on LeNet conv2: 40 against 43 us).
     if constexpr (!BWD && sizeof(T) == 8) {
-        ResPlan rp;
-        if (!a.csr && a.nbanks <= 1 && !zero_skip && M >= kResRows &&
-            res_plan(sizeof(T), M, Cs, Qh, Qw, a.Hf, a.Wf, a.S, nimg, pool, rp)) {
+        if (c.kernel == kConvResident) {
+            const ResPlan &rp = c.rp;
             a.KC = rp.KC;
             a.KCK = rp.KCK;
             a.SA = rp.SA;
@@ -1502,8 +1593,8 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
             return hipGetLastError();
         }
     }
-    if (!make_plan(sizeof(T), M, Cs, Qw, a.Q, a.Hf, a.Wf, a.S, nimg, p, pool ? Qw * a.PS : 0))
-        return pool ? hipErrorNotSupported : hipErrorInvalidValue;
+    if (c.kernel == kConvResident) return hipErrorInvalidValue;  // not reached
+    const Plan &p = c.p;
     a.tiles_per_img = p.tiles_per_img;
     a.TS = p.TS;
     a.KC = p.KC;
@@ -1515,14 +1606,9 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.magic_kck = host_magic(p.KCK);
     a.magic_hw = host_magic(a.HfWf);
     a.magic_wf = host_magic(a.Wf);
-
-    const size_t img_bytes = (size_t)Cs * a.Sh * a.Sw * sizeof(T);
-    const size_t w_bytes = (size_t)M * Cs * a.HfWf * sizeof(T);
-    if (a.csr) a.pipelined = 0;  // sparse staging is the direct path only
-    Plan pd = p;
-    DmaLayout L;
-    if (!a.csr && make_dma_plan(sizeof(T), BWD, M, Cs, a.HfWf, p.CH / p.Wpad, p.Wpad, img_bytes, w_bytes, pd,
-                      L)) {
+    if (c.kernel == kConvDma) {
+        const Plan &pd = c.pd;
+        const unsigned w_bytes = (unsigned)((size_t)M * Cs * a.HfWf * sizeof(T));
         IgemmArgs ad = a;
         ad.KC = pd.KC;
         ad.KCK = pd.KCK;
@@ -1530,35 +1616,15 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         ad.magic_wpad = host_magic(pd.Wpad);
         ad.magic_sa = host_magic(pd.SA);
         ad.magic_qw = host_magic(Qw);
-        // The smallest tiles (NB = 1: small layers with few blocks) split the
-        // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
-        // when a chunk has enough steps to share (12+) and enough rows (M > 16).
-        // (LeNet conv2 forward, 13 steps a chunk: 64 -> 60 us against the 2 x 2
-        // wave form.)
-        ad.k4 = (pd.NB == 1 && pd.KCK >= 48 && M > 16) ? (M <= 32 ? 2 : 4) : 0;
-        ad.ksplit = !ad.k4 && M <= 32;
-        if (ad.ksplit) {  // the partial-tile hand-over reuses the stages
-            const size_t red = sizeof(T) * (size_t)2 * 2 * pd.NB * 4 * kWave;
-            if (pd.lds < red) pd.lds = red;
-        }
-        if (ad.k4) {  // so do the four partial tiles
-            const size_t red = sizeof(T) * (size_t)4 * 64 * 32;
-            if (pd.lds < red) pd.lds = red;
-        }
-        if (pool) {  // so does the pooling tile (32 rows x 32 NB)
-            const size_t pt = sizeof(T) * (size_t)32 * 32 * pd.NB;
-            if (pd.lds < pt) pd.lds = pt;
-            if (pd.lds > (sizeof(T) == 4 ? kLdsPerBlock32 : kLdsPerBlock))
-                return hipErrorNotSupported;
-        }
+        ad.k4 = c.k4;
+        ad.ksplit = c.ksplit;
         switch (pd.NB) {
-        case 7: return launch_dma<T, 7, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
-        case 4: return launch_dma<T, 4, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
-        case 2: return launch_dma<T, 2, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
-        default: return launch_dma<T, 1, BWD>(ad, pd, L, (unsigned)w_bytes, nimg, zero_skip, s);
+        case 7: return launch_dma<T, 7, BWD>(ad, pd, c.L, w_bytes, nimg, zero_skip, s);
+        case 4: return launch_dma<T, 4, BWD>(ad, pd, c.L, w_bytes, nimg, zero_skip, s);
+        case 2: return launch_dma<T, 2, BWD>(ad, pd, c.L, w_bytes, nimg, zero_skip, s);
+        default: return launch_dma<T, 1, BWD>(ad, pd, c.L, w_bytes, nimg, zero_skip, s);
         }
     }
-    if (pool || a.require_dma) return hipErrorNotSupported;  // fused epilogues: LDS-DMA only
     switch (p.NB) {
     case 7: return launch_nb<T, 7, BWD>(a, p, nimg, zero_skip, s);
     case 4: return launch_nb<T, 4, BWD>(a, p, nimg, zero_skip, s);
@@ -1568,6 +1634,58 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
 }
 
 }  // namespace
+
+hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
+                          ConvPlanInfo &info)
+{
+    info = ConvPlanInfo{};
+    if (pass == 1) return wgrad_plan_info(dtype, d, info);
+    const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
+    const bool bwd = pass == 2;
+    // backward_data is the same GEMM over the up-sampled gradient: M = C rows,
+    // F source channels of Hout x Wout, Hin x Win output pixels, stride 1
+    const ConvGeo g = bwd ? ConvGeo{d.C, d.F, d.Hout, d.Wout, d.Hin, d.Win, d.Hf, d.Wf, 1, d.N,
+                                    false, 0, 0, 0, 0, zero_skip}
+                          : ConvGeo{d.F, d.C, d.Hin, d.Win, d.Hout, d.Wout, d.Hf, d.Wf, d.stride,
+                                    d.N, false, 0, 0, 0, 0, zero_skip};
+    ConvChoice c;
+    const hipError_t e = choose_conv(tsz, bwd, g, c);
+    if (e != hipSuccess) return e;
+    const int Q = g.Qh * g.Qw;
+    info.kernel = c.kernel;
+    info.lds = c.lds;
+    info.k_split = 1;
+    switch (c.kernel) {
+    case kConvSmallM:
+        info.tile_m = c.small_MM;
+        info.tile_pixels = kSmallPix;
+        info.blocks = (Q + kSmallPix - 1) / kSmallPix * d.N;
+        info.chunk = c.small_kc;
+        info.window_width = c.small_Wpad;
+        info.window_rows = c.small_CH / c.small_Wpad;
+        break;
+    case kConvResident:
+        info.tile_m = kResRows;
+        info.tile_pixels = Q;
+        info.blocks = d.N * ((g.M + kResRows - 1) / kResRows);
+        info.chunk = c.rp.KC;
+        info.k_split = kResKs;
+        info.window_width = c.rp.Wpad;
+        info.window_rows = c.rp.CH / c.rp.Wpad;
+        break;
+    default: {
+        const Plan &p = c.kernel == kConvDma ? c.pd : c.p;
+        info.tile_m = kBM;
+        info.tile_pixels = 32 * p.NB;
+        info.blocks = d.N * p.tiles_per_img * p.m_tiles;
+        info.chunk = p.KC;
+        info.k_split = c.k4 ? 4 : (c.ksplit ? 2 : 1);
+        info.window_width = p.Wpad;
+        info.window_rows = p.CH / p.Wpad;
+    }
+    }
+    return hipSuccess;
+}
 
 hipError_t launch_conv_forward(int dtype, const void *X, const void *W, const void *b, void *out,
                                const ConvDims &d, int relu, int zero_skip, hipStream_t s)

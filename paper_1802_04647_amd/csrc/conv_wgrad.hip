@@ -17,6 +17,15 @@
 // channels of its k-range (zero padded).  Each of the 4 waves owns all 64 f rows
 // and NBW 16-column blocks of the k-range: per 4-pixel step it reads 4 g
 // fragments and NBW patch fragments and issues 4 x NBW MFMAs.
+//
+// Zero skip (the ZSKIP instantiations; paper, Section 3 "Sparse Operations":
+// operations that are safe on sparse inputs do fewer flops): an MFMA whose g
+// fragment (16 filters x 4 pixels of the masked gradient) or patch fragment
+// (4 pixels x 16 columns of X) is entirely zero, by a wavefront ballot, is not
+// issued.  Its product is exactly zero, so the result is bitwise that of the
+// dense kernel up to the sign of zero results.
+#include <algorithm>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -28,7 +37,9 @@ constexpr int kBM = 64;
 constexpr size_t kLdsBudget = 72 * 1024;
 // Upper bound on resident blocks (256 CUs x 4 blocks) used to size the workspace
 // without a device; the launch uses the measured occupancy, up to this bound.
-constexpr int kMaxResident = 1024;
+constexpr int kCUs = 256;          // MI355X compute units
+constexpr int kMaxThreadsPerCU = 2048;
+constexpr size_t kLdsPerCU = 160 * 1024;
 constexpr int kMinTiles = 2;  // fewest pixel tiles a split reduces
 constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
 constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
@@ -45,7 +56,7 @@ struct WgradArgs {
     unsigned long long magic_rq, magic_wpad, magic_ch, magic_wout, magic_hwf, magic_wf;
 };
 
-template <typename T, int NBW>
+template <typename T, int NBW, bool ZSKIP>
 __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
@@ -254,10 +265,16 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             for (int mb = 0; mb < 4; ++mb) nav[mb] = grow[mb * 16 * a.SG + qq + 4];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) nbv[nb] = s_x[kof[nb] + nqo];
+            bool za[4];
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
+            for (int mb = 0; mb < 4; ++mb) za[mb] = ZSKIP && wave_all_zero(av[mb]);
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv[nb], acc[mb][nb]);
+            for (int nb = 0; nb < NBW; ++nb) {
+                if (ZSKIP && wave_all_zero(bv[nb])) continue;
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+                    if (!za[mb]) acc[mb][nb] = MF::mma(av[mb], bv[nb], acc[mb][nb]);
+            }
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb) av[mb] = nav[mb];
 #pragma unroll
@@ -346,7 +363,7 @@ constexpr int kRingWaves = kRingThreads / kWave;
 constexpr int kRG = 5;  // g-tile elements each thread stages per tile
 constexpr int kRX = 5;  // new X-row elements each thread stages per tile
 
-template <typename T, int NBW>
+template <typename T, int NBW, bool ZSKIP>
 __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
@@ -517,11 +534,16 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             T av[4];
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb) av[mb] = grow[mb * 16 * a.SG + qq];
+            bool za[4];
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) za[mb] = ZSKIP && wave_all_zero(av[mb]);
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) {
                 const T bv = s_x[kof[nb] + qo];
+                if (ZSKIP && wave_all_zero(bv)) continue;
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
+                for (int mb = 0; mb < 4; ++mb)
+                    if (!za[mb]) acc[mb][nb] = MF::mma(av[mb], bv, acc[mb][nb]);
             }
         }
 
@@ -572,6 +594,20 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     }
 }
 
+// The most splits a launch may use, and the workspace holds: one resident
+// round of blocks on a 256-CU device at one CU's LDS and thread limits (the
+// launch takes the occupancy HIP reports, which is never above these), with at
+// least kMinTiles pixel tiles per split.
+long long split_bound(size_t lds, int threads, int per_split, long long T_total)
+{
+    long long per_cu = (long long)(kLdsPerCU / std::max<size_t>(lds, 1));
+    per_cu = std::min<long long>(per_cu, kMaxThreadsPerCU / threads);
+    per_cu = std::max<long long>(per_cu, 1);
+    long long sp = kCUs * per_cu / per_split;
+    sp = std::min(sp, T_total / kMinTiles);
+    return std::max<long long>(sp, 1);
+}
+
 struct WPlan {
     int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined, spr;
     long long T_total;
@@ -614,11 +650,7 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
         p.pipelined = kBM * p.RQ <= kThreads * kMG && (long long)nch_alloc * p.CH <= kThreads * kMX;
         p.tiles_per_img = d.Hout * spr;
         p.T_total = (long long)d.N * p.tiles_per_img;
-        const int per_split = p.nkr * p.nft;
-        long long splits = (kMaxResident + per_split - 1) / per_split;
-        if (splits > p.T_total) splits = p.T_total;
-        if (splits < 1) splits = 1;
-        p.splits = (int)splits;
+        p.splits = (int)split_bound(p.lds, kThreads, p.nkr * p.nft, p.T_total);
         return true;
     }
     // Pixel tile: whole output rows (at most 56 pixels so the g tile fits the
@@ -647,11 +679,7 @@ bool make_wplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.pipelined = kBM * p.RQ <= kThreads * kMG && (long long)nch_alloc * p.CH <= kThreads * kMX;
     p.tiles_per_img = (Q + p.RQ - 1) / p.RQ;
     p.T_total = (long long)d.N * p.tiles_per_img;
-    const int per_split = p.nkr * p.nft;
-    long long splits = (kMaxResident + per_split - 1) / per_split;
-    if (splits > p.T_total) splits = p.T_total;
-    if (splits < 1) splits = 1;
-    p.splits = (int)splits;  // the most splits a launch may use (workspace size)
+    p.splits = (int)split_bound(p.lds, kThreads, p.nkr * p.nft, p.T_total);
     return true;
 }
 
@@ -695,27 +723,22 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.pipelined = 1;
     p.tiles_per_img = d.Hout;
     p.T_total = (long long)d.N * d.Hout;
-    const int per_split = p.nkr * p.nft;
-    long long splits = (kMaxResident + per_split - 1) / per_split;
-    if (splits > p.T_total) splits = p.T_total;
-    if (splits < 1) splits = 1;
-    p.splits = (int)splits;
+    p.splits = (int)split_bound(p.lds, kRingThreads, p.nkr * p.nft, p.T_total);
     return true;
 }
 
-template <typename T>
+template <typename T, bool ZSKIP>
 hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3>
-                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2> : conv_wgrad_ring_kernel<T, 1>);
+    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP>
+                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP>
+                                      : conv_wgrad_ring_kernel<T, 1, ZSKIP>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
     int splits = resident_slots(k, kRingThreads, p.lds) / per_split;
-    const long long cap = p.T_total / kMinTiles;
-    if (splits > cap) splits = (int)cap;
-    if (splits < 1) splits = 1;
     if (splits > p.splits) splits = p.splits;
+    if (splits < 1) splits = 1;
     a.splits = splits;
     hipLaunchKernelGGL(k, dim3(splits * per_split), dim3(kRingThreads), p.lds, s, a);
     e = hipGetLastError();
@@ -728,11 +751,12 @@ hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStrea
     return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, bool ZSKIP>
 hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3> : (p.NBW == 2 ? conv_wgrad_kernel<T, 2>
-                                                                : conv_wgrad_kernel<T, 1>);
+    auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3, ZSKIP>
+                        : (p.NBW == 2 ? conv_wgrad_kernel<T, 2, ZSKIP>
+                                      : conv_wgrad_kernel<T, 1, ZSKIP>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     // One resident round: as many splits as the device holds blocks at once (a
@@ -740,12 +764,11 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
     const int per_split = p.nkr * p.nft;
     int slots = resident_slots(k, kThreads, p.lds);
     int splits = slots / per_split;
-    // at least kMinTiles tiles per split: tiny layers would otherwise spend their
-    // time in block start-up and in the split reduction
-    const long long cap = p.T_total / kMinTiles;
-    if (splits > cap) splits = (int)cap;
-    if (splits < 1) splits = 1;
+    // at most p.splits: at least kMinTiles tiles per split (tiny layers would
+    // otherwise spend their time in block start-up and in the split reduction)
+    // and within the workspace
     if (splits > p.splits) splits = p.splits;
+    if (splits < 1) splits = 1;
     a.splits = splits;
     dim3 grid(splits * per_split), block(kThreads);
     hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
@@ -759,17 +782,48 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
     return hipGetLastError();
 }
 
+// The plan a backward_filter call takes: the row ring when the layer suits it,
+// else the 4-wave split kernel.
+bool choose_wplan(size_t tsz, const ConvDims &d, WPlan &p, bool &ring)
+{
+    WPlan r;
+    ring = make_rplan(tsz, d, r);
+    if (ring) {
+        p = r;
+        return true;
+    }
+    return make_wplan(tsz, d, p);
+}
+
 }  // namespace
 
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d)
 {
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
-    WPlan p, r;
-    if (!make_wplan(tsz, d, p)) return 0;
-    int splits = p.splits;
-    if (make_rplan(tsz, d, r) && r.splits > splits) splits = r.splits;
+    WPlan p;
+    bool ring;
+    if (!choose_wplan(tsz, d, p, ring)) return 0;
     const size_t K = (size_t)d.C * d.Hf * d.Wf;
-    return tsz * (size_t)splits * ((size_t)d.F * K + (size_t)d.F);
+    return tsz * (size_t)p.splits * ((size_t)d.F * K + (size_t)d.F);
+}
+
+hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info)
+{
+    const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
+    WPlan p;
+    bool ring;
+    if (!choose_wplan(tsz, d, p, ring)) return hipErrorInvalidValue;
+    info.kernel = ring ? kWgradRing : kWgradTiles;
+    info.tile_m = kBM;
+    info.tile_pixels = p.RQ;
+    info.blocks = p.nkr * p.nft;
+    info.chunk = p.KR;
+    info.k_split = 1;
+    info.splits = p.splits;
+    info.window_width = p.Wpad;
+    info.window_rows = p.rows_max;
+    info.lds = p.lds;
+    return hipSuccess;
 }
 
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
@@ -777,10 +831,10 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
                                        const ConvDims &d, void *ws, int zero_skip,
                                        hipStream_t s)
 {
-    (void)zero_skip;
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
     WPlan p;
-    if (!make_wplan(tsz, d, p)) return hipErrorInvalidValue;
+    bool ring;
+    if (!choose_wplan(tsz, d, p, ring)) return hipErrorInvalidValue;
     WgradArgs a = {};
     a.X = X;
     a.dout = dout;
@@ -815,31 +869,23 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.spr = p.spr;
     a.magic_rq = host_magic(p.RQ);
     a.magic_wpad = host_magic(p.Wpad);
-    a.magic_ch = host_magic(p.CH);
     a.magic_wout = host_magic(d.Wout);
     a.magic_hwf = host_magic(a.HfWf);
     a.magic_wf = host_magic(d.Wf);
-    WPlan r;
-    if (make_rplan(tsz, d, r)) {
-        WgradArgs b = a;
-        b.KR = r.KR;
-        b.nkr = r.nkr;
-        b.RQ = r.RQ;
-        b.tiles_per_img = r.tiles_per_img;
-        b.T_total = (int)r.T_total;
-        b.Wpad = r.Wpad;
-        b.CH = r.CH;
-        b.SG = r.SG;
-        b.rows_max = r.rows_max;
-        b.spr = 0;
-        b.magic_rq = host_magic(r.RQ);
-        b.magic_wpad = host_magic(r.Wpad);
-        b.magic_ch = host_magic((d.stride < d.Hf ? d.stride : d.Hf) * r.Wpad);
-        if (dtype == 0) return launch_ring<double>(b, r, dW, db, s);
-        return launch_ring<float>(b, r, dW, db, s);
+    if (ring) {
+        // the ring's new-row staging divides by the new rows' span per channel
+        a.magic_ch = host_magic((d.stride < d.Hf ? d.stride : d.Hf) * p.Wpad);
+        if (dtype == 0)
+            return zero_skip ? launch_ring<double, true>(a, p, dW, db, s)
+                             : launch_ring<double, false>(a, p, dW, db, s);
+        return zero_skip ? launch_ring<float, true>(a, p, dW, db, s)
+                         : launch_ring<float, false>(a, p, dW, db, s);
     }
-    if (dtype == 0) return launch_w<double>(a, p, dW, db, s);
-    return launch_w<float>(a, p, dW, db, s);
+    a.magic_ch = host_magic(p.CH);
+    if (dtype == 0)
+        return zero_skip ? launch_w<double, true>(a, p, dW, db, s)
+                         : launch_w<double, false>(a, p, dW, db, s);
+    return zero_skip ? launch_w<float, true>(a, p, dW, db, s) : launch_w<float, false>(a, p, dW, db, s);
 }
 
 }  // namespace dmlnn

@@ -13,6 +13,32 @@ struct ConvDims {
     int N, C, Hin, Win, F, Hf, Wf, stride, pad, Hout, Wout;
 };
 
+// Kernel families of the conv2d passes (reported by the plan query).
+enum ConvKernel {
+    kConvDma = 1,       // implicit GEMM, LDS-DMA staging (forward / backward_data)
+    kConvReg = 2,       // implicit GEMM, register-staged (forward / backward_data)
+    kConvSmallM = 3,    // vector-ALU kernel for at most four output rows
+    kConvResident = 4,  // filter-resident forward for small images (fp64)
+    kWgradRing = 5,     // backward_filter, row ring over the whole k range
+    kWgradTiles = 6     // backward_filter, 4-wave (f-tile, k-range, split) blocks
+};
+
+// What the plan query reports about one pass (host only, no device access).
+struct ConvPlanInfo {
+    int kernel;        // ConvKernel
+    int tile_m;        // GEMM rows of a block tile
+    int tile_pixels;   // output pixels of a block tile (backward_filter: a pixel tile)
+    int blocks;        // blocks of the main launch (backward_filter: per split)
+    int chunk;         // source channels staged per chunk (backward_filter: k columns a block covers)
+    int k_split;       // in-block split of the k-steps: 1, 2 or 4
+    int splits;        // backward_filter: the most reduction splits a launch uses
+    int window_width;  // staged window row length (elements)
+    int window_rows;   // staged window rows per channel
+    size_t lds;        // dynamic LDS bytes per block
+};
+hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
+                          ConvPlanInfo &info);
+
 // Forward (relu(conv + b)) and input-gradient passes share one implicit-GEMM
 // kernel family; see conv_igemm.hip.
 hipError_t launch_conv_forward(int dtype, const void *X, const void *W, const void *b, void *out,
@@ -43,6 +69,8 @@ hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
 
 // Filter/bias gradient: split reduction into a workspace, then a fixed-order sum.
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d);
+// The backward_filter part of conv_plan_info.
+hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info);
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
                                        const void *out_fwd, void *dW, void *db,
                                        const ConvDims &d, void *ws, int zero_skip,

@@ -1,6 +1,7 @@
-// Fused softmax + cross-entropy forward and backward (paper, Section 2 listing:
-// probs = softmax::forward(scores); dprobs = cross_entropy_loss::backward(probs, y);
-// dscores = softmax::backward(dprobs, scores)).  Per row, with m = max_k s:
+// Fused softmax + cross-entropy forward and backward (paper, Section 2: the
+// softmax classifier's training loop chains the softmax forward, the
+// cross-entropy backward and the softmax backward; here the three are one pass
+// whose result equals that chain).  Per row, with m = max_k s:
 //   p = exp(s - m) / sum exp(s - m)
 //   row loss = -sum_k y (s - m - log sum exp(s - m))
 //   ds = (p * sum_k y - y) / N

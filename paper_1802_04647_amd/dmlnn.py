@@ -37,6 +37,19 @@ class DmlnnError(RuntimeError):
 
 _lib = None
 _vp = ctypes.c_void_p
+
+
+class ConvPlan(ctypes.Structure):
+    """dmlnn_conv_plan of include/dmlnn.h."""
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "kernel", "zero_skip", "tile_m", "tile_pixels", "blocks", "chunk", "k_split", "splits",
+        "window_width", "window_rows")] + [("lds_bytes", ctypes.c_size_t),
+                                           ("workspace_bytes", ctypes.c_size_t)]
+
+
+KERNELS = {1: "igemm_dma", 2: "igemm_reg", 3: "small_m", 4: "resident", 5: "wgrad_ring",
+           6: "wgrad_tiles"}
+PASSES = {"forward": 0, "backward_filter": 1, "backward_data": 2}
 _i = ctypes.c_int
 
 
@@ -81,6 +94,8 @@ def load():
         "adam_update": (_i, [_i, _vp, _vp, _vp, _vp] + [ctypes.c_double] * 4
                         + [ctypes.c_longlong, ctypes.c_longlong, _vp]),
         "count_nonzero": (_i, [_i, _vp, ctypes.c_longlong, _vp, _vp]),
+        "conv2d_plan": (_i, [_i] * 12 + [ctypes.POINTER(ConvPlan)]),
+        "conv2d_zero_skip_choice": (_i, [_i, _i, ctypes.c_longlong] + [_i] * 9),
         "dmlnn_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -154,6 +169,29 @@ def set_zero_skip(mode: int) -> int:
     r = load().dmlnn_set_zero_skip(int(mode))
     if r < 0:
         raise ValueError(f"invalid zero-skip mode {mode}")
+    return r
+
+
+def conv2d_plan(dtype, pass_name, N, C, Hin, Win, F, Hf, Wf, stride, pad, zero_skip=0) -> dict:
+    """The kernel and tiling a conv2d pass would take (host-only query, no GPU
+    needed); ``kernel`` is named as in ``KERNELS``."""
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    plan = ConvPlan()
+    _check("conv2d_plan", load().conv2d_plan(dt, PASSES[pass_name], N, C, Hin, Win, F, Hf, Wf,
+                                             stride, pad, int(zero_skip), ctypes.byref(plan)))
+    d = {name: getattr(plan, name) for name, _ in ConvPlan._fields_}
+    d["kernel"] = KERNELS[plan.kernel]
+    return d
+
+
+def conv2d_zero_skip_choice(dtype, pass_name, nnz, N, C, Hin, Win, F, Hf, Wf, stride, pad) -> int:
+    """The zero-skip mode (0 or 1) the library's nnz rule picks for a pass whose
+    staged operand has ``nnz`` non-zeros (host only)."""
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    r = load().conv2d_zero_skip_choice(dt, PASSES[pass_name], int(nnz), N, C, Hin, Win, F, Hf, Wf,
+                                       stride, pad)
+    if r < 0:
+        raise ValueError("conv2d_zero_skip_choice: invalid arguments")
     return r
 
 

@@ -183,3 +183,25 @@ def random_conv_case(seed: int, shape: ConvShape, zero_frac: float = 0.0, bias: 
 def rng(seed: int):
     """A plain seeded generator for ad-hoc test data."""
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence(BASE_SEED ^ seed)))
+
+
+def structured_zero_conv_case(seed: int, shape: ConvShape):
+    """X, W, b, dout, mask source with structured zeros (the supplementary input
+    of the zero-skip path): besides ~30% i.i.d. zeros, X has a zero band over
+    the top third of every image and every third channel zero; dout and the
+    mask source (relu of a normal draw) have zero bands over the bottom half of
+    the even-numbered filters and every fourth filter zero.  Whole matrix-core
+    fragments of these inputs are zero, which i.i.d. zeros almost never give."""
+    s = shape
+    X, W, b, dout = random_conv_case(seed, s, zero_frac=0.3)
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(BASE_SEED ^ (seed * 104729 + 7))))
+    X = X.reshape(s.N, s.C, s.Hin, s.Win)
+    X[:, :, : max(1, s.Hin // 3), :] = 0.0
+    X[:, ::3] = 0.0
+    mask = relu_normal(g, (s.N, s.F, s.Hout, s.Wout))
+    dout = dout.reshape(s.N, s.F, s.Hout, s.Wout)
+    for a in (dout, mask):
+        a[:, ::2, s.Hout // 2:, :] = 0.0
+        a[:, 1::4] = 0.0
+    return (X.reshape(s.N, -1).copy(), W, b, dout.reshape(s.N, -1).copy(),
+            mask.reshape(s.N, -1).copy())

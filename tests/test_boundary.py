@@ -1,7 +1,9 @@
 """The C ABI boundary on the CPU: the library loads, exports every entry point
 that include/dmlnn.h declares, and rejects bad arguments on the host with the
-documented status codes before launching anything (no GPU needed: every call
-below fails validation, so no pointer is ever dereferenced)."""
+documented status codes before launching anything.  No GPU is needed and no
+pointer is ever dereferenced: every call below fails validation, except the
+ones marked, which pass it and therefore run only on hosts without a GPU, where
+the device check stops them."""
 import ctypes
 
 import pytest
@@ -42,7 +44,10 @@ def test_workspace_size(lib):
     f = lib.conv2d_backward_filter_workspace_size
     w64 = f(0, 256, 64, 56, 56, 64, 3, 3, 1, 1)
     w32 = f(1, 256, 64, 56, 56, 64, 3, 3, 1, 1)
-    assert w64 > 0 and w32 > 0 and w64 == 2 * w32
+    # splits x (F*K + F) elements of the dtype; the split count follows the
+    # kernel's per-CU occupancy bound (fp32 blocks take half the LDS)
+    FK = 64 * 576 + 64
+    assert w64 > 0 and w32 > 0 and w64 % (8 * FK) == 0 and w32 % (4 * FK) == 0
     assert f(0, 4, 1, 8, 8, 2, 3, 3, 1, 1) > 0
     assert f(7, 4, 1, 8, 8, 2, 3, 3, 1, 1) == 0          # bad dtype
     assert f(0, 0, 1, 8, 8, 2, 3, 3, 1, 1) == 0          # N = 0
@@ -92,9 +97,6 @@ def test_other_validation(lib):
     assert lib.affine_fwd(0, FAKE, FAKE, None, FAKE, 0, 3, 4, 0, None) == ERR_ARG
     assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, None, None, None, 2, 3, 4, None) == ERR_NULL
     assert lib.affine_bwd(0, None, FAKE, FAKE, None, FAKE, FAKE, None, 2, 3, 4, None) == ERR_NULL
-    # any one output alone is a valid request (it passes argument validation)
-    for outs in ((FAKE, None, None), (None, FAKE, None), (None, None, FAKE)):
-        assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, *outs, 2, 3, 4, None) not in (ERR_NULL, ERR_ARG)
     assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None) == ERR_NULL
     assert lib.sgd_momentum_update(0, FAKE, FAKE, FAKE, 0.1, 0.9, 0, None) == ERR_ARG
     assert lib.count_nonzero(3, FAKE, 10, FAKE, None) == ERR_DTYPE
@@ -109,13 +111,28 @@ def test_zero_skip_mode(lib):
         lib.dmlnn_set_zero_skip(prev)
 
 
-def test_no_device_is_reported_not_crashed(lib):
-    # Without a GPU a valid call must return DMLNN_ERR_DEVICE rather than abort.
+def _skip_on_gpu_host():
+    # Calls below pass validation with never-allocated pointers: on a host with
+    # a GPU they would launch kernels on those addresses, so they run only where
+    # the device check stops them.
     import torch
     if torch.cuda.device_count() > 0:
-        pytest.skip("a GPU is present")
+        pytest.skip("a GPU is present: a call that passes validation would launch")
+
+
+def test_no_device_is_reported_not_crashed(lib):
+    # Without a GPU a valid call must return DMLNN_ERR_DEVICE rather than abort.
+    _skip_on_gpu_host()
     assert _conv_fwd(lib) == ERR_DEVICE
     assert dmlnn.last_error() != ""
+
+
+def test_affine_bwd_accepts_any_single_output(lib):
+    # Any one of dX, dW, db alone is a valid request: validation passes and only
+    # the device check (no GPU here) stops the call.
+    _skip_on_gpu_host()
+    for outs in ((FAKE, None, None), (None, FAKE, None), (None, None, FAKE)):
+        assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, *outs, 2, 3, 4, None) == ERR_DEVICE
 
 
 def test_binding_rejects_host_tensors():

@@ -47,6 +47,12 @@ CASES = [
     (ConvShape(3, 6, 9, 14, 70, 3, 3, 2, 1), 0.5),
     (ConvShape(2, 20, 8, 8, 16, 5, 5, 1, 2), 0.99),   # below 5% density: zero-skip kernel
     (ConvShape(1, 2, 5, 300, 3, 3, 3, 1, 1), 0.6),    # wide rows
+    # strides that leave input columns past the last window (they feed no output
+    # and must not be scattered into the staged row)
+    (ConvShape(2, 3, 8, 8, 16, 3, 3, 2, 0), 0.3),     # leftover 1 > pad 0
+    (ConvShape(1, 4, 10, 11, 8, 3, 3, 3, 1), 0.3),    # leftover 1 = pad 1
+    (ConvShape(1, 4, 10, 12, 8, 3, 3, 3, 1), 0.3),    # leftover 2 > pad 1
+    (ConvShape(2, 5, 9, 13, 6, 2, 2, 4, 0), 0.3),     # leftover 3 > pad 0, 2x2 filter
 ]
 
 

@@ -196,7 +196,8 @@ def test_softmax_closed_forms_and_invariants():
 
 
 def test_softmax_fused_equals_paper_chain():
-    # probs = softmax(scores); dprobs = xent backward; dscores = softmax backward.
+    # the unfused chain of Section 2's example: softmax forward, then the
+    # cross-entropy backward, then the softmax backward
     g = rng(29)
     N, K = 8, 10
     S = g.standard_normal((N, K)) * 2
@@ -222,7 +223,7 @@ def test_sgd_momentum_two_step_closed_form():
     assert np.allclose(th2, th0 - lr * g1 + mu * (-lr * g1) - lr * g2, rtol=1e-14, atol=1e-15)
     th, v = oracle.sgd_momentum_update(th0, g1, np.zeros(11), 0.0, mu)
     assert np.array_equal(th, th0)
-    # mu = 0 is the paper listing's plain update W - lr*dW
+    # mu = 0 is the plain gradient step of Section 2's example
     th, _ = oracle.sgd_momentum_update(th0, g1, np.zeros(11), lr, 0.0)
     assert np.array_equal(th, th0 - lr * g1)
 

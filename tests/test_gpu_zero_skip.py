@@ -47,6 +47,11 @@ def _plans(s, dt):
             for p in ("forward", "backward_filter", "backward_data")}
 
 
+def _plan_key(s, dt, pname, zs):
+    p = dmlnn.conv2d_plan(TORCH[dt], pname, *s.args(), zero_skip=zs)
+    return (p["kernel"], p["k_split"], p["tile_pixels"], p["chunk"], p["splits"])
+
+
 def _passes(s, X, W, b, dout, mask, dt):
     a = _args(s)
     out, _, _ = dmlnn.conv2d_forward(dev(X, dt), dev(W, dt), dev(b, dt), *a, relu=True)
@@ -66,8 +71,16 @@ def _skip_on_vs_oracle(s, X, W, b, dout, mask, dt):
         off = _passes(s, X, W, b, dout, mask, dt)
     finally:
         dmlnn.set_zero_skip(prev)
-    for u, v, what in zip(on, off, ("forward", "dW", "db", "dX")):
-        assert torch.equal(u, v), f"{what}: skip path differs from the dense path"
+    # bitwise equal to the dense path of the same kernel form (the filter-resident
+    # forward has no skip form: with the skip on, that pass takes the LDS-DMA
+    # kernel, whose summation order differs; the oracle bound holds for both)
+    same = {p: _plan_key(s, dt, p, 1) == _plan_key(s, dt, p, 0)
+            for p in ("forward", "backward_filter", "backward_data")}
+    for u, v, what, pname in zip(on, off, ("forward", "dW", "db", "dX"),
+                                 ("forward", "backward_filter", "backward_filter",
+                                  "backward_data")):
+        if same[pname]:
+            assert torch.equal(u, v), f"{what}: skip path differs from the dense path"
     ref_out, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
     ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, mask, *a, s.F)
     ref_dX = oracle.conv2d_backward_data(W, dout, mask, *a)

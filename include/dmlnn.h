@@ -105,6 +105,27 @@ DMLNN_API int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const voi
                            int F, int Hf, int Wf, int stride, int pad,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* conv2d_backward_filter for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation, plan and result — bitwise equal to
+ * conv2d_backward_filter for the same arguments — with the split reduction's
+ * partials kept in a scratch array the library holds in device memory
+ * (DMLNN_NOALLOC_SCRATCH_BYTES per GPU, reserved when the library's code is
+ * loaded on that GPU and held until the process ends) instead of a caller
+ * workspace.  The call allocates nothing.  Sizes whose workspace
+ * (conv2d_backward_filter_workspace_size) exceeds DMLNN_NOALLOC_SCRATCH_BYTES
+ * are rejected with DMLNN_ERR_WORKSPACE before anything is launched.  Every
+ * call on one GPU uses that GPU's one scratch array: calls that overlap in time
+ * on one GPU (on different streams, or from different host threads without
+ * ordering) race and give undefined results; calls in one stream order are
+ * safe.  Each call writes every scratch entry it later reads, so nothing left
+ * by an earlier call is ever read. */
+#define DMLNN_NOALLOC_SCRATCH_BYTES (80u * 1024u * 1024u)
+DMLNN_API int conv2d_backward_filter_noalloc(dmlnn_dtype dtype, const void *X, const void *dout,
+                                             const void *out_fwd, void *dW, void *db, int N,
+                                             int C, int Hin, int Win, int F, int Hf, int Wf,
+                                             int stride, int pad, void *stream);
+
 /* Input gradient, with the relu mask fused into the prologue:
  *   dX[n,c,h,w] = sum_{f,i,j} W[f,c,i,j] * g[n,f,(h+pad-i)/stride,(w+pad-j)/stride]
  * over the (i,j) whose quotients are exact and inside the output; input cells

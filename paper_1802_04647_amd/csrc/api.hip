@@ -19,6 +19,13 @@ namespace {
 thread_local char g_err[512] = "";
 std::atomic<int> g_zero_skip{-1};
 
+// Device scratch of conv2d_backward_filter_noalloc: one array per GPU (each
+// device holds its own copy of a __device__ variable), reserved when the code
+// object is loaded on that GPU.  In host code `scratch` names a host-side
+// stand-in, never the device memory: its device address is looked up once per
+// device with hipGetSymbolAddress and only that address is used.
+static __device__ __align__(256) unsigned char scratch[DMLNN_NOALLOC_SCRATCH_BYTES];
+
 int fail(int code, const char *fmt, ...)
 {
     va_list ap;
@@ -69,6 +76,33 @@ int device_check()
     }
     if (state[dev] != 1) return fail(DMLNN_ERR_DEVICE, "device %d is not gfx950", dev);
     return DMLNN_OK;
+}
+
+// Device address of this device's scratch array (looked up on the first call
+// on each device, with that device current), or null after a failed lookup.
+void *scratch_ptr(int &status)
+{
+    static std::mutex mu;
+    static void *ptr[64] = {nullptr};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= 64) {
+        status = fail(DMLNN_ERR_DEVICE, "no usable HIP device (%s)", hipGetErrorString(e));
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lk(mu);
+    if (!ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            status = fail(DMLNN_ERR_DEVICE, "scratch lookup on device %d failed: %s", dev,
+                          hipGetErrorString(e));
+            return nullptr;
+        }
+        ptr[dev] = p;
+    }
+    status = DMLNN_OK;
+    return ptr[dev];
 }
 
 int launched(hipError_t e, const char *what)
@@ -172,6 +206,34 @@ int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const void *dout, c
     return launched(dmlnn::launch_conv_backward_filter(dtype, X, dout, out_fwd, dW, db, d, workspace,
                                                        zero_skip_mode(), (hipStream_t)stream),
                     "conv2d_backward_filter");
+}
+
+int conv2d_backward_filter_noalloc(dmlnn_dtype dtype, const void *X, const void *dout,
+                                   const void *out_fwd, void *dW, void *db, int N, int C, int Hin,
+                                   int Win, int F, int Hf, int Wf, int stride, int pad,
+                                   void *stream)
+{
+    if (!dtype_ok(dtype))
+        return fail(DMLNN_ERR_DTYPE, "conv2d_backward_filter_noalloc: bad dtype %d", (int)dtype);
+    if (!X || !dout || !dW)
+        return fail(DMLNN_ERR_NULL, "conv2d_backward_filter_noalloc: X, dout and dW are required");
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    const size_t need = dmlnn::conv_wgrad_workspace_bytes(dtype, d);
+    if (need == 0)
+        return fail(DMLNN_ERR_ARG, "conv2d_backward_filter_noalloc: no tiling fits these sizes");
+    if (need > (size_t)DMLNN_NOALLOC_SCRATCH_BYTES)
+        return fail(DMLNN_ERR_WORKSPACE,
+                    "conv2d_backward_filter_noalloc: these sizes need %zu bytes of scratch, above "
+                    "the library's %u; use conv2d_backward_filter with a workspace",
+                    need, (unsigned)DMLNN_NOALLOC_SCRATCH_BYTES);
+    if (int r = device_check()) return r;
+    int status = DMLNN_OK;
+    void *ws = scratch_ptr(status);
+    if (!ws) return status;
+    return launched(dmlnn::launch_conv_backward_filter(dtype, X, dout, out_fwd, dW, db, d, ws,
+                                                       zero_skip_mode(), (hipStream_t)stream),
+                    "conv2d_backward_filter_noalloc");
 }
 
 int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void *dout, const void *out_fwd,

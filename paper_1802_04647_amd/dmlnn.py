@@ -69,6 +69,7 @@ def load():
         "conv2d_backward_filter": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9
                                    + [_vp, ctypes.c_size_t, _vp]),
         "conv2d_backward_data": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
+        "conv2d_backward_filter_noalloc": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
         "dmlnn_set_zero_skip": (_i, [_i]),
         "bias_add_relu": (_i, [_i, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
         "max_pool2d_fwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
@@ -240,6 +241,23 @@ def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F
     _check("conv2d_backward_filter", load().conv2d_backward_filter(
         dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
         stride, pad, _p(workspace), workspace.numel() * workspace.element_size(), _stream()))
+    return dW, db
+
+
+def conv2d_backward_filter_noalloc(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F, dW, db=None):
+    """conv2d_backward_filter with the library's own device scratch instead of a
+    workspace: allocates nothing (dW, and db if wanted, are supplied)."""
+    dt = _dtype(X, dout, out_fwd, dW, db)
+    N = X.shape[0]
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    _need(X, N * C * Hin * Win, "X")
+    _need(dout, N * F * max(Hout, 0) * max(Wout, 0), "dout")
+    _need(out_fwd, N * F * max(Hout, 0) * max(Wout, 0), "out_fwd")
+    _need(dW, F * C * Hf * Wf, "dW")
+    _need(db, F, "db")
+    _check("conv2d_backward_filter_noalloc", load().conv2d_backward_filter_noalloc(
+        dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf, stride, pad,
+        _stream()))
     return dW, db
 
 

@@ -161,3 +161,20 @@ def test_optimizer_validation(lib):
         == ERR_ARG                                                       # beta1 = 1
     assert adam(0, FAKE, FAKE, FAKE, None, d(1e-3), d(0.9), d(0.999), d(1e-8), 1, 10, None) \
         == ERR_NULL
+
+
+def test_noalloc_backward_filter_validation(lib):
+    f = lib.conv2d_backward_filter_noalloc
+    # a layer whose split partials (5x5 filters over 256 channels, 61-wide rows:
+    # the tiled kernel) exceed the scratch: rejected before anything else happens
+    big = (64, 256, 8, 61, 64, 5, 5, 1, 2)
+    assert lib.conv2d_backward_filter_workspace_size(0, *big) > 80 * 2 ** 20
+    assert f(0, FAKE, FAKE, None, FAKE, None, *big, None) == ERR_WS
+    assert "scratch" in dmlnn.last_error()
+    # the benchmark layer's partials fit
+    assert lib.conv2d_backward_filter_workspace_size(0, 256, 64, 56, 56, 64, 3, 3, 1, 1) \
+        <= 80 * 2 ** 20
+    assert f(0, None, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_NULL
+    assert f(0, FAKE, FAKE, None, None, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_NULL
+    assert f(9, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_DTYPE
+    assert f(0, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 0, 1, None) == ERR_ARG

@@ -43,6 +43,10 @@ def parse():
                     help="skip the fp32, LeNet, other-config and other-kernel extras")
     ap.add_argument("--only-lenet", action="store_true",
                     help="only time the LeNet training step (for kernel-trace runs)")
+    ap.add_argument("--lenet-trace", choices=("fused", "unfused"),
+                    help="only run the LeNet step in one form, eager and on one stream, so a "
+                         "kernel trace of the run adds up to the step (fused: the conv backward "
+                         "passes read the pool gradients; unfused: pool backward kernels first)")
     return ap.parse_args()
 
 
@@ -126,19 +130,25 @@ def lenet_timing(steps=50, warmup=10):
     from paper_1802_04647_amd.lenet import LeNetTrainer
 
     X, Y, params = lenet_train_inputs()
-    tr = LeNetTrainer(params)
     Xd = torch.from_numpy(X).cuda()
     Yd = torch.from_numpy(Y).cuda()
-    for _ in range(warmup):
-        tr.step(Xd, Yd)
-    torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        tr.step(Xd, Yd)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
+
+    def eager_ms(tr):
+        for _ in range(warmup):
+            tr.step(Xd, Yd)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            tr.step(Xd, Yd)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    # the conv backward passes reading the pool gradients directly (the
+    # step's form), and the pool backward as its own kernel, for comparison
+    ms = eager_ms(LeNetTrainer(params))
+    unfused_ms = eager_ms(LeNetTrainer(params, fused_pool_backward=False))
     # the same step recorded once as a HIP graph and replayed
     gtr = LeNetTrainer(params)
     gtr.capture(Xd, Yd, warmup=2)
@@ -152,7 +162,30 @@ def lenet_timing(steps=50, warmup=10):
     torch.cuda.synchronize()
     gms = e0.elapsed_time(e1) / steps
     return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3), graph_ms_per_step=gms,
-                graph_images_per_s=64.0 / (gms / 1e3))
+                graph_images_per_s=64.0 / (gms / 1e3), unfused_pool_backward_ms_per_step=unfused_ms)
+
+
+def lenet_trace(fused, steps, warmup):
+    """The LeNet step in one form, eager on one stream (kernels back to back)."""
+    import torch
+    from paper_1802_04647_amd.inputs import lenet_train_inputs
+    from paper_1802_04647_amd.lenet import LeNetTrainer
+
+    X, Y, params = lenet_train_inputs()
+    tr = LeNetTrainer(params, fused_pool_backward=fused)
+    tr.two_streams = False
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    for _ in range(warmup):
+        tr.step(Xd, Yd)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        tr.step(Xd, Yd)
+    e1.record()
+    torch.cuda.synchronize()
+    return {"form": "fused" if fused else "unfused", "streams": 1, "steps": steps,
+            "ms_per_step": round(e0.elapsed_time(e1) / steps, 4)}
 
 
 def _median_ms(fn, reps=20, warmup=5, with_min=False):
@@ -215,6 +248,45 @@ def horizontal_fusion_timing():
             "fused_ms": round(fused, 4), "separate_ms": round(sep, 4),
             "fused_tflops": round(flops / (fused / 1e3) / 1e12, 3),
             "separate_tflops": round(flops / (sep / 1e3) / 1e12, 3)}
+
+
+def pooled_backward_timing():
+    """Backward of conv -> relu -> 2x2/2 max-pool on the ResNet-shaped layer
+    (256 x 64 x 56x56, 64 filters 3x3 p1, fp64): both conv backward passes
+    reading the pool's gradient, argmax and pooled values directly, against the
+    pool backward kernel storing the conv-output gradient (411 MB) that the two
+    passes then read."""
+    import torch
+    from paper_1802_04647_amd import dmlnn
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
+
+    s = SHAPES["resnet_conv"]
+    X0, W0, b0, _ = conv_layer_inputs("resnet_conv")
+    X, W, b = (torch.from_numpy(v).cuda() for v in (X0, W0, b0))
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    _, pooled, argmax, Hp, Wp = dmlnn.conv2d_forward_pool(X, W, b, *a, 2, 2, 2, 0)
+    g = torch.Generator(device="cuda").manual_seed(13)
+    dpool = torch.randn(pooled.shape, dtype=torch.float64, device="cuda", generator=g)
+    ws = torch.empty(dmlnn.conv2d_backward_filter_workspace_size(torch.float64, *s.args()),
+                     dtype=torch.uint8, device="cuda")
+    dW, db = torch.empty_like(W), torch.empty_like(b)
+    dX = torch.empty_like(X)
+    dc = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=torch.float64, device="cuda")
+
+    def fused():
+        dmlnn.conv2d_backward_filter_pooled(X, dpool, argmax, pooled, *a, s.F, 2, 2, 2, 0,
+                                            workspace=ws, dW=dW, db=db)
+        dmlnn.conv2d_backward_data_pooled(W, dpool, argmax, pooled, *a, 2, 2, 2, 0, dX=dX)
+
+    def unfused():
+        dmlnn.max_pool2d_bwd_relu(dpool, argmax, pooled, s.F, s.Hout, s.Wout, 2, 2, 2, 0, dX=dc)
+        dmlnn.conv2d_backward_filter(X, dc, None, *a, s.F, workspace=ws, dW=dW, db=db)
+        dmlnn.conv2d_backward_data(W, dc, None, *a, dX=dX)
+
+    f_ms = _median_ms(fused, reps=10, warmup=3)
+    u_ms = _median_ms(unfused, reps=10, warmup=3)
+    return {"shape": "256 x 64 x 56x56, 64 filters 3x3 p1, then relu and 2x2/2 max-pool, fp64",
+            "fused_ms": round(f_ms, 4), "unfused_ms": round(u_ms, 4)}
 
 
 def sparse_conv_timing():
@@ -515,6 +587,10 @@ def main():
     if args.zero_skip_probe:
         print(json.dumps({"zero_skip": zero_skip_timing()}), flush=True)
         return
+    if args.lenet_trace:
+        print(json.dumps({"lenet_trace": lenet_trace(args.lenet_trace == "fused", args.steps,
+                                                     args.warmup)}), flush=True)
+        return
     if args.only_lenet:
         lt = lenet_timing()
         print(json.dumps({"lenet_training": {k: round(v, 4) for k, v in lt.items()}}), flush=True)
@@ -570,10 +646,13 @@ def main():
                                  "ms_per_step": round(lt["ms_per_step"], 4),
                                  "images_per_s": round(lt["images_per_s"], 1),
                                  "hip_graph_ms_per_step": round(lt["graph_ms_per_step"], 4),
-                                 "hip_graph_images_per_s": round(lt["graph_images_per_s"], 1)}
+                                 "hip_graph_images_per_s": round(lt["graph_images_per_s"], 1),
+                                 "unfused_pool_backward_ms_per_step":
+                                     round(lt["unfused_pool_backward_ms_per_step"], 4)}
         rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
         rec["horizontal_fusion"] = horizontal_fusion_timing()
+        rec["pooled_backward"] = pooled_backward_timing()
         rec["sparse_conv"] = sparse_conv_timing()
         rec["zero_skip"] = zero_skip_timing()
         rec["aux_kernels"] = aux_kernel_timing()

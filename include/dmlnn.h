@@ -294,6 +294,36 @@ DMLNN_API int max_pool2d_bwd_relu(dmlnn_dtype dtype, const void *dout, const int
                                   const void *pooled, void *dX, int N, int C, int Hin, int Win,
                                   int Hf, int Wf, int stride, int pad, void *stream);
 
+/* ------------------------------------------- conv2d backward from a pool ----
+ * Paper: Section "Future Work" (vertical fusion across layers); the layers are
+ * Section 2's conv2d -> relu -> max_pool2d, run forward by conv2d_forward_pool.
+ * The conv backward passes take the pool's upstream gradient directly: the
+ * conv's output gradient
+ *   g[n,f,oh,ow] = dpool[n,o] if argmax[n,o] == f*Hout*Wout + oh*Wout + ow and
+ *                  pooled[n,o] > 0, for the window o that covers (oh, ow); else 0
+ * (the result of max_pool2d_bwd_relu) is built while the kernels stage it and
+ * is never stored.  Requires windows that do not overlap and no pool padding
+ * (pool_pad == 0, pool_stride >= pool_h and >= pool_w; for other pools run
+ * max_pool2d_bwd_relu and the plain calls) and Hout, Wout < 65536; else
+ * DMLNN_ERR_ARG.  dpool, argmax and pooled are N x (F*Hp*Wp) with
+ * Hp = conv2d_out_dim(Hout, pool_h, pool_stride, 0) (likewise Wp); argmax and
+ * pooled are those of the forward.  Other arguments, outputs and the workspace
+ * as in conv2d_backward_filter / conv2d_backward_data (same workspace size);
+ * the zero-skip mode has no effect on these calls. */
+DMLNN_API int conv2d_backward_filter_pooled(dmlnn_dtype dtype, const void *X, const void *dpool,
+                                            const int32_t *argmax, const void *pooled, void *dW,
+                                            void *db, int N, int C, int Hin, int Win, int F,
+                                            int Hf, int Wf, int stride, int pad, int pool_h,
+                                            int pool_w, int pool_stride, int pool_pad,
+                                            void *workspace, size_t workspace_bytes,
+                                            void *stream);
+
+DMLNN_API int conv2d_backward_data_pooled(dmlnn_dtype dtype, const void *W, const void *dpool,
+                                          const int32_t *argmax, const void *pooled, void *dX,
+                                          int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                                          int stride, int pad, int pool_h, int pool_w,
+                                          int pool_stride, int pool_pad, void *stream);
+
 /* ----------------------------------------------------------------- affine ----
  * Paper: Section 2 (the affine layer of the softmax-classifier example: the
  * product X W plus a bias row; its backward returns dX, dW, db in that order).  X is N x D, W is D x M, b is 1 x M, out is N x M.

@@ -12,6 +12,7 @@
 #include <mutex>
 
 #include "../../include/dmlnn.h"
+#include "common.hpp"
 #include "internal.hpp"
 
 namespace {
@@ -470,6 +471,81 @@ int conv2d_forward_pool(dmlnn_dtype dtype, const void *X, const void *W, const v
                                            pool_h, pool_w, pool_stride, pool_pad, Hp, Wp, s);
     }
     return launched(e, "conv2d_forward_pool");
+}
+
+// Validation shared by the two pooled backward calls: the pool after the conv
+// must have windows that do not overlap and no padding.
+static int pooled_src(const char *name, const dmlnn::ConvDims &d, const void *dpool,
+                      const int32_t *argmax, const void *pooled, int ph, int pw, int ps, int pp,
+                      dmlnn::PoolSrc &src)
+{
+    int Hp, Wp;
+    if (int r = pool_dims(d.N, d.F, d.Hout, d.Wout, ph, pw, ps, pp, Hp, Wp)) return r;
+    if (pp != 0 || ps < ph || ps < pw)
+        return fail(DMLNN_ERR_ARG,
+                    "%s: the pool windows (%dx%d stride %d pad %d) overlap or are padded; run "
+                    "max_pool2d_bwd_relu and the plain conv backward call instead",
+                    name, ph, pw, ps, pp);
+    if (d.Hout >= 65536 || d.Wout >= 65536)
+        return fail(DMLNN_ERR_ARG, "%s: conv output of %dx%d is too large", name, d.Hout, d.Wout);
+    src.dpool = dpool;
+    src.argmax = argmax;
+    src.pooled = pooled;
+    src.PH = ph;
+    src.PW = pw;
+    src.PS = ps;
+    src.Hp = Hp;
+    src.Wp = Wp;
+    src.magic_ps = dmlnn::host_magic(ps);
+    return DMLNN_OK;
+}
+
+int conv2d_backward_filter_pooled(dmlnn_dtype dtype, const void *X, const void *dpool,
+                                  const int32_t *argmax, const void *pooled, void *dW, void *db,
+                                  int N, int C, int Hin, int Win, int F, int Hf, int Wf, int stride,
+                                  int pad, int pool_h, int pool_w, int pool_stride, int pool_pad,
+                                  void *workspace, size_t workspace_bytes, void *stream)
+{
+    const char *name = "conv2d_backward_filter_pooled";
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "%s: bad dtype %d", name, (int)dtype);
+    if (!X || !dpool || !argmax || !pooled || !dW)
+        return fail(DMLNN_ERR_NULL, "%s: X, dpool, argmax, pooled and dW are required", name);
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    dmlnn::PoolSrc src;
+    if (int r = pooled_src(name, d, dpool, argmax, pooled, pool_h, pool_w, pool_stride, pool_pad,
+                           src))
+        return r;
+    const size_t need = dmlnn::conv_wgrad_workspace_bytes(dtype, d);
+    if (need == 0) return fail(DMLNN_ERR_ARG, "%s: no tiling fits these sizes", name);
+    if (!workspace || workspace_bytes < need)
+        return fail(DMLNN_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name,
+                    need, workspace ? workspace_bytes : (size_t)0);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_backward_filter(dtype, X, nullptr, nullptr, dW, db, d,
+                                                       workspace, 0, (hipStream_t)stream, &src),
+                    name);
+}
+
+int conv2d_backward_data_pooled(dmlnn_dtype dtype, const void *W, const void *dpool,
+                                const int32_t *argmax, const void *pooled, void *dX, int N, int C,
+                                int Hin, int Win, int F, int Hf, int Wf, int stride, int pad,
+                                int pool_h, int pool_w, int pool_stride, int pool_pad, void *stream)
+{
+    const char *name = "conv2d_backward_data_pooled";
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "%s: bad dtype %d", name, (int)dtype);
+    if (!W || !dpool || !argmax || !pooled || !dX)
+        return fail(DMLNN_ERR_NULL, "%s: W, dpool, argmax, pooled and dX are required", name);
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    dmlnn::PoolSrc src;
+    if (int r = pooled_src(name, d, dpool, argmax, pooled, pool_h, pool_w, pool_stride, pool_pad,
+                           src))
+        return r;
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_backward_data(dtype, W, nullptr, nullptr, dX, d, 0,
+                                                     (hipStream_t)stream, &src),
+                    name);
 }
 
 int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out, int N,

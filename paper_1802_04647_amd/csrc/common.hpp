@@ -94,6 +94,38 @@ __device__ __forceinline__ T relu_if(T v, int relu)
     return (relu && !(v > T(0))) ? T(0) : v;
 }
 
+// Gradient of a conv's output taken straight from the backward of a following
+// relu -> max-pool (vertical fusion: the routed gradient is never stored).
+// Windows PH x PW at stride PS >= PH, PW without padding do not overlap, so
+// output cell (oy, ox) of filter f lies in at most one window (py, px); it
+// receives that window's gradient when it is the window's argmax (the in-row
+// index f*Q + oy*Wout + ox) and the pooled value is positive (the routed cell
+// holds the pooled value, so that is its relu mask).
+struct PoolSrc {
+    const void *dpool;       // [N][F][Hp][Wp] gradient of the pooled output
+    const int32_t *argmax;   // [N][F][Hp][Wp] in-row argmax of each window
+    const void *pooled;      // [N][F][Hp][Wp] pooled values
+    int PH, PW, PS, Hp, Wp;
+    unsigned long long magic_ps;  // host_magic(PS); oy, ox < 2^16 (checked on the host)
+};
+
+// Branch-free, so the loads of several cells issue together (a load under a
+// divergent branch is waited for where the branch ends): a cell no window
+// covers reads its plane's first window and is dropped.  (n, f) must name a
+// plane and (oy, ox) lie in [0, 2^16).
+template <typename T>
+__device__ __forceinline__ T pool_src_grad(const PoolSrc &p, int n, int F, int f, int Q, int Wout,
+                                           int oy, int ox)
+{
+    const int py = div_magic(oy, p.magic_ps), px = div_magic(ox, p.magic_ps);
+    const bool in = oy - py * p.PS < p.PH && ox - px * p.PS < p.PW && py < p.Hp && px < p.Wp;
+    const size_t o = ((size_t)n * F + f) * p.Hp * p.Wp + (in ? (size_t)py * p.Wp + px : 0);
+    const T d = reinterpret_cast<const T *>(p.dpool)[o];
+    const int32_t am = p.argmax[o];
+    const T pv = reinterpret_cast<const T *>(p.pooled)[o];
+    return (in && am == f * Q + oy * Wout + ox && pv > T(0)) ? d : T(0);
+}
+
 // Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8).
 // Renumber so that logically consecutive blocks share an XCD (and its L2): with
 // m = floor(n / 8), block b < 8m gets logical id (b % 8) * m + b / 8; the last

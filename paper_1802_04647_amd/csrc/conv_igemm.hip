@@ -83,9 +83,15 @@ struct IgemmArgs {
     const void *csr_val;
     unsigned long long magic_kck, magic_hw, magic_wf;
     unsigned long long magic_wpad, magic_sa, magic_qw;  // LDS-DMA kernel set-up
+    // Pooled source (backward, the PB instantiations): the conv was followed by
+    // relu and a non-overlapping max-pool, and the masked dout is built while
+    // staging from that pool's gradient, argmax and pooled values (src and
+    // mask are unused).
+    int pb;
+    PoolSrc pool;
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP, bool CSR = false>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool CSR = false, bool PB = false>
 __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
 {
     using MF = Mfma<T>;
@@ -132,8 +138,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
         for (int y = 0; y < NB; ++y) acc[x][y] = MF::zero();
 
     const size_t img = (size_t)n * a.Cs * a.Sh * a.Sw;
-    const T *src = reinterpret_cast<const T *>(a.src) + img;
-    const T *msk = (BWD && a.mask) ? reinterpret_cast<const T *>(a.mask) + img : nullptr;
+    const T *src = PB ? nullptr : reinterpret_cast<const T *>(a.src) + img;
+    const T *msk = (BWD && !PB && a.mask) ? reinterpret_cast<const T *>(a.mask) + img : nullptr;
     const T *wgt = reinterpret_cast<const T *>(a.wgt);
 
     // Staging is software-pipelined: the global loads of chunk c0+KC are issued
@@ -153,7 +159,21 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
             const int slot = wave + 4 * it;
             const int r = slot / ncg, cgi = slot - r * ncg;
             T v = T(0), mv = T(1);
-            if (r < nrows) {
+            if (PB) {
+                // branch-free: a clamped cell, dropped when outside the window
+                // (r is wave-uniform, so the row terms are too)
+                const int c = r / rows_need, t = r - c * rows_need;
+                const int cg = c0 + c, yv = ybase + t;
+                const int ys = max(yv, 0) / a.up;
+                const int u = lane + kWave * cgi;
+                const int xv = u - a.Pw;
+                const int xs = max(xv, 0) / a.up;
+                const bool ok = r < nrows && cg < a.Cs && yv >= 0 && ys * a.up == yv &&
+                                ys < a.Sh && u < a.Wpad && xv >= 0 && xs * a.up == xv && xs < a.Sw;
+                const T pg = pool_src_grad<T>(a.pool, n, a.Cs, min(cg, a.Cs - 1), a.Sh * a.Sw,
+                                              a.Sw, min(ys, a.Sh - 1), min(xs, a.Sw - 1));
+                v = ok ? pg : T(0);
+            } else if (r < nrows) {
                 const int c = r / rows_need, t = r - c * rows_need;
                 const int cg = c0 + c, yv = ybase + t;
                 const int ys = yv / a.up;
@@ -250,8 +270,12 @@ __global__ __launch_bounds__(kThreads, 2) void conv_igemm_kernel(IgemmArgs a)
                 const int xv = u - a.Pw;
                 const int xs = xv / a.up;
                 if (rowok && xv >= 0 && xs * a.up == xv && xs < a.Sw) {
-                    v = src[roff + xs];
-                    if (BWD && msk && !(msk[roff + xs] > T(0))) v = T(0);
+                    if (PB) {
+                        v = pool_src_grad<T>(a.pool, n, a.Cs, cg, a.Sh * a.Sw, a.Sw, ys, xs);
+                    } else {
+                        v = src[roff + xs];
+                        if (BWD && msk && !(msk[roff + xs] > T(0))) v = T(0);
+                    }
                 }
                 s_src[r * a.Wpad + u] = v;
             }
@@ -356,7 +380,8 @@ struct DmaLayout {
                 // filter, and no pair mixes a tap with a zero column)
 };
 
-template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL, int K4 = 0>
+template <typename T, int NB, bool BWD, bool ZSKIP, bool KS, bool POOL, int K4 = 0,
+          bool PB = false>
 __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, sizeof(T) == 4 ? 3 : 2))) void conv_igemm_dma_kernel(IgemmArgs a, DmaLayout L,
                                                                      unsigned w_bytes)
 {
@@ -420,7 +445,7 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
 
     const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
     const unsigned img_bytes = (unsigned)(img * sizeof(T));
-    const bool has_mask = BWD && a.mask != nullptr;
+    const bool has_mask = BWD && !PB && a.mask != nullptr;
     const i32x4 rs_src = buffer_rsrc(reinterpret_cast<const T *>(a.src) + (size_t)n * img, img_bytes);
     const i32x4 rs_msk = has_mask ? buffer_rsrc(reinterpret_cast<const T *>(a.mask) + (size_t)n * img,
                                                 img_bytes)
@@ -499,7 +524,7 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
         for (int j = 0; j < kMaxDmaS; ++j) {
             const int ii = wave + 4 * j;
-            if (ii < NIs) {
+            if (!PB && ii < NIs) {
                 dma_dword(rs_src, ps + ii * 256, vs_off[j], so_src);
                 if (has_mask) dma_dword(rs_msk, pm + ii * 256, vs_off[j], so_src);
             }
@@ -519,7 +544,88 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
         }
     };
 
+    // PB: the gradient window of a chunk is written from registers by window
+    // owners.  Element e of a chunk is (channel c, stride region (py, px)) of
+    // the pool: the PS x PS cells whose window is (py, px).  Its owner loads
+    // the window's gradient, argmax and pooled value once and writes the
+    // region's cells that lie in the staged window: the gradient at the argmax
+    // when the pooled value is positive, zeros elsewhere.  The loads of chunk
+    // c+1 are issued before the MFMAs of chunk c and written to the other stage
+    // after them.  Window cells outside the gradient plane (padding, the
+    // up-sampling gaps) are zeroed once and never written again.
+    constexpr int kRP = 4;  // regions a thread owns per chunk (the plan keeps KC to that)
+    constexpr int NRP = PB ? kRP : 1;
+    T rd[NRP], rpv[NRP];
+    int ra[NRP];
+    int ys_lo = 0, ys_hi = -1, py_lo = 0, npx = 1, nw = 0;
+    if (PB) {
+        // gradient rows the window holds: ys*up - ybase in [0, rows_need)
+        const int last = ybase + rows_need - 1;
+        ys_lo = (max(ybase, 0) + a.up - 1) / a.up;
+        ys_hi = last < 0 ? -1 : min(last / a.up, a.Sh - 1);
+        if (ys_hi >= ys_lo) {
+            py_lo = div_magic(ys_lo, a.pool.magic_ps);
+            npx = div_magic(a.Sw + a.pool.PS - 1, a.pool.magic_ps);
+            nw = (div_magic(ys_hi, a.pool.magic_ps) - py_lo + 1) * npx;
+        }
+    }
+    const int nreg = a.KC * nw;
+    const int nreg_it = (nreg + kThreads - 1) / kThreads;  // iterations with owners (block-uniform)
+    const float rcp_nw = 1.0f / (float)max(nw, 1), rcp_npx = 1.0f / (float)npx;
+    auto region = [&](int e, int &c, int &py, int &px) {
+        c = div_small(e, max(nw, 1), rcp_nw);
+        const int w = e - c * nw;
+        const int wy = div_small(w, npx, rcp_npx);
+        py = py_lo + wy;
+        px = w - wy * npx;
+    };
+    auto rload = [&](int cn) {
+#pragma unroll
+        for (int i = 0; i < NRP; ++i) {
+            if (i >= nreg_it) break;
+            int c, py, px;
+            region(tid + kThreads * i, c, py, px);
+            const size_t o = (((size_t)n * a.Cs + min(cn + c, a.Cs - 1)) * a.pool.Hp +
+                              min(py, a.pool.Hp - 1)) * a.pool.Wp + min(px, a.pool.Wp - 1);
+            rd[i] = reinterpret_cast<const T *>(a.pool.dpool)[o];
+            ra[i] = a.pool.argmax[o];
+            rpv[i] = reinterpret_cast<const T *>(a.pool.pooled)[o];
+        }
+    };
+    auto rstore = [&](int cn, T *win) {
+        const int Qs = a.Sh * a.Sw;
+#pragma unroll
+        for (int i = 0; i < NRP; ++i) {
+            if (i >= nreg_it) break;
+            const int e = tid + kThreads * i;
+            int c, py, px;
+            region(e, c, py, px);
+            if (e >= nreg) continue;
+            const int cg = cn + c;
+            const bool ok = cg < a.Cs && py < a.pool.Hp && px < a.pool.Wp && rpv[i] > T(0);
+            const int tgt = ok ? ra[i] - cg * Qs : -1;
+            T *wc = win + c * CHn;
+            for (int dy = 0; dy < a.pool.PS; ++dy) {
+                const int ys = py * a.pool.PS + dy;
+                if (ys < ys_lo || ys > ys_hi) continue;
+                const int t = ys * a.up - ybase;
+                for (int dx = 0; dx < a.pool.PS; ++dx) {
+                    const int xs = px * a.pool.PS + dx, x = xs * a.up + a.Pw;
+                    if (xs < a.Sw && x < a.Wpad) wc[t * a.Wpad + x] = ys * a.Sw + xs == tgt ? rd[i] : T(0);
+                }
+            }
+        }
+    };
+    if (PB) {
+        for (int e = tid; e < a.KC * CHn; e += kThreads) {
+            stage_src(0)[e] = T(0);
+            stage_src(1)[e] = T(0);
+        }
+        __syncthreads();
+        rload(0);
+    }
     issue(0, 0);
+    if (PB) rstore(0, stage_src(0));
     wait_dma();
     __syncthreads();
     int st = 0;
@@ -533,7 +639,10 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
                 if (!(s_msk[e] > T(0))) w[e] = T(0);
             __syncthreads();
         }
-        if (c0 + a.KC < a.Cs) issue(st ^ 1, c0 + a.KC);
+        if (c0 + a.KC < a.Cs) {
+            issue(st ^ 1, c0 + a.KC);
+            if (PB) rload(c0 + a.KC);
+        }
 
         const T *s_src = stage_src(st);
         const int mrow = KS ? 0 : wm * 32;
@@ -624,6 +733,8 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
             }
             if (kk < a.KCK) mma4(fa[0], fb[0]);
         }
+        // the next chunk's gradient window, into the stage no wave reads now
+        if (PB && c0 + a.KC < a.Cs) rstore(c0 + a.KC, stage_src(st ^ 1));
         wait_dma();
         __syncthreads();
         st ^= 1;
@@ -794,7 +905,7 @@ constexpr size_t kSmallLds = 32 * 1024;
 // WF: the filter width when it is 3 or 5 (taps fully unrolled), else 0 (any
 // width up to kSmallMaxWf).  MM: 1 when M = 1, else 4 (filter rows past M are
 // staged as zeros, so no row test is needed).
-template <typename T, bool BWD, int WF, int MM>
+template <typename T, bool BWD, int WF, int MM, bool PB = false>
 __global__ __launch_bounds__(kSmallPix * kSmallWaves) void conv_small_m_kernel(IgemmArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -815,8 +926,9 @@ __global__ __launch_bounds__(kSmallPix * kSmallWaves) void conv_small_m_kernel(I
         lb = (qy - qy0) * a.S * a.Wpad + qx * a.S;
     }
     const size_t img = (size_t)a.Cs * a.Sh * a.Sw;
-    const T *src = reinterpret_cast<const T *>(a.src) + (size_t)n * img;
-    const T *msk = (BWD && a.mask) ? reinterpret_cast<const T *>(a.mask) + (size_t)n * img : nullptr;
+    const T *src = PB ? nullptr : reinterpret_cast<const T *>(a.src) + (size_t)n * img;
+    const T *msk = (BWD && !PB && a.mask) ? reinterpret_cast<const T *>(a.mask) + (size_t)n * img
+                                          : nullptr;
     const T *W = reinterpret_cast<const T *>(a.wgt);
     const int MW = MM * a.HfWf;
     const float rcp_ch = 1.0f / (float)CHn, rcp_wpad = 1.0f / (float)a.Wpad;
@@ -848,10 +960,17 @@ __global__ __launch_bounds__(kSmallPix * kSmallWaves) void conv_small_m_kernel(I
                 const int xs = div_small(max(xv, 0), a.up, rcp_up);
                 const bool in = yv >= 0 && xv >= 0 && ys * a.up == yv && xs * a.up == xv &&
                                 ys < a.Sh && xs < a.Sw;
-                const size_t o = in ? ((size_t)(c0 + c) * a.Sh + ys) * a.Sw + xs : 0;
                 ok[u] = in;
-                v[u] = src[o];
-                mv[u] = mskp[o];
+                if (PB) {
+                    // branch-free: a clamped cell, dropped by ok[u] when outside
+                    v[u] = pool_src_grad<T>(a.pool, n, a.Cs, c0 + c, a.Sh * a.Sw, a.Sw,
+                                            min(ys, a.Sh - 1), min(xs, a.Sw - 1));
+                    mv[u] = T(1);
+                } else {
+                    const size_t o = in ? ((size_t)(c0 + c) * a.Sh + ys) * a.Sw + xs : 0;
+                    v[u] = src[o];
+                    mv[u] = mskp[o];
+                }
             }
 #pragma unroll
             for (int u = 0; u < kSmallStage; ++u) {
@@ -1278,8 +1397,10 @@ bool make_plan(size_t tsz, int M, int Cs, int Qw, int Q, int Hf, int Wf, int S, 
 // per-block LDS share.  False when the problem needs the register-staged path
 // (very wide rows, very large filters, or tensors of 2 GiB and more, whose byte
 // offsets would reach the out-of-range marker).
-bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, int Wpad,
-                   size_t img_bytes, size_t w_bytes, Plan &p, DmaLayout &L)
+// pb_rpc (pooled source): the most pool regions one channel of a staged window
+// meets; a chunk's regions must fit the owners' registers (kRP a thread).
+bool make_dma_plan(size_t tsz, bool bwd, int pb_rpc, int M, int Cs, int HfWf, int rows_max,
+                   int Wpad, size_t img_bytes, size_t w_bytes, Plan &p, DmaLayout &L)
 {
     const int max_a = dma_a_max(p.NB), rows_a = dma_a_rows(M);
     if (img_bytes >= 0x80000000ull || w_bytes >= 0x80000000ull) return false;
@@ -1299,12 +1420,14 @@ bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, 
         const long long nia = vec ? ((long long)rows_a * sa / 2 + kWave - 1) / kWave
                                   : ((long long)rows_a * sa * dpe + kWave - 1) / kWave;
         if ((nis + 3) / 4 > kMaxDmaS || (nia + 3) / 4 > max_a) continue;
+        if (pb_rpc && kc * pb_rpc > kThreads * 4) continue;
         DmaLayout l;
         l.src_bytes = (int)nis * 256;
         l.a_bytes = (int)nia * (vec ? 1024 : 256) + 256;  // + slack read by the last step's prefetch
         l.a_vec = vec;
         l.stage_bytes = l.src_bytes + l.a_bytes;
-        const size_t total = 2 * (size_t)l.stage_bytes + (bwd ? (size_t)l.src_bytes : 0);
+        // + the mask window of the backward pass (not with a pooled source)
+        const size_t total = 2 * (size_t)l.stage_bytes + (bwd && !pb_rpc ? (size_t)l.src_bytes : 0);
         // fp32 kernels fit three blocks per CU in registers; keep LDS to a third
         if (total > (tsz == 4 ? kLdsPerBlock32 : kLdsPerBlock)) continue;
         Plan q = p;
@@ -1330,13 +1453,17 @@ bool make_dma_plan(size_t tsz, bool bwd, int M, int Cs, int HfWf, int rows_max, 
     return true;
 }
 
-template <typename T, int NB, bool BWD, bool KS, bool POOL, int K4 = 0>
+template <typename T, int NB, bool BWD, bool KS, bool POOL, int K4 = 0, bool PB = false>
 hipError_t launch_dma_ks(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                          int nimg, int zero_skip, hipStream_t s)
 {
     dim3 grid(nimg * p.tiles_per_img, p.m_tiles), block(kThreads);
     hipError_t e;
-    if (zero_skip) {
+    if (PB) {  // the pooled source has no zero-skip form
+        auto k = conv_igemm_dma_kernel<T, NB, BWD, false, KS, POOL, K4, true>;
+        if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
+    } else if (zero_skip) {
         auto k = conv_igemm_dma_kernel<T, NB, BWD, true, KS, POOL, K4>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a, L, w_bytes);
@@ -1348,18 +1475,21 @@ hipError_t launch_dma_ks(const IgemmArgs &a, const Plan &p, const DmaLayout &L, 
     return hipGetLastError();
 }
 
-template <typename T, int NB, bool BWD, bool POOL>
+template <typename T, int NB, bool BWD, bool POOL, bool PB = false>
 hipError_t launch_dma_k4(const IgemmArgs &a, const Plan &p, const DmaLayout &L, unsigned w_bytes,
                          int nimg, int zero_skip, hipStream_t s)
 {
     if constexpr (NB == 1) {
         if (a.k4 == 4)
-            return launch_dma_ks<T, NB, BWD, false, POOL, 4>(a, p, L, w_bytes, nimg, zero_skip, s);
+            return launch_dma_ks<T, NB, BWD, false, POOL, 4, PB>(a, p, L, w_bytes, nimg, zero_skip,
+                                                                 s);
         if (a.k4 == 2)
-            return launch_dma_ks<T, NB, BWD, false, POOL, 2>(a, p, L, w_bytes, nimg, zero_skip, s);
+            return launch_dma_ks<T, NB, BWD, false, POOL, 2, PB>(a, p, L, w_bytes, nimg, zero_skip,
+                                                                 s);
     }
-    if (a.ksplit) return launch_dma_ks<T, NB, BWD, true, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
-    return launch_dma_ks<T, NB, BWD, false, POOL>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (a.ksplit)
+        return launch_dma_ks<T, NB, BWD, true, POOL, 0, PB>(a, p, L, w_bytes, nimg, zero_skip, s);
+    return launch_dma_ks<T, NB, BWD, false, POOL, 0, PB>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
 
 template <typename T, int NB, bool BWD>
@@ -1368,6 +1498,7 @@ hipError_t launch_dma(const IgemmArgs &a, const Plan &p, const DmaLayout &L, uns
 {
     if (!BWD && a.pool_out)
         return launch_dma_k4<T, NB, false, true>(a, p, L, w_bytes, nimg, zero_skip, s);
+    if (BWD && a.pb) return launch_dma_k4<T, NB, true, false, true>(a, p, L, w_bytes, nimg, 0, s);
     return launch_dma_k4<T, NB, BWD, false>(a, p, L, w_bytes, nimg, zero_skip, s);
 }
 
@@ -1379,6 +1510,12 @@ hipError_t launch_nb(const IgemmArgs &a, const Plan &p, int nimg, int zero_skip,
     if (!BWD && a.csr) {
         auto k = zero_skip ? conv_igemm_kernel<T, NB, false, true, true>
                            : conv_igemm_kernel<T, NB, false, false, true>;
+        if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
+        return hipGetLastError();
+    }
+    if (BWD && a.pb) {
+        auto k = conv_igemm_kernel<T, NB, true, false, false, true>;
         if ((e = allow_dynamic_lds(k, p.lds)) != hipSuccess) return e;
         hipLaunchKernelGGL(k, grid, block, p.lds, s, a);
         return hipGetLastError();
@@ -1457,6 +1594,8 @@ struct ConvGeo {
     bool pool;
     int PS;
     int csr, nbanks, require_dma, zero_skip;
+    int pb;            // backward from a pooled source
+    int pb_ps, pb_up;  // its pool stride; the stride up-sampling the gradient
 };
 
 // The kernel family a launch takes and its tiling.
@@ -1509,8 +1648,15 @@ hipError_t choose_conv(size_t tsz, bool bwd, const ConvGeo &g, ConvChoice &c)
     const size_t w_bytes = (size_t)g.M * g.Cs * HfWf * tsz;
     if (g.csr) c.p.pipelined = 0;  // sparse staging is the direct path only
     c.pd = c.p;
-    if (!g.csr && make_dma_plan(tsz, bwd, g.M, g.Cs, HfWf, c.p.CH / c.p.Wpad, c.p.Wpad,
-                                img_bytes, w_bytes, c.pd, c.L)) {
+    // pooled source: the pool regions one channel of a staged window can meet
+    // (its rows hold at most dr gradient rows)
+    int pb_rpc = 0;
+    if (bwd && g.pb) {
+        const int dr = (c.p.CH / c.p.Wpad - 1) / g.pb_up + 1;
+        pb_rpc = ((dr - 1) / g.pb_ps + 2) * ((g.Sw + g.pb_ps - 1) / g.pb_ps);
+    }
+    if (!g.csr && make_dma_plan(tsz, bwd, pb_rpc, g.M, g.Cs, HfWf, c.p.CH / c.p.Wpad,
+                                c.p.Wpad, img_bytes, w_bytes, c.pd, c.L)) {
         c.kernel = kConvDma;
         // The smallest tiles (NB = 1: small layers with few blocks) split the
         // k-steps four ways so every wave has 4 or 8 independent MFMAs per step,
@@ -1552,7 +1698,7 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
     a.HfWf = a.Hf * a.Wf;
     const bool pool = !BWD && a.pool_out;
     ConvGeo g = {M, Cs, a.Sh, a.Sw, Qh, Qw, a.Hf, a.Wf, a.S, nimg, pool, a.PS, a.csr,
-                 a.nbanks, a.require_dma, zero_skip};
+                 a.nbanks, a.require_dma, zero_skip, a.pb, a.pool.PS, a.up};
     ConvChoice c;
     const hipError_t ce = choose_conv(sizeof(T), BWD, g, c);
     if (ce != hipSuccess) return ce;
@@ -1560,14 +1706,20 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
         a.KC = c.small_kc;
         a.CH = c.small_CH;
         a.Wpad = c.small_Wpad;
-        auto pick = [&](auto mm) {
+        auto pick = [&](auto mm, auto pbc) {
             constexpr int MM = decltype(mm)::value;
-            return a.Wf == 3 ? conv_small_m_kernel<T, BWD, 3, MM>
-                             : (a.Wf == 5 ? conv_small_m_kernel<T, BWD, 5, MM>
-                                          : conv_small_m_kernel<T, BWD, 0, MM>);
+            constexpr bool PBV = decltype(pbc)::value;
+            return a.Wf == 3 ? conv_small_m_kernel<T, BWD, 3, MM, PBV>
+                             : (a.Wf == 5 ? conv_small_m_kernel<T, BWD, 5, MM, PBV>
+                                          : conv_small_m_kernel<T, BWD, 0, MM, PBV>);
         };
-        auto k = M == 1 ? pick(std::integral_constant<int, 1>())
-                        : pick(std::integral_constant<int, kSmallM>());
+        auto pick_pb = [&](auto mm) {
+            if constexpr (BWD)
+                if (a.pb) return pick(mm, std::true_type());
+            return pick(mm, std::false_type());
+        };
+        auto k = M == 1 ? pick_pb(std::integral_constant<int, 1>())
+                        : pick_pb(std::integral_constant<int, kSmallM>());
         hipError_t e = allow_dynamic_lds(k, c.lds);
         if (e != hipSuccess) return e;
         dim3 grid((a.Q + kSmallPix - 1) / kSmallPix, nimg);
@@ -1645,9 +1797,9 @@ hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
     // backward_data is the same GEMM over the up-sampled gradient: M = C rows,
     // F source channels of Hout x Wout, Hin x Win output pixels, stride 1
     const ConvGeo g = bwd ? ConvGeo{d.C, d.F, d.Hout, d.Wout, d.Hin, d.Win, d.Hf, d.Wf, 1, d.N,
-                                    false, 0, 0, 0, 0, zero_skip}
+                                    false, 0, 0, 0, 0, zero_skip, 0, 0, 1}
                           : ConvGeo{d.F, d.C, d.Hin, d.Win, d.Hout, d.Wout, d.Hf, d.Wf, d.stride,
-                                    d.N, false, 0, 0, 0, 0, zero_skip};
+                                    d.N, false, 0, 0, 0, 0, zero_skip, 0, 0, 1};
     ConvChoice c;
     const hipError_t e = choose_conv(tsz, bwd, g, c);
     if (e != hipSuccess) return e;
@@ -1848,11 +2000,18 @@ hipError_t launch_conv_forward_csr(int dtype, const int32_t *rowptr, const int32
 
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
                                      const void *out_fwd, void *dX, const ConvDims &d,
-                                     int zero_skip, hipStream_t s)
+                                     int zero_skip, hipStream_t s, const PoolSrc *pool)
 {
     IgemmArgs a = {};
     a.src = dout;
     a.mask = out_fwd;
+    if (pool) {
+        a.pb = 1;
+        a.pool = *pool;
+        a.src = pool->dpool;
+        a.mask = nullptr;
+        zero_skip = 0;
+    }
     a.wgt = W;
     a.bias = nullptr;
     a.out = dX;

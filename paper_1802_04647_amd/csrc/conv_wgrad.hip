@@ -24,6 +24,11 @@
 // (4 pixels x 16 columns of X) is entirely zero, by a wavefront ballot, is not
 // issued.  Its product is exactly zero, so the result is bitwise that of the
 // dense kernel up to the sign of zero results.
+//
+// Pooled source (the PB instantiations; paper, Section "Future Work": vertical
+// fusion): the conv was followed by relu and a non-overlapping max-pool, and g
+// is built while staging from that pool's upstream gradient, argmax and pooled
+// values (pool_src_grad), so the routed gradient is never stored.
 #include <algorithm>
 
 #include "common.hpp"
@@ -43,6 +48,7 @@ constexpr size_t kLdsPerCU = 160 * 1024;
 constexpr int kMinTiles = 2;  // fewest pixel tiles a split reduces
 constexpr int kMG = 14;  // g-tile elements each thread stages per pixel tile
 constexpr int kMX = 16;  // X-window elements each thread stages per pixel tile
+constexpr int kMGP = 8;  // pooled source: pool windows each thread stages per pixel tile
 
 struct WgradArgs {
     const void *X, *dout, *mask;
@@ -54,9 +60,10 @@ struct WgradArgs {
     int rows_max;
     int spr;        // 0: tiles are runs of whole output rows; else slices per output row
     unsigned long long magic_rq, magic_wpad, magic_ch, magic_wout, magic_hwf, magic_wf;
+    PoolSrc pool;   // PB kernels: g comes from a following max-pool's backward
 };
 
-template <typename T, int NBW, bool ZSKIP>
+template <typename T, int NBW, bool ZSKIP, bool PB>
 __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
@@ -106,6 +113,10 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     // output row when rows are wider than a tile (spr > 0).
     struct TileGeo {
         int n, q0, qend, qy0, ow0, rows_need, ybase, xbase;
+        // pooled source: the tile's cells lie in the stride regions (PS x PS
+        // cells, region (py, px) holding window (py, px) in its corner) of
+        // pool rows py_lo .. and columns px_lo .., npx a row, nw in all
+        int py_lo, px_lo, npx, nw;
     };
     auto geo = [&](long long tt) {
         TileGeo g;
@@ -127,6 +138,16 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
         }
         g.ybase = g.qy0 * a.S - a.P;
         g.xbase = g.ow0 * a.S - a.P;
+        if (PB) {
+            const int len = g.qend - g.q0;
+            const int rows = a.spr ? 1 : div_magic(g.qend - 1 - g.qy0 * a.Wout, a.magic_wout) + 1;
+            g.py_lo = div_magic(g.qy0, a.pool.magic_ps);
+            const int py_hi = div_magic(g.qy0 + rows - 1, a.pool.magic_ps);
+            g.px_lo = div_magic(g.ow0, a.pool.magic_ps);
+            const int px_hi = div_magic(a.spr ? g.ow0 + len - 1 : a.Wout - 1, a.pool.magic_ps);
+            g.npx = px_hi - g.px_lo + 1;
+            g.nw = (py_hi - g.py_lo + 1) * g.npx;
+        }
         return g;
     };
 
@@ -134,10 +155,38 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     // registers before the MFMA loop of tile tt and written to LDS after it.
     const int tot_g = kBM * a.RQ;
     const int tot_x = nch * a.CH;  // channels x rows_max x Wpad (rows past rows_need are 0)
-    T vg[kMG], vm[kMG], vx[kMX];
+    constexpr int NG = PB ? 1 : kMG, NP = PB ? kMGP : 1;
+    T vg[NG], vm[NG], vx[kMX];
+    T pd[NP], pp[NP];  // pooled source: each owned window's gradient and pooled value
+    int pa[NP];        // and argmax
+    // Pooled source: element e of a tile is (filter row r, stride region w).
+    auto region = [&](const TileGeo &g, int e, int &r, int &py, int &px) {
+        r = div_small(e, g.nw, 1.0f / (float)g.nw);
+        const int w = e - r * g.nw;
+        const int wy = div_small(w, g.npx, 1.0f / (float)g.npx);
+        py = g.py_lo + wy;
+        px = g.px_lo + (w - wy * g.npx);
+    };
     auto load = [&](const TileGeo &g) {
         const int tid = opaque(threadIdx.x);
         const size_t gbase = ((size_t)g.n * a.F + ft * kBM) * a.Q;
+        if constexpr (PB) {
+            // one window's three values per element (clamped: always a valid
+            // address, so the loads issue together)
+            const int nit = (kBM * g.nw + kThreads - 1) / kThreads;  // tile-uniform
+#pragma unroll
+            for (int it = 0; it < kMGP; ++it) {
+                if (it >= nit) break;
+                int r, py, px;
+                region(g, tid + kThreads * it, r, py, px);
+                const int f = min(ft * kBM + r, a.F - 1);
+                const size_t o = ((size_t)g.n * a.F + f) * a.pool.Hp * a.pool.Wp +
+                                 (size_t)min(py, a.pool.Hp - 1) * a.pool.Wp + min(px, a.pool.Wp - 1);
+                pd[it] = reinterpret_cast<const T *>(a.pool.dpool)[o];
+                pa[it] = a.pool.argmax[o];
+                pp[it] = reinterpret_cast<const T *>(a.pool.pooled)[o];
+            }
+        } else {
 #pragma unroll
         for (int it = 0; it < kMG; ++it) {
             const int e = tid + kThreads * it;
@@ -153,6 +202,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             }
             vg[it] = v;
             vm[it] = mv;
+        }
         }
 #pragma unroll
         for (int it = 0; it < kMX; ++it) {
@@ -170,6 +220,40 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     };
     auto store = [&](const TileGeo &g) {
         const int tid = opaque(threadIdx.x);
+        if constexpr (PB) {
+            // Each element writes its region's cells that lie in the tile: the
+            // window's gradient at its argmax when the pooled value is positive,
+            // zeros elsewhere (every cell of the tile is in one region).
+            const int len = g.qend - g.q0;
+            const int nit = (kBM * g.nw + kThreads - 1) / kThreads;  // tile-uniform
+#pragma unroll
+            for (int it = 0; it < kMGP; ++it) {
+                if (it >= nit) break;
+                const int e = tid + kThreads * it;
+                int r, py, px;
+                region(g, e, r, py, px);
+                if (e >= kBM * g.nw) continue;
+                const int f = ft * kBM + r;
+                const bool win = f < a.F && py < a.pool.Hp && px < a.pool.Wp && pp[it] > T(0);
+                const int tgt = win ? pa[it] - f * a.Q : -1;
+                T *row = s_g + r * a.SG - g.q0;
+                for (int dy = 0; dy < a.pool.PS; ++dy) {
+                    const int oy = py * a.pool.PS + dy;
+                    for (int dx = 0; dx < a.pool.PS; ++dx) {
+                        const int ox = px * a.pool.PS + dx;
+                        const int q = oy * a.Wout + ox;
+                        if (oy < a.Hout && ox < a.Wout && q >= g.q0 && q < g.qend)
+                            row[q] = q == tgt ? pd[it] : T(0);
+                    }
+                }
+            }
+            // columns past a short tile's end stay zero
+            const int tail = a.RQ - len;
+            for (int e = tid; e < kBM * tail; e += kThreads) {
+                const int r = div_small(e, tail, 1.0f / (float)tail);
+                s_g[r * a.SG + len + (e - r * tail)] = T(0);
+            }
+        } else {
 #pragma unroll
         for (int it = 0; it < kMG; ++it) {
             const int e = tid + kThreads * it;
@@ -177,6 +261,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
                 const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
                 s_g[r * a.SG + u] = (vm[it] > T(0)) ? vg[it] : T(0);
             }
+        }
         }
 #pragma unroll
         for (int it = 0; it < kMX; ++it) {
@@ -193,8 +278,13 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
                 int q = g.q0 + u;
                 T v = T(0);
                 if (fg < a.F && q < g.qend) {
-                    v = dout[goff + q];
-                    if (mask && !(mask[goff + q] > T(0))) v = T(0);
+                    if (PB) {
+                        const int oy = q / a.Wout;
+                        v = pool_src_grad<T>(a.pool, g.n, a.F, fg, a.Q, a.Wout, oy, q - oy * a.Wout);
+                    } else {
+                        v = dout[goff + q];
+                        if (mask && !(mask[goff + q] > T(0))) v = T(0);
+                    }
                 }
                 s_g[r * a.SG + u] = v;
             }
@@ -362,8 +452,9 @@ constexpr int kRingThreads = 768;
 constexpr int kRingWaves = kRingThreads / kWave;
 constexpr int kRG = 5;  // g-tile elements each thread stages per tile
 constexpr int kRX = 5;  // new X-row elements each thread stages per tile
+constexpr int kRGP = 5; // pooled source: pool windows each thread stages per tile (64 x 60 / 768)
 
-template <typename T, int NBW, bool ZSKIP>
+template <typename T, int NBW, bool ZSKIP, bool PB>
 __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
@@ -406,12 +497,37 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         return T(0);
     };
 
-    T vg[kRG], vm[kRG], vx[kRX];
+    constexpr int NG = PB ? 1 : kRG, NP = PB ? kRGP : 1;
+    T vg[NG], vm[NG], vx[kRX];
+    // Pooled source: element e of a row is (filter row r, pool column px): the
+    // window's three values are loaded once and its PS cells of the row written
+    // from them (the gradient at the argmax, zeros elsewhere).
+    T pd[NP], pp[NP];
+    int pa[NP];
+    const int npx = PB ? div_magic(a.Wout + a.pool.PS - 1, a.pool.magic_ps) : 1;
+    const float rcp_npx = 1.0f / (float)npx;
+    const int nit_r = (kBM * npx + kRingThreads - 1) / kRingThreads;  // owner iterations
     auto load_g = [&](int n, int oh) {
         const int tid = opaque(threadIdx.x);
         const size_t gbase = ((size_t)n * a.F + ft * kBM) * a.Q + (size_t)oh * a.Wout;
+        if constexpr (PB) {
+            const int py = min(div_magic(oh, a.pool.magic_ps), a.pool.Hp - 1);
 #pragma unroll
-        for (int it = 0; it < kRG; ++it) {
+            for (int it = 0; it < kRGP; ++it) {
+                if (it >= nit_r) break;
+                const int e = tid + kRingThreads * it;
+                const int r = div_small(e, npx, rcp_npx), px = e - r * npx;
+                const int f = min(ft * kBM + r, a.F - 1);
+                const size_t o = (((size_t)n * a.F + f) * a.pool.Hp + py) * a.pool.Wp +
+                                 min(px, a.pool.Wp - 1);
+                pd[it] = reinterpret_cast<const T *>(a.pool.dpool)[o];
+                pa[it] = a.pool.argmax[o];
+                pp[it] = reinterpret_cast<const T *>(a.pool.pooled)[o];
+            }
+            return;
+        }
+#pragma unroll
+        for (int it = 0; it < NG; ++it) {
             const int e = tid + kRingThreads * it;
             T v = T(0), mv = T(1);
             if (e < kBM * a.RQ) {
@@ -426,10 +542,28 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             vm[it] = mv;
         }
     };
-    auto store_g = [&]() {
+    auto store_g = [&](int oh) {
         const int tid = opaque(threadIdx.x);
+        if constexpr (PB) {
+            const int py = div_magic(oh, a.pool.magic_ps);
 #pragma unroll
-        for (int it = 0; it < kRG; ++it) {
+            for (int it = 0; it < kRGP; ++it) {
+                if (it >= nit_r) break;
+                const int e = tid + kRingThreads * it;
+                const int r = div_small(e, npx, rcp_npx), px = e - r * npx;
+                if (e >= kBM * npx) continue;
+                const int f = ft * kBM + r;
+                const bool win = f < a.F && py < a.pool.Hp && px < a.pool.Wp && pp[it] > T(0);
+                const int tgt = win ? pa[it] - f * a.Q - oh * a.Wout : -1;
+                for (int dx = 0; dx < a.pool.PS; ++dx) {
+                    const int ox = px * a.pool.PS + dx;
+                    if (ox < a.Wout) s_g[r * a.SG + ox] = ox == tgt ? pd[it] : T(0);
+                }
+            }
+            return;
+        }
+#pragma unroll
+        for (int it = 0; it < NG; ++it) {
             const int e = tid + kRingThreads * it;
             if (e < kBM * a.RQ) {
                 const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
@@ -491,7 +625,15 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     if (t_begin < t_end) {
         const int n0 = (int)(t_begin / a.Hout), oh0 = (int)(t_begin - (long long)n0 * a.Hout);
         load_g(n0, oh0);
-        store_g();
+        if (PB) {
+            // the g-tile columns past the row are never written by the windows
+            const int tail = a.RQ - a.Wout;
+            for (int e = tid; e < kBM * tail; e += kRingThreads) {
+                const int r = div_small(e, tail, 1.0f / (float)tail);
+                s_g[r * a.SG + a.Wout + (e - r * tail)] = T(0);
+            }
+        }
+        store_g(oh0);
         stage_x_full(n0, oh0);
         __syncthreads();
         if (t_begin + 1 < t_end) {
@@ -549,7 +691,7 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
 
         if (tt + 1 < t_end) {
             __syncthreads();
-            store_g();
+            store_g(oh1);
             if (oh1 != 0)
                 store_x(oh1);
             else
@@ -727,12 +869,12 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     return true;
 }
 
-template <typename T, bool ZSKIP>
+template <typename T, bool ZSKIP, bool PB>
 hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP>
-                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP>
-                                      : conv_wgrad_ring_kernel<T, 1, ZSKIP>);
+    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP, PB>
+                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP, PB>
+                                      : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
@@ -751,12 +893,12 @@ hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStrea
     return hipGetLastError();
 }
 
-template <typename T, bool ZSKIP>
+template <typename T, bool ZSKIP, bool PB>
 hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3, ZSKIP>
-                        : (p.NBW == 2 ? conv_wgrad_kernel<T, 2, ZSKIP>
-                                      : conv_wgrad_kernel<T, 1, ZSKIP>);
+    auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3, ZSKIP, PB>
+                        : (p.NBW == 2 ? conv_wgrad_kernel<T, 2, ZSKIP, PB>
+                                      : conv_wgrad_kernel<T, 1, ZSKIP, PB>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     // One resident round: as many splits as the device holds blocks at once (a
@@ -780,6 +922,35 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
                        reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
                        reinterpret_cast<T *>(db), FK, a.F, a.splits);
     return hipGetLastError();
+}
+
+// Most stride regions of a pool (PS x PS cells holding one window each) that
+// one pixel tile of the plan meets: the tiled kernel's pooled-source staging
+// holds kMGP of them per thread.
+int max_regions(const WPlan &p, const ConvDims &d, int PS)
+{
+    int best = 0;
+    for (int qt = 0; qt < p.tiles_per_img; ++qt) {
+        int qy0, rows, ox0, ox1;
+        if (p.spr) {
+            const int oh = qt / p.spr, ow0 = (qt - oh * p.spr) * p.RQ;
+            const int len = p.RQ < d.Wout - ow0 ? p.RQ : d.Wout - ow0;
+            qy0 = oh;
+            rows = 1;
+            ox0 = ow0;
+            ox1 = ow0 + len - 1;
+        } else {
+            const int Q = d.Hout * d.Wout, q0 = qt * p.RQ;
+            const int qend = q0 + p.RQ < Q ? q0 + p.RQ : Q;
+            qy0 = q0 / d.Wout;
+            rows = (qend - 1) / d.Wout - qy0 + 1;
+            ox0 = 0;
+            ox1 = d.Wout - 1;
+        }
+        const int nw = ((qy0 + rows - 1) / PS - qy0 / PS + 1) * (ox1 / PS - ox0 / PS + 1);
+        best = nw > best ? nw : best;
+    }
+    return best;
 }
 
 // The plan a backward_filter call takes: the row ring when the layer suits it,
@@ -829,7 +1000,7 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info)
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
                                        const void *out_fwd, void *dW, void *db,
                                        const ConvDims &d, void *ws, int zero_skip,
-                                       hipStream_t s)
+                                       hipStream_t s, const PoolSrc *pool)
 {
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
     WPlan p;
@@ -872,20 +1043,37 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.magic_wout = host_magic(d.Wout);
     a.magic_hwf = host_magic(a.HfWf);
     a.magic_wf = host_magic(d.Wf);
+    if (pool) {
+        // the pooled source has no zero-skip form (its routed gradient has no
+        // all-zero fragments: one cell per window holds a value)
+        a.pool = *pool;
+        a.mask = nullptr;
+        // the tiled kernel's register staging holds kMGP windows a thread; more
+        // take the direct staging path (one cell at a time)
+        if (!ring && kBM * max_regions(p, d, pool->PS) > kThreads * kMGP) a.pipelined = 0;
+        a.magic_ch = ring ? host_magic((d.stride < d.Hf ? d.stride : d.Hf) * p.Wpad)
+                          : host_magic(p.CH);
+        if (ring)
+            return dtype == 0 ? launch_ring<double, false, true>(a, p, dW, db, s)
+                              : launch_ring<float, false, true>(a, p, dW, db, s);
+        return dtype == 0 ? launch_w<double, false, true>(a, p, dW, db, s)
+                          : launch_w<float, false, true>(a, p, dW, db, s);
+    }
     if (ring) {
         // the ring's new-row staging divides by the new rows' span per channel
         a.magic_ch = host_magic((d.stride < d.Hf ? d.stride : d.Hf) * p.Wpad);
         if (dtype == 0)
-            return zero_skip ? launch_ring<double, true>(a, p, dW, db, s)
-                             : launch_ring<double, false>(a, p, dW, db, s);
-        return zero_skip ? launch_ring<float, true>(a, p, dW, db, s)
-                         : launch_ring<float, false>(a, p, dW, db, s);
+            return zero_skip ? launch_ring<double, true, false>(a, p, dW, db, s)
+                             : launch_ring<double, false, false>(a, p, dW, db, s);
+        return zero_skip ? launch_ring<float, true, false>(a, p, dW, db, s)
+                         : launch_ring<float, false, false>(a, p, dW, db, s);
     }
     a.magic_ch = host_magic(p.CH);
     if (dtype == 0)
-        return zero_skip ? launch_w<double, true>(a, p, dW, db, s)
-                         : launch_w<double, false>(a, p, dW, db, s);
-    return zero_skip ? launch_w<float, true>(a, p, dW, db, s) : launch_w<float, false>(a, p, dW, db, s);
+        return zero_skip ? launch_w<double, true, false>(a, p, dW, db, s)
+                         : launch_w<double, false, false>(a, p, dW, db, s);
+    return zero_skip ? launch_w<float, true, false>(a, p, dW, db, s)
+                     : launch_w<float, false, false>(a, p, dW, db, s);
 }
 
 }  // namespace dmlnn

@@ -7,6 +7,8 @@
 
 namespace dmlnn {
 
+struct PoolSrc;  // common.hpp
+
 // ---------------------------------------------------------------- conv2d ----
 // Geometry of one conv2d call (already validated).
 struct ConvDims {
@@ -65,16 +67,18 @@ hipError_t launch_conv_forward_csr(int dtype, const int32_t *rowptr, const int32
                                    int zero_skip, hipStream_t s);
 hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
                                      const void *out_fwd, void *dX, const ConvDims &d,
-                                     int zero_skip, hipStream_t s);
+                                     int zero_skip, hipStream_t s, const PoolSrc *pool = nullptr);
 
 // Filter/bias gradient: split reduction into a workspace, then a fixed-order sum.
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d);
 // The backward_filter part of conv_plan_info.
 hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info);
+// pool (optional): dout is not given; g is built from a following max-pool's
+// backward (see PoolSrc in common.hpp).
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
                                        const void *out_fwd, void *dW, void *db,
                                        const ConvDims &d, void *ws, int zero_skip,
-                                       hipStream_t s);
+                                       hipStream_t s, const PoolSrc *pool = nullptr);
 
 // ----------------------------------------------------------------- others ----
 hipError_t launch_bias_add_relu(int dtype, const void *X, const void *b, void *out, int N, int C,

@@ -70,6 +70,9 @@ def load():
                                    + [_vp, ctypes.c_size_t, _vp]),
         "conv2d_backward_data": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
         "conv2d_backward_filter_noalloc": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
+        "conv2d_backward_filter_pooled": (_i, [_i] + [_vp] * 6 + [_i] * 13
+                                          + [_vp, ctypes.c_size_t, _vp]),
+        "conv2d_backward_data_pooled": (_i, [_i] + [_vp] * 5 + [_i] * 13 + [_vp]),
         "dmlnn_set_zero_skip": (_i, [_i]),
         "bias_add_relu": (_i, [_i, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
         "max_pool2d_fwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
@@ -259,6 +262,63 @@ def conv2d_backward_filter_noalloc(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride
         dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf, stride, pad,
         _stream()))
     return dW, db
+
+
+def _pool_out(Hout, Wout, pool_h, pool_w, pool_stride, pool_pad):
+    return (conv2d_out_dim(Hout, pool_h, pool_stride, pool_pad),
+            conv2d_out_dim(Wout, pool_w, pool_stride, pool_pad))
+
+
+def conv2d_backward_filter_pooled(X, dpool, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, F,
+                                  pool_h, pool_w, pool_stride, pool_pad, want_db=True,
+                                  workspace=None, dW=None, db=None):
+    """Filter and bias gradients of conv -> relu -> max-pool from the pool's
+    upstream gradient (dpool), argmax and pooled values.  Returns (dW, db)."""
+    dt = _dtype(X, dpool, pooled, dW, db)
+    N = X.shape[0]
+    need = conv2d_backward_filter_workspace_size(dt, N, C, Hin, Win, F, Hf, Wf, stride, pad)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=X.device)
+    if dW is None:
+        dW = _empty((F, C * Hf * Wf), X)
+    if db is None and want_db:
+        db = _empty((F,), X)
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    Hp, Wp = _pool_out(Hout, Wout, pool_h, pool_w, pool_stride, pool_pad)
+    _need(X, N * C * Hin * Win, "X")
+    for t, name in ((dpool, "dpool"), (argmax, "argmax"), (pooled, "pooled")):
+        _need(t, N * F * max(Hp, 0) * max(Wp, 0), name)
+    if argmax.dtype != torch.int32:
+        raise TypeError("argmax must be int32")
+    _need(dW, F * C * Hf * Wf, "dW")
+    _need(db, F, "db")
+    _check("conv2d_backward_filter_pooled", load().conv2d_backward_filter_pooled(
+        dt, _p(X), _p(dpool), _p(argmax), _p(pooled), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
+        stride, pad, pool_h, pool_w, pool_stride, pool_pad, _p(workspace),
+        workspace.numel() * workspace.element_size(), _stream()))
+    return dW, db
+
+
+def conv2d_backward_data_pooled(W, dpool, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad,
+                                pool_h, pool_w, pool_stride, pool_pad, dX=None):
+    """Input gradient of conv -> relu -> max-pool from the pool's upstream
+    gradient (dpool), argmax and pooled values: N x C*Hin*Win."""
+    dt = _dtype(W, dpool, pooled, dX)
+    N, F = dpool.shape[0], W.shape[0]
+    Hout, Wout = conv2d_out_dim(Hin, Hf, stride, pad), conv2d_out_dim(Win, Wf, stride, pad)
+    Hp, Wp = _pool_out(Hout, Wout, pool_h, pool_w, pool_stride, pool_pad)
+    if dX is None:
+        dX = _empty((N, C * Hin * Win), W)
+    _need(W, F * C * Hf * Wf, "W")
+    for t, name in ((dpool, "dpool"), (argmax, "argmax"), (pooled, "pooled")):
+        _need(t, N * F * max(Hp, 0) * max(Wp, 0), name)
+    if argmax.dtype != torch.int32:
+        raise TypeError("argmax must be int32")
+    _need(dX, N * C * Hin * Win, "dX")
+    _check("conv2d_backward_data_pooled", load().conv2d_backward_data_pooled(
+        dt, _p(W), _p(dpool), _p(argmax), _p(pooled), _p(dX), N, C, Hin, Win, F, Hf, Wf, stride,
+        pad, pool_h, pool_w, pool_stride, pool_pad, _stream()))
+    return dX
 
 
 def conv2d_backward_data(W, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, dX=None):

@@ -5,8 +5,10 @@ max-pool 2x2/2 -> affine 3136->512 + relu -> affine 512->10 -> softmax +
 cross-entropy; backward in reverse order; then v <- mu v - lr g and
 theta <- theta + v for the eight parameter tensors (paper, Section 2: the NN
 library's layers, its minibatch training loop and SGD with momentum).  Each
-conv+relu+pool runs as one fused call, and each pool backward carries the relu
-mask, so the conv outputs are never stored.
+conv+relu+pool runs as one fused call forward, and backward the conv passes
+take the pool's gradient, argmax and pooled values directly (the relu mask and
+the pool routing built while staging), so neither the conv outputs nor their
+gradients are ever stored.
 
 All activations, gradients and the backward-filter workspaces are allocated
 once; ``step`` only enqueues library calls (about twenty launches, one of them
@@ -26,8 +28,12 @@ PARAM_ORDER = ("W1", "b1", "W2", "b2", "W3", "b3", "W4", "b4")
 
 class LeNetTrainer:
     def __init__(self, params: dict, N: int = 64, lr: float = 0.01, mu: float = 0.9,
-                 dtype=torch.float64, device="cuda"):
+                 dtype=torch.float64, device="cuda", fused_pool_backward: bool = True):
         self.N, self.lr, self.mu = N, lr, mu
+        # False: the pool backward runs as its own kernel (max_pool2d_bwd_relu)
+        # into a stored conv-output gradient, which the plain conv backward
+        # calls read (kept to measure the fusion against)
+        self.fused_pool_backward = fused_pool_backward
         kw = dict(dtype=dtype, device=device)
         # Parameters, gradients and velocities each live in one flat buffer (the
         # tensors are contiguous views into it), so the optimizer update of all
@@ -54,8 +60,9 @@ class LeNetTrainer:
         self.p2, self.i2 = e(N, 64 * 49), i32(N, 64 * 49)
         self.h, self.s = e(N, 512), e(N, 10)
         self.loss, self.ds = e(1), e(N, 10)
-        self.dh, self.dp2, self.dc2 = e(N, 512), e(N, 3136), e(N, 64 * 196)
-        self.dp1, self.dc1 = e(N, 32 * 196), e(N, 32 * 784)
+        self.dh, self.dp2, self.dp1 = e(N, 512), e(N, 3136), e(N, 32 * 196)
+        if not fused_pool_backward:
+            self.dc2, self.dc1 = e(N, 64 * 196), e(N, 32 * 784)
         ws1 = dmlnn.conv2d_backward_filter_workspace_size(dtype, N, 1, 28, 28, 32, 5, 5, 1, 2)
         ws2 = dmlnn.conv2d_backward_filter_workspace_size(dtype, N, 32, 14, 14, 64, 5, 5, 1, 2)
         self.ws1 = torch.empty(ws1, dtype=torch.uint8, device=device)
@@ -86,19 +93,32 @@ class LeNetTrainer:
                              db=g["b3"])
         dmlnn.affine_bwd(self.dh, self.p2, p["W3"], self.h, dX=self.dp2, want_dW=False,
                          want_db=False)
-        dmlnn.max_pool2d_bwd_relu(self.dp2, self.i2, self.p2, 64, 14, 14, 2, 2, 2, 0,
-                                  dX=self.dc2)
-        if side is not main:
-            side.wait_stream(main)  # dc2 is ready
-        with torch.cuda.stream(side):
-            dmlnn.conv2d_backward_filter(self.p1, self.dc2, None, 32, 14, 14, 5, 5, 1, 2, 64,
-                                         workspace=self.ws2, dW=g["W2"], db=g["b2"])
-        dmlnn.conv2d_backward_data(p["W2"], self.dc2, None, 32, 14, 14, 5, 5, 1, 2,
-                                   dX=self.dp1)
-        dmlnn.max_pool2d_bwd_relu(self.dp1, self.i1, self.p1, 32, 28, 28, 2, 2, 2, 0,
-                                  dX=self.dc1)
-        dmlnn.conv2d_backward_filter(X, self.dc1, None, 1, 28, 28, 5, 5, 1, 2, 32,
-                                     workspace=self.ws1, dW=g["W1"], db=g["b1"])
+        if self.fused_pool_backward:
+            if side is not main:
+                side.wait_stream(main)  # dp2 is ready
+            with torch.cuda.stream(side):
+                dmlnn.conv2d_backward_filter_pooled(self.p1, self.dp2, self.i2, self.p2, 32, 14,
+                                                    14, 5, 5, 1, 2, 64, 2, 2, 2, 0,
+                                                    workspace=self.ws2, dW=g["W2"], db=g["b2"])
+            dmlnn.conv2d_backward_data_pooled(p["W2"], self.dp2, self.i2, self.p2, 32, 14, 14, 5,
+                                              5, 1, 2, 2, 2, 2, 0, dX=self.dp1)
+            dmlnn.conv2d_backward_filter_pooled(X, self.dp1, self.i1, self.p1, 1, 28, 28, 5, 5, 1,
+                                                2, 32, 2, 2, 2, 0, workspace=self.ws1,
+                                                dW=g["W1"], db=g["b1"])
+        else:
+            dmlnn.max_pool2d_bwd_relu(self.dp2, self.i2, self.p2, 64, 14, 14, 2, 2, 2, 0,
+                                      dX=self.dc2)
+            if side is not main:
+                side.wait_stream(main)  # dc2 is ready
+            with torch.cuda.stream(side):
+                dmlnn.conv2d_backward_filter(self.p1, self.dc2, None, 32, 14, 14, 5, 5, 1, 2, 64,
+                                             workspace=self.ws2, dW=g["W2"], db=g["b2"])
+            dmlnn.conv2d_backward_data(p["W2"], self.dc2, None, 32, 14, 14, 5, 5, 1, 2,
+                                       dX=self.dp1)
+            dmlnn.max_pool2d_bwd_relu(self.dp1, self.i1, self.p1, 32, 28, 28, 2, 2, 2, 0,
+                                      dX=self.dc1)
+            dmlnn.conv2d_backward_filter(X, self.dc1, None, 1, 28, 28, 5, 5, 1, 2, 32,
+                                         workspace=self.ws1, dW=g["W1"], db=g["b1"])
         # join: the optimizer reads the side stream's gradients, and the next
         # step's forward overwrites p1 and p2, which the side stream reads
         if side is not main:

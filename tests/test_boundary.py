@@ -178,3 +178,24 @@ def test_noalloc_backward_filter_validation(lib):
     assert f(0, FAKE, FAKE, None, None, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_NULL
     assert f(9, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_DTYPE
     assert f(0, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 0, 1, None) == ERR_ARG
+
+
+def test_pooled_backward_validation(lib):
+    bf, bd = lib.conv2d_backward_filter_pooled, lib.conv2d_backward_data_pooled
+    conv = (2, 3, 10, 10, 8, 3, 3, 1, 1)           # 10x10 conv output
+    need = lib.conv2d_backward_filter_workspace_size(0, *conv)
+    # overlapping windows (stride 2 < 3) and padded pools are refused
+    assert bd(0, FAKE, FAKE, FAKE, FAKE, FAKE, *conv, 3, 3, 2, 0, None) == ERR_ARG
+    assert "overlap" in dmlnn.last_error()
+    assert bd(0, FAKE, FAKE, FAKE, FAKE, FAKE, *conv, 2, 2, 2, 1, None) == ERR_ARG
+    assert bf(0, FAKE, FAKE, FAKE, FAKE, FAKE, None, *conv, 3, 3, 2, 0, FAKE, need,
+              None) == ERR_ARG
+    # missing pool inputs, workspace, bad dtype
+    assert bd(0, FAKE, FAKE, None, FAKE, FAKE, *conv, 2, 2, 2, 0, None) == ERR_NULL
+    assert bf(0, FAKE, FAKE, FAKE, None, FAKE, None, *conv, 2, 2, 2, 0, FAKE, need,
+              None) == ERR_NULL
+    assert bf(0, FAKE, FAKE, FAKE, FAKE, FAKE, None, *conv, 2, 2, 2, 0, FAKE, need - 1,
+              None) == ERR_WS
+    assert bd(6, FAKE, FAKE, FAKE, FAKE, FAKE, *conv, 2, 2, 2, 0, None) == ERR_DTYPE
+    # a window larger than the conv output
+    assert bd(0, FAKE, FAKE, FAKE, FAKE, FAKE, *conv, 11, 11, 11, 0, None) == ERR_ARG

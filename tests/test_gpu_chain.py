@@ -17,11 +17,14 @@ from paper_1802_04647_amd.lenet import PARAM_ORDER, LeNetTrainer
 pytestmark = pytest.mark.gpu
 
 
+@pytest.mark.parametrize("fused", [True, False], ids=["pool-backward-fused", "unfused"])
 @pytest.mark.parametrize("steps", [1, 3])
-def test_lenet_training_steps(steps):
-    print(f"\n[gpu] lenet training {steps} step(s)", flush=True)
+def test_lenet_training_steps(steps, fused):
+    """fused: the conv backward passes read the pool gradients directly;
+    unfused: the pool backward kernel stores the conv-output gradients first."""
+    print(f"\n[gpu] lenet training {steps} step(s), fused pool backward {fused}", flush=True)
     X, Y, params = lenet_train_inputs()
-    tr = LeNetTrainer(params)
+    tr = LeNetTrainer(params, fused_pool_backward=fused)
     Xd, Yd = dev(X, "f64"), dev(Y, "f64")
     p, v = params, lenet_oracle.zero_velocities(params)
     for _ in range(steps):

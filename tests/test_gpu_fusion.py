@@ -110,3 +110,53 @@ def test_conv_forward_multi(case, dt):
     for k, (W, b) in enumerate(zip(Ws, bs)):
         ref, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
         assert_close(host(outs[k]), ref, dt, f"bank {k}")
+
+
+# conv backward passes straight from a following max-pool's backward (the
+# routed gradient never stored): (conv shape, pool_h, pool_w, pool_stride)
+PB_CASES = [
+    (ConvShape(64, 32, 14, 14, 64, 5, 5, 1, 2), 2, 2, 2),   # LeNet conv2 (config 3)
+    (ConvShape(64, 1, 28, 28, 32, 5, 5, 1, 2), 2, 2, 2),    # LeNet conv1: small-M backward_data
+    (ConvShape(2, 40, 12, 12, 48, 3, 3, 1, 1), 2, 2, 2),    # row-ring backward_filter
+    (ConvShape(3, 6, 15, 13, 20, 3, 3, 1, 1), 3, 3, 3),     # windows leave trailing rows/cols
+    (ConvShape(2, 4, 10, 20, 24, 3, 3, 1, 1), 2, 3, 3),     # gaps between windows
+    (ConvShape(2, 12, 16, 16, 40, 3, 3, 2, 1), 2, 2, 2),    # conv stride 2: up-sampled source
+    (ConvShape(1, 6, 5, 500, 8, 3, 3, 1, 1), 2, 2, 2),      # wide rows: register-staged kernels
+    (ConvShape(2, 3, 9, 70, 10, 3, 3, 1, 1), 1, 1, 1),      # 1x1 pool; rows sliced in backward_filter
+]
+
+
+def _pooled_case(s, ph, pw, ps, dt, seed):
+    """Inputs, the oracle's forward (conv -> relu -> pool) and the pooled
+    gradient; the oracle's reference routes it with the relu mask folded in
+    (a routed cell holds the pooled value, so its mask is pooled > 0)."""
+    X0, W0, b0, _ = random_conv_case(seed, s, zero_frac=0.3)
+    X, W, b = (rounded(v, dt) for v in (X0, W0, b0))
+    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+    out, _, _ = oracle.conv2d_forward(X, W, b, *a, relu=True)
+    pooled, idx, Hp, Wp = oracle.max_pool2d_fwd(rounded(out, dt), s.F, s.Hout, s.Wout, ph, pw, ps, 0)
+    dpool = rounded(np.random.Generator(np.random.PCG64(seed + 5)).standard_normal(pooled.shape), dt)
+    g = oracle.max_pool2d_bwd(dpool * (pooled > 0), idx, s.F, s.Hout, s.Wout, ph, pw, ps, 0)
+    return X, W, a, pooled, idx, dpool, g
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("case", PB_CASES, ids=lambda c: f"{c[0]}-pool{c[1]}x{c[2]}s{c[3]}")
+def test_conv_backward_from_pool(case, dt):
+    s, ph, pw, ps = case
+    X, W, a, pooled, idx, dpool, g = _pooled_case(s, ph, pw, ps, dt, 53)
+    print(f"\n[gpu] conv backward from pool {s} pool {ph}x{pw}/{ps} {dt}", flush=True)
+    pd, idd, dpd = dev(pooled, dt), torch.from_numpy(idx).cuda(), dev(dpool, dt)
+    dW, db = dmlnn.conv2d_backward_filter_pooled(dev(X, dt), dpd, idd, pd, *a, s.F, ph, pw, ps, 0)
+    dX = dmlnn.conv2d_backward_data_pooled(dev(W, dt), dpd, idd, pd, *a, ph, pw, ps, 0)
+    # the unfused route on the GPU: pool backward with the mask, then the plain calls
+    dc = dmlnn.max_pool2d_bwd_relu(dpd, idd, pd, s.F, s.Hout, s.Wout, ph, pw, ps, 0)
+    uW, ub = dmlnn.conv2d_backward_filter(dev(X, dt), dc, None, *a, s.F)
+    uX = dmlnn.conv2d_backward_data(dev(W, dt), dc, None, *a)
+    torch.cuda.synchronize()
+    ref_dW, ref_db = oracle.conv2d_backward_filter(X, g, None, *a, s.F)
+    ref_dX = oracle.conv2d_backward_data(W, g, None, *a)
+    for got, unf, ref, what in ((dW, uW, ref_dW, "dW"), (db, ub, ref_db, "db"),
+                                (dX, uX, ref_dX, "dX")):
+        assert_close(host(got), ref, dt, what)
+        assert_close(host(unf), ref, dt, what + " (unfused)")

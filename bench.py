@@ -41,6 +41,11 @@ def parse():
                     help="only run the config 2 zero-skip measurement (for counter runs)")
     ap.add_argument("--only-f64", action="store_true",
                     help="skip the fp32, LeNet, other-config and other-kernel extras")
+    ap.add_argument("--only-f32", action="store_true",
+                    help="only time the fp32 mode of the ResNet-shaped layer (for counter runs)")
+    ap.add_argument("--only-aux", action="store_true",
+                    help="only time the bandwidth-bound ops and the copy calibration (for "
+                         "counter runs)")
     ap.add_argument("--only-lenet", action="store_true",
                     help="only time the LeNet training step (for kernel-trace runs)")
     ap.add_argument("--lenet-trace", choices=("fused", "unfused"),
@@ -586,6 +591,15 @@ def main():
 
     if args.zero_skip_probe:
         print(json.dumps({"zero_skip": zero_skip_timing()}), flush=True)
+        return
+    if args.only_f32:
+        r32 = conv_step_timing("f32", args.steps, args.warmup)
+        print(json.dumps({"f32_per_pass_ms": {k: round(v, 4) for k, v in
+                                              r32["per_pass_ms"].items()}}), flush=True)
+        return
+    if args.only_aux:
+        print(json.dumps({"aux_kernels": aux_kernel_timing(), "hbm_copy": copy_calibration()}),
+              flush=True)
         return
     if args.lenet_trace:
         print(json.dumps({"lenet_trace": lenet_trace(args.lenet_trace == "fused", args.steps,

@@ -4,10 +4,14 @@
 // Both are memory-bound streaming kernels over the row-major N x (C*H*W)
 // matrices.  Forward: one thread per output, window scanned row by row,
 // replacing the running maximum only on a strictly larger value (first maximum
-// wins ties; +0 and -0 compare equal).  Backward: one thread per INPUT cell
-// gathers the outputs whose window covers it and whose argmax is that cell, so
-// every dX element is written exactly once, without atomics and in a fixed
-// order.
+// wins ties; +0 and -0 compare equal).  Backward: windows that do not overlap
+// (stride >= window, no padding) are routed by one thread per stride region
+// (the stride x stride input cells holding one window in their corner): it
+// reads the window's gradient and argmax once and writes all of the region's
+// cells (the gradient at the argmax, zeros elsewhere).  Other windows: one
+// thread per INPUT cell gathers the outputs whose window covers it and whose
+// argmax is that cell.  Either way every dX element is written exactly once,
+// without atomics and in a fixed order.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -107,6 +111,51 @@ __global__ __launch_bounds__(256) void max_pool_bwd_kernel(const T *__restrict__
     }
 }
 
+// Disjoint windows: thread (plane, region ry, rx) of the Ry x Rx stride regions
+// (Ry = ceil(Hin / S)) writes the region's cells of dX.  VEC2 (S == 2 and an
+// even Win, so every plane and region row is 2-element aligned): a region row
+// is one 2-element vector store.
+template <typename T, bool VEC2>
+__global__ __launch_bounds__(256) void max_pool_bwd_regions_kernel(
+    const T *__restrict__ dout, const int32_t *__restrict__ argmax, const T *__restrict__ pooled,
+    T *__restrict__ dX, long long planes, int C, int Hin, int Win, int S, int Hout, int Wout,
+    int Ry, int Rx)
+{
+    typedef T T2 __attribute__((ext_vector_type(2)));
+    const int HW = Hin * Win, R = Ry * Rx;
+    for (long long pl = blockIdx.y; pl < planes; pl += gridDim.y) {
+        const int c = (int)(pl % C);
+        const T *dp = dout + (size_t)pl * Hout * Wout;
+        const int32_t *ap = argmax + (size_t)pl * Hout * Wout;
+        const T *pp = pooled ? pooled + (size_t)pl * Hout * Wout : nullptr;
+        T *dXp = dX + (size_t)pl * HW;
+        for (int idx = blockIdx.x * 256 + threadIdx.x; idx < R; idx += gridDim.x * 256) {
+            const int ry = idx / Rx, rx = idx - ry * Rx;
+            const bool win = ry < Hout && rx < Wout;
+            const int o = win ? ry * Wout + rx : 0;  // a valid address either way
+            const int32_t am = ap[o];
+            const T d = dp[o];
+            const T pv = pp ? pp[o] : T(1);
+            // in-plane index of the routed cell, or -1
+            const int tgt = (win && pv > T(0)) ? am - c * HW : -1;
+            for (int dy = 0; dy < S; ++dy) {
+                const int y = ry * S + dy;
+                if (y >= Hin) break;
+                const int q = y * Win + rx * S;
+                if (VEC2) {
+                    T2 v;
+                    v.x = q == tgt ? d : T(0);
+                    v.y = q + 1 == tgt ? d : T(0);
+                    *reinterpret_cast<T2 *>(dXp + q) = v;
+                } else {
+                    for (int dx = 0; dx < S && rx * S + dx < Win; ++dx)
+                        dXp[q + dx] = q + dx == tgt ? d : T(0);
+                }
+            }
+        }
+    }
+}
+
 int grid_for(long long total)
 {
     long long g = (total + 255) / 256;
@@ -140,6 +189,33 @@ hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argma
 {
     const long long planes = (long long)N * C;
     const int HW = Hin * Win;
+    if (stride >= Hf && stride >= Wf && pad == 0) {
+        // disjoint windows: one thread per stride region
+        const int Ry = (Hin + stride - 1) / stride, Rx = (Win + stride - 1) / stride;
+        const int R = Ry * Rx;
+        int gx = (R + 255) / 256;
+        if (gx > 8) gx = 8;
+        long long gy = planes;
+        const long long cap = 32768 / gx;
+        if (gy > cap) gy = cap;
+        const dim3 grid(gx, (unsigned)gy);
+        const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
+        const bool vec2 = stride == 2 && Win % 2 == 0 && (uintptr_t)dX % (2 * tsz) == 0;
+        if (dtype == 0) {
+            auto k = vec2 ? max_pool_bwd_regions_kernel<double, true>
+                          : max_pool_bwd_regions_kernel<double, false>;
+            hipLaunchKernelGGL(k, grid, dim3(256), 0, s, (const double *)dout, argmax,
+                               (const double *)pooled, (double *)dX, planes, C, Hin, Win, stride,
+                               Hout, Wout, Ry, Rx);
+        } else {
+            auto k = vec2 ? max_pool_bwd_regions_kernel<float, true>
+                          : max_pool_bwd_regions_kernel<float, false>;
+            hipLaunchKernelGGL(k, grid, dim3(256), 0, s, (const float *)dout, argmax,
+                               (const float *)pooled, (float *)dX, planes, C, Hin, Win, stride,
+                               Hout, Wout, Ry, Rx);
+        }
+        return hipGetLastError();
+    }
     // About 16k blocks in all, each thread walking several cells and planes:
     // tiny one-element blocks would leave the dispatcher as the bottleneck.
     int gx = (HW + 1023) / 1024;

@@ -20,7 +20,30 @@ POOLS = [  # (N, C, H, W, Hf, Wf, s, p)
     (1, 2, 9, 9, 3, 2, 3, 0),
     (1, 2, 10, 11, 3, 3, 3, 0),       # trailing rows/columns no window covers
     (2, 3, 8, 8, 2, 2, 3, 0),         # gaps between windows
+    (2, 3, 9, 9, 2, 2, 2, 0),         # odd width: scalar region stores, trailing row/col
+    (2, 2, 7, 8, 2, 2, 2, 0),         # even width, odd height: vector stores, trailing row
+    (1, 3, 4, 5, 1, 1, 1, 0),         # 1x1 windows at stride 1
 ]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_max_pool_bwd_into_misaligned_output(dt):
+    # an output one element past an aligned address: the 2-element vector
+    # stores of 2x2/2 windows must not be used there
+    N, C, H, W = 2, 3, 6, 8
+    g = rng(41)
+    X = rounded(g.standard_normal((N, C * H * W)), dt)
+    _, ref_idx, Ho, Wo = oracle.max_pool2d_fwd(X, C, H, W, 2, 2, 2, 0)
+    dout = rounded(g.standard_normal((N, C * Ho * Wo)), dt)
+    buf = torch.full((N * C * H * W + 1,), 7.0, dtype=dev(dout, dt).dtype, device="cuda")
+    dX = buf[1:]
+    assert dX.data_ptr() % 16 != 0
+    dmlnn.max_pool2d_bwd(dev(dout, dt), torch.from_numpy(ref_idx).cuda(), C, H, W, 2, 2, 2, 0,
+                         dX=dX)
+    torch.cuda.synchronize()
+    ref = oracle.max_pool2d_bwd(dout, ref_idx, C, H, W, 2, 2, 2, 0)
+    assert np.array_equal(host(dX).reshape(ref.shape), ref)
+    assert float(buf[0]) == 7.0
 
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])

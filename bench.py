@@ -353,46 +353,69 @@ def _reach_counts(H, Hf, S, P, Hout):
 
 
 def zero_skip_timing():
-    """Config 2 forward (LeNet conv1, ~80% i.i.d. zeros) and a structured-zero
-    supplement (the same draw with a 6-pixel zero border) with the zero-fragment
-    skip off and on: dense-equivalent GFLOP/s and the nnz-based algorithmic work
-    2*F*sum over non-zero inputs of the outputs each reaches."""
+    """The three conv passes with the zero-fragment skip off and on, on the
+    workloads of configs 2, 3 and 5 with their own zeros, plus a structured-zero
+    supplement (config 2's draw with a 6-pixel zero border), fp64.  Config 3's
+    backward passes take the pooled gradient (>= 75% zeros) with the conv output
+    as relu mask; the others the workload's dout and mask.  Per pass: median ms
+    of each mode; the forward also reports the nnz-based algorithmic work
+    2*F*sum over non-zero inputs of the outputs each reaches.  (The MFMA counts
+    of each mode come from a counter run of --zero-skip-probe.)"""
     import numpy as np
     import torch
     from paper_1802_04647_amd import dmlnn
     from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
 
-    s = SHAPES["lenet_conv1"]
-    X0, W0, b0, _ = conv_layer_inputs("lenet_conv1")
-    Xs = X0.reshape(s.N, s.C, s.Hin, s.Win).copy()
-    Xs[:, :, :6, :] = 0.0
-    Xs[:, :, -6:, :] = 0.0
-    Xs[:, :, :, :6] = 0.0
-    Xs[:, :, :, -6:] = 0.0
-    rh = _reach_counts(s.Hin, s.Hf, s.stride, s.pad, s.Hout)
-    rw = _reach_counts(s.Win, s.Wf, s.stride, s.pad, s.Wout)
-    reach = np.outer(rh, rw)  # outputs per (h, w) for one filter
-    W, b = torch.from_numpy(W0).cuda(), torch.from_numpy(b0).cuda()
-    a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
-    out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=torch.float64, device="cuda")
-    dense_flops = s.flops_per_pass()
+    def workload(name, structured=False):
+        s = SHAPES[name]
+        X0, W0, b0, d0 = conv_layer_inputs(name)
+        if structured:
+            Xs = X0.reshape(s.N, s.C, s.Hin, s.Win).copy()
+            for sl in (np.s_[:, :, :6, :], np.s_[:, :, -6:, :], np.s_[:, :, :, :6], np.s_[:, :, :, -6:]):
+                Xs[sl] = 0.0
+            X0 = Xs.reshape(s.N, -1)
+        return s, X0, W0, b0, d0
+
     res = {}
-    for name, Xh in (("config2_iid_zeros", X0), ("config2_structured_zeros", Xs.reshape(s.N, -1))):
-        nz = (Xh.reshape(s.N, s.C, s.Hin, s.Win) != 0)
-        nnz_flops = 2.0 * s.F * float((nz * reach).sum())
-        X = torch.from_numpy(np.ascontiguousarray(Xh)).cuda()
-        row = {"zero_fraction": round(float(np.mean(Xh == 0)), 4),
-               "dense_gflop": round(dense_flops / 1e9, 4), "nnz_gflop": round(nnz_flops / 1e9, 4)}
-        for mode in (0, 1):
-            prev = dmlnn.set_zero_skip(mode)
-            ms, mn = _median_ms(lambda: dmlnn.conv2d_forward(X, W, b, *a, out=out), reps=20,
-                                warmup=5, with_min=True)
-            dmlnn.set_zero_skip(prev)
-            row["skip" if mode else "dense"] = {
-                "median_ms": round(ms, 4), "min_ms": round(mn, 4),
-                "dense_equiv_gflops": round(dense_flops / (ms / 1e3) / 1e9, 1),
-                "nnz_gflops": round(nnz_flops / (ms / 1e3) / 1e9, 1)}
-        res[name] = row
+    for label, name, structured in (("config2", "lenet_conv1", False),
+                                    ("config2_structured_zeros", "lenet_conv1", True),
+                                    ("config3", "lenet_conv2", False),
+                                    ("config5", "resnet_conv", False)):
+        s, X0, W0, b0, d0 = workload(name, structured)
+        a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+        X, W, b = (torch.from_numpy(np.ascontiguousarray(v)).cuda() for v in (X0, W0, b0))
+        out = torch.empty((s.N, s.F * s.Hout * s.Wout), dtype=torch.float64, device="cuda")
+        dmlnn.conv2d_forward(X, W, b, *a, out=out)
+        if name == "lenet_conv2":
+            # the pooled gradient routed back through the 2x2/2 pool of the output
+            _, idx, _, _ = dmlnn.max_pool2d_fwd(out, s.F, s.Hout, s.Wout, 2, 2, 2, 0)
+            dout = dmlnn.max_pool2d_bwd(torch.from_numpy(d0).cuda(), idx, s.F, s.Hout, s.Wout,
+                                        2, 2, 2, 0)
+        else:
+            dout = torch.from_numpy(d0).cuda()
+        dW, db, dX = torch.empty_like(W), torch.empty_like(b), torch.empty_like(X)
+        ws = torch.empty(dmlnn.conv2d_backward_filter_workspace_size(torch.float64, *s.args()),
+                         dtype=torch.uint8, device="cuda")
+        rh = _reach_counts(s.Hin, s.Hf, s.stride, s.pad, s.Hout)
+        rw = _reach_counts(s.Win, s.Wf, s.stride, s.pad, s.Wout)
+        nz = X0.reshape(s.N, s.C, s.Hin, s.Win) != 0
+        nnz_flops = 2.0 * s.F * float((nz * np.outer(rh, rw)).sum())
+        row = {"x_zero_fraction": round(float(np.mean(X0 == 0)), 4),
+               "g_zero_fraction": round(float(((dout == 0) | (out <= 0)).double().mean()), 4),
+               "dense_gflop_per_pass": round(s.flops_per_pass() / 1e9, 4),
+               "forward_nnz_gflop": round(nnz_flops / 1e9, 4)}
+        fns = {"forward": lambda: dmlnn.conv2d_forward(X, W, b, *a, out=out),
+               "backward_filter": lambda: dmlnn.conv2d_backward_filter(
+                   X, dout, out, *a, s.F, workspace=ws, dW=dW, db=db),
+               "backward_data": lambda: dmlnn.conv2d_backward_data(W, dout, out, *a, dX=dX)}
+        reps = 10 if name == "resnet_conv" else 20
+        for pname, fn in fns.items():
+            for mode in (0, 1):
+                prev = dmlnn.set_zero_skip(mode)
+                ms = _median_ms(fn, reps=reps, warmup=3)
+                dmlnn.set_zero_skip(prev)
+                row.setdefault(pname, {})["skip_ms" if mode else "dense_ms"] = round(ms, 4)
+        res[label] = row
     return res
 
 

@@ -49,7 +49,15 @@ extern "C" {
 #define DMLNN_API
 #endif
 
-typedef enum { DMLNN_F64 = 0, DMLNN_F32 = 1 } dmlnn_dtype;
+typedef enum {
+    DMLNN_F64 = 0,
+    DMLNN_F32 = 1,
+    /* The two bounds widen the type to the whole int range, so any int a caller
+     * passes is a value of the type and an invalid one is reported
+     * (DMLNN_ERR_DTYPE) rather than undefined.  They are not dtypes. */
+    DMLNN_DTYPE_RANGE_MIN_ = -0x7fffffff - 1,
+    DMLNN_DTYPE_RANGE_MAX_ = 0x7fffffff
+} dmlnn_dtype;
 
 typedef enum {
     DMLNN_OK = 0,

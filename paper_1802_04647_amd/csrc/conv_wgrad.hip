@@ -77,6 +77,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
     const int rest = L / a.nkr;
     const int ft = rest % a.nft;
     const int split = rest / a.nft;
+    // 16-row blocks of the filter tile that hold filters (the others' g rows are zero)
+    const int nmb = min(4, (a.F - ft * kBM + 15) / 16);
 
     const int kbeg = kr * a.KR;
     const int kend = min(a.K, kbeg + a.KR);
@@ -357,7 +359,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
             for (int nb = 0; nb < NBW; ++nb) nbv[nb] = s_x[kof[nb] + nqo];
             bool za[4];
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb) za[mb] = ZSKIP && wave_all_zero(av[mb]);
+            for (int mb = 0; mb < 4; ++mb) za[mb] = mb >= nmb || (ZSKIP && wave_all_zero(av[mb]));
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) {
                 if (ZSKIP && wave_all_zero(bv[nb])) continue;

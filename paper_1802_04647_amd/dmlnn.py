@@ -58,10 +58,13 @@ def load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+    # DMLNN_LIBRARY: another build of the same library (the host-sanitized copy
+    # that the CPU sanitizer tests load)
+    path = os.environ.get("DMLNN_LIBRARY") or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
                            "`python -m paper_1802_04647_amd.build`")
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     sig = {
         "conv2d_out_dim": (_i, [_i] * 4),
         "conv2d_forward": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 10 + [_vp]),

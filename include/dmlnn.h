@@ -191,11 +191,50 @@ typedef struct {
     int window_rows;   /* staged input-window rows per channel */
     size_t lds_bytes;  /* dynamic LDS per block */
     size_t workspace_bytes; /* backward_filter: conv2d_backward_filter_workspace_size; else 0 */
+    /* Layout of the staged tiles (for tools that model the kernels' LDS use):
+     * implicit-GEMM kernels: pixels between tile origins, k per chunk (padded to
+     * whole k-steps), row stride of the staged filter slice, bytes of a stage,
+     * of its input window and of its filter slice, 1 when the slice moves 16
+     * bytes a lane; backward_filter: row stride of the staged gradient tile and
+     * the slices a wide output row is cut into (0: tiles are whole rows). */
+    int tile_stride, k_chunk, slice_stride, stage_bytes, window_bytes, slice_bytes, slice_vec;
+    int g_stride, row_slices;
+    int pipelined;     /* register-staged kernels: 1 when a tile's global loads are held in
+                          registers across the previous tile's MFMAs, 0 when staged directly */
+    int fused;         /* conv2d_plan_fused: 1 when the fused kernel runs, 0 when the call
+                          falls back to the plain kernels (then described here) */
 } dmlnn_conv_plan;
 
 DMLNN_API int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F,
                           int Hf, int Wf, int stride, int pad, int zero_skip,
                           dmlnn_conv_plan *plan);
+
+/* The same query for the fused calls (paper, Section "Future Work": vertical
+ * and horizontal fusion; Section 3 "Sparse Operations" for the CSR input).
+ * form:
+ *   DMLNN_FORM_PLAIN            as conv2d_plan;
+ *   DMLNN_FORM_POOL_EPILOGUE    conv2d_forward_pool (pass FORWARD);
+ *   DMLNN_FORM_POOLED_SOURCE    conv2d_backward_filter_pooled / conv2d_backward_data_pooled
+ *                               (pass BACKWARD_FILTER / BACKWARD_DATA);
+ *   DMLNN_FORM_CSR_INPUT        conv2d_forward_csr (pass FORWARD);
+ *   DMLNN_FORM_BANKS            conv2d_forward_multi (pass FORWARD, F = the banks' total;
+ *                               when not fused each bank runs as a plain forward, whose plans
+ *                               conv2d_plan gives).
+ * pool_h, pool_w, pool_stride, pool_pad: the pool of the two pool forms (validated as the
+ * calls validate them), else ignored.  Returns DMLNN_ERR_ARG for a form that does not apply
+ * to the pass. */
+typedef enum {
+    DMLNN_FORM_PLAIN = 0,
+    DMLNN_FORM_POOL_EPILOGUE = 1,
+    DMLNN_FORM_POOLED_SOURCE = 2,
+    DMLNN_FORM_CSR_INPUT = 3,
+    DMLNN_FORM_BANKS = 4
+} dmlnn_conv_form;
+
+DMLNN_API int conv2d_plan_fused(dmlnn_dtype dtype, int pass, int form, int pool_h, int pool_w,
+                                int pool_stride, int pool_pad, int N, int C, int Hin, int Win,
+                                int F, int Hf, int Wf, int stride, int pad, int zero_skip,
+                                dmlnn_conv_plan *plan);
 
 /* nnz-driven operator choice for a dense operand (paper, Section 3 "Sparse
  * Operations": the number of non-zeros kept for every intermediate selects

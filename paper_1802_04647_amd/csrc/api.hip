@@ -253,24 +253,53 @@ int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void *dout, con
                     "conv2d_backward_data");
 }
 
-int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F, int Hf, int Wf,
-                int stride, int pad, int zero_skip, dmlnn_conv_plan *plan)
+static int pool_dims(int N, int C, int Hin, int Win, int Hf, int Wf, int stride, int pad, int &Hout,
+                     int &Wout);
+
+static int plan_query(const char *name, dmlnn_dtype dtype, int pass, int form, int pool_h,
+                      int pool_w, int pool_stride, int pool_pad, int N, int C, int Hin, int Win,
+                      int F, int Hf, int Wf, int stride, int pad, int zero_skip,
+                      dmlnn_conv_plan *plan)
 {
-    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "conv2d_plan: bad dtype %d", (int)dtype);
-    if (!plan) return fail(DMLNN_ERR_NULL, "conv2d_plan: plan is required");
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "%s: bad dtype %d", name, (int)dtype);
+    if (!plan) return fail(DMLNN_ERR_NULL, "%s: plan is required", name);
     if (pass < DMLNN_PASS_FORWARD || pass > DMLNN_PASS_BACKWARD_DATA)
-        return fail(DMLNN_ERR_ARG, "conv2d_plan: bad pass %d", pass);
+        return fail(DMLNN_ERR_ARG, "%s: bad pass %d", name, pass);
     if (zero_skip != 0 && zero_skip != 1)
-        return fail(DMLNN_ERR_ARG, "conv2d_plan: zero_skip must be 0 or 1");
+        return fail(DMLNN_ERR_ARG, "%s: zero_skip must be 0 or 1", name);
     dmlnn::ConvDims d;
     if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    const bool fwd = pass == DMLNN_PASS_FORWARD;
+    switch (form) {
+    case DMLNN_FORM_PLAIN: break;
+    case DMLNN_FORM_POOL_EPILOGUE:
+    case DMLNN_FORM_POOLED_SOURCE: {
+        if (fwd != (form == DMLNN_FORM_POOL_EPILOGUE))
+            return fail(DMLNN_ERR_ARG, "%s: form %d does not apply to pass %d", name, form, pass);
+        int Hp, Wp;
+        if (int r = pool_dims(N, F, d.Hout, d.Wout, pool_h, pool_w, pool_stride, pool_pad, Hp, Wp))
+            return r;
+        if (form == DMLNN_FORM_POOLED_SOURCE &&
+            (pool_pad != 0 || pool_stride < pool_h || pool_stride < pool_w))
+            return fail(DMLNN_ERR_ARG, "%s: a pooled source needs unpadded windows that do not "
+                        "overlap", name);
+        break;
+    }
+    case DMLNN_FORM_CSR_INPUT:
+    case DMLNN_FORM_BANKS:
+        if (!fwd)
+            return fail(DMLNN_ERR_ARG, "%s: form %d does not apply to pass %d", name, form, pass);
+        break;
+    default: return fail(DMLNN_ERR_ARG, "%s: bad form %d", name, form);
+    }
     dmlnn::ConvPlanInfo info;
-    if (dmlnn::conv_plan_info(dtype, pass, d, zero_skip, info) != hipSuccess)
-        return fail(DMLNN_ERR_ARG, "conv2d_plan: no tiling fits these sizes");
+    if (dmlnn::conv_plan_info(dtype, pass, d, zero_skip, form, pool_h, pool_w, pool_stride,
+                              pool_pad, info) != hipSuccess)
+        return fail(DMLNN_ERR_ARG, "%s: no tiling fits these sizes", name);
     memset(plan, 0, sizeof(*plan));
     plan->kernel = info.kernel;
     plan->zero_skip = zero_skip && info.kernel != dmlnn::kConvSmallM &&
-                      info.kernel != dmlnn::kConvResident;
+                      info.kernel != dmlnn::kConvResident && form != DMLNN_FORM_POOLED_SOURCE;
     plan->tile_m = info.tile_m;
     plan->tile_pixels = info.tile_pixels;
     plan->blocks = info.blocks;
@@ -282,8 +311,34 @@ int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int
     plan->lds_bytes = info.lds;
     plan->workspace_bytes =
         pass == DMLNN_PASS_BACKWARD_FILTER ? dmlnn::conv_wgrad_workspace_bytes(dtype, d) : 0;
+    plan->tile_stride = info.tile_stride;
+    plan->k_chunk = info.k_chunk;
+    plan->slice_stride = info.slice_stride;
+    plan->stage_bytes = info.stage_bytes;
+    plan->window_bytes = info.window_bytes;
+    plan->slice_bytes = info.slice_bytes;
+    plan->slice_vec = info.slice_vec;
+    plan->g_stride = info.g_stride;
+    plan->row_slices = info.row_slices;
+    plan->pipelined = info.pipelined;
+    plan->fused = info.fused;
     g_err[0] = '\0';
     return DMLNN_OK;
+}
+
+int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                int stride, int pad, int zero_skip, dmlnn_conv_plan *plan)
+{
+    return plan_query("conv2d_plan", dtype, pass, DMLNN_FORM_PLAIN, 0, 0, 0, 0, N, C, Hin, Win, F,
+                      Hf, Wf, stride, pad, zero_skip, plan);
+}
+
+int conv2d_plan_fused(dmlnn_dtype dtype, int pass, int form, int pool_h, int pool_w,
+                      int pool_stride, int pool_pad, int N, int C, int Hin, int Win, int F, int Hf,
+                      int Wf, int stride, int pad, int zero_skip, dmlnn_conv_plan *plan)
+{
+    return plan_query("conv2d_plan_fused", dtype, pass, form, pool_h, pool_w, pool_stride,
+                      pool_pad, N, C, Hin, Win, F, Hf, Wf, stride, pad, zero_skip, plan);
 }
 
 int conv2d_zero_skip_choice(dmlnn_dtype dtype, int pass, long long nnz, int N, int C, int Hin,
@@ -296,7 +351,7 @@ int conv2d_zero_skip_choice(dmlnn_dtype dtype, int pass, long long nnz, int N, i
                                                          : (long long)N * C * Hin * Win;
     if (nnz < 0 || nnz > n) return -1;
     dmlnn::ConvPlanInfo info;
-    if (dmlnn::conv_plan_info(dtype, pass, d, 1, info) != hipSuccess) return -1;
+    if (dmlnn::conv_plan_info(dtype, pass, d, 1, 0, 0, 0, 0, 0, info) != hipSuccess) return -1;
     if (info.kernel == dmlnn::kConvSmallM) return 0;  // no skip form
     // expected share of all-zero 64-value fragments under independent zeros
     const double density = (double)nnz / (double)n;

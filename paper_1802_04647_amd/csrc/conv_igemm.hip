@@ -1787,21 +1787,49 @@ hipError_t launch_typed(IgemmArgs a, int M, int Cs, int Qh, int Qw, int nimg, in
 
 }  // namespace
 
-hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
-                          ConvPlanInfo &info)
+hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip, int form,
+                          int ph, int pw, int ps, int pp, ConvPlanInfo &info)
 {
     info = ConvPlanInfo{};
-    if (pass == 1) return wgrad_plan_info(dtype, d, info);
+    if (pass == 1) return wgrad_plan_info(dtype, d, form == kFormPooledSource ? ps : 0, info);
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
     const bool bwd = pass == 2;
     // backward_data is the same GEMM over the up-sampled gradient: M = C rows,
     // F source channels of Hout x Wout, Hin x Win output pixels, stride 1
-    const ConvGeo g = bwd ? ConvGeo{d.C, d.F, d.Hout, d.Wout, d.Hin, d.Win, d.Hf, d.Wf, 1, d.N,
-                                    false, 0, 0, 0, 0, zero_skip, 0, 0, 1}
-                          : ConvGeo{d.F, d.C, d.Hin, d.Win, d.Hout, d.Wout, d.Hf, d.Wf, d.stride,
-                                    d.N, false, 0, 0, 0, 0, zero_skip, 0, 0, 1};
+    ConvGeo g = bwd ? ConvGeo{d.C, d.F, d.Hout, d.Wout, d.Hin, d.Win, d.Hf, d.Wf, 1, d.N,
+                              false, 0, 0, 0, 0, zero_skip, 0, 0, 1}
+                    : ConvGeo{d.F, d.C, d.Hin, d.Win, d.Hout, d.Wout, d.Hf, d.Wf, d.stride,
+                              d.N, false, 0, 0, 0, 0, zero_skip, 0, 0, 1};
+    // the fused forms as their calls set them up (the pool form fuses only
+    // unpadded pools whose stride is at least the window height; the calls fall
+    // back to the plain kernels when the fused kernel does not fit)
+    bool applied = true;
+    if (!bwd && form == kFormPoolEpilogue && pp == 0 && ps >= ph) {
+        g.pool = true;
+        g.PS = ps;
+    } else if (!bwd && form == kFormBanks) {
+        g.nbanks = 2;
+        g.require_dma = 1;
+    } else if (!bwd && form == kFormCsr) {
+        g.csr = 1;
+    } else if (bwd && form == kFormPooledSource) {
+        g.pb = 1;
+        g.pb_ps = ps;
+        g.pb_up = d.stride;
+        g.zero_skip = 0;
+    } else {
+        applied = false;
+    }
+    (void)pw;
     ConvChoice c;
-    const hipError_t e = choose_conv(tsz, bwd, g, c);
+    hipError_t e = choose_conv(tsz, bwd, g, c);
+    info.fused = applied && e == hipSuccess;
+    if (e == hipErrorNotSupported && (g.pool || g.nbanks > 1)) {
+        g.pool = false;
+        g.nbanks = 0;
+        g.require_dma = 0;
+        e = choose_conv(tsz, bwd, g, c);
+    }
     if (e != hipSuccess) return e;
     const int Q = g.Qh * g.Qw;
     info.kernel = c.kernel;
@@ -1811,6 +1839,7 @@ hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
     case kConvSmallM:
         info.tile_m = c.small_MM;
         info.tile_pixels = kSmallPix;
+        info.tile_stride = kSmallPix;
         info.blocks = (Q + kSmallPix - 1) / kSmallPix * d.N;
         info.chunk = c.small_kc;
         info.window_width = c.small_Wpad;
@@ -1824,6 +1853,11 @@ hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
         info.k_split = kResKs;
         info.window_width = c.rp.Wpad;
         info.window_rows = c.rp.CH / c.rp.Wpad;
+        info.tile_stride = Q;
+        info.k_chunk = c.rp.KCK;
+        info.slice_stride = c.rp.SA;
+        info.stage_bytes = c.rp.stage;
+        info.slice_bytes = c.rp.lds_a;
         break;
     default: {
         const Plan &p = c.kernel == kConvDma ? c.pd : c.p;
@@ -1834,6 +1868,16 @@ hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
         info.k_split = c.k4 ? 4 : (c.ksplit ? 2 : 1);
         info.window_width = p.Wpad;
         info.window_rows = p.CH / p.Wpad;
+        info.tile_stride = p.TS;
+        info.k_chunk = p.KCK;
+        info.slice_stride = p.SA;
+        info.pipelined = c.kernel == kConvReg ? p.pipelined : 0;
+        if (c.kernel == kConvDma) {
+            info.stage_bytes = c.L.stage_bytes;
+            info.window_bytes = c.L.src_bytes;
+            info.slice_bytes = c.L.a_bytes;
+            info.slice_vec = c.L.a_vec;
+        }
     }
     }
     return hipSuccess;

@@ -980,7 +980,7 @@ size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d)
     return tsz * (size_t)p.splits * ((size_t)d.F * K + (size_t)d.F);
 }
 
-hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info)
+hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanInfo &info)
 {
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
     WPlan p;
@@ -996,6 +996,12 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info)
     info.window_width = p.Wpad;
     info.window_rows = p.rows_max;
     info.lds = p.lds;
+    info.g_stride = p.SG;
+    info.row_slices = p.spr;
+    info.tile_stride = p.RQ;
+    info.pipelined = p.pipelined;
+    if (pool_ps && !ring && kBM * max_regions(p, d, pool_ps) > kThreads * kMGP) info.pipelined = 0;
+    info.fused = pool_ps ? 1 : 0;
     return hipSuccess;
 }
 

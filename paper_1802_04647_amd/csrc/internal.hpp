@@ -37,9 +37,18 @@ struct ConvPlanInfo {
     int window_width;  // staged window row length (elements)
     int window_rows;   // staged window rows per channel
     size_t lds;        // dynamic LDS bytes per block
+    int tile_stride, k_chunk, slice_stride, stage_bytes, window_bytes, slice_bytes, slice_vec;
+    int g_stride, row_slices;
+    int pipelined;  // register-staged kernels: loads held in registers across the MFMAs
+    int fused;      // fused forms: 1 when the fused kernel runs, 0 for the unfused fallback
 };
-hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip,
-                          ConvPlanInfo &info);
+
+// Fused forms a plan query may ask about (the values of dmlnn_conv_form).
+enum ConvForm { kFormPlain = 0, kFormPoolEpilogue = 1, kFormPooledSource = 2, kFormCsr = 3,
+                kFormBanks = 4 };
+// form: ConvForm; ph, pw, ps, pp: the pool of the pool forms (else unused).
+hipError_t conv_plan_info(int dtype, int pass, const ConvDims &d, int zero_skip, int form,
+                          int ph, int pw, int ps, int pp, ConvPlanInfo &info);
 
 // Forward (relu(conv + b)) and input-gradient passes share one implicit-GEMM
 // kernel family; see conv_igemm.hip.
@@ -72,7 +81,8 @@ hipError_t launch_conv_backward_data(int dtype, const void *W, const void *dout,
 // Filter/bias gradient: split reduction into a workspace, then a fixed-order sum.
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d);
 // The backward_filter part of conv_plan_info.
-hipError_t wgrad_plan_info(int dtype, const ConvDims &d, ConvPlanInfo &info);
+// pool_ps: the pool stride of a pooled source, or 0.
+hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanInfo &info);
 // pool (optional): dout is not given; g is built from a following max-pool's
 // backward (see PoolSrc in common.hpp).
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,

@@ -44,7 +44,10 @@ class ConvPlan(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in (
         "kernel", "zero_skip", "tile_m", "tile_pixels", "blocks", "chunk", "k_split", "splits",
         "window_width", "window_rows")] + [("lds_bytes", ctypes.c_size_t),
-                                           ("workspace_bytes", ctypes.c_size_t)]
+                                           ("workspace_bytes", ctypes.c_size_t)] + [
+        (n, ctypes.c_int) for n in ("tile_stride", "k_chunk", "slice_stride", "stage_bytes",
+                                    "window_bytes", "slice_bytes", "slice_vec", "g_stride",
+                                    "row_slices", "pipelined", "fused")]
 
 
 KERNELS = {1: "igemm_dma", 2: "igemm_reg", 3: "small_m", 4: "resident", 5: "wgrad_ring",
@@ -102,6 +105,7 @@ def load():
                         + [ctypes.c_longlong, ctypes.c_longlong, _vp]),
         "count_nonzero": (_i, [_i, _vp, ctypes.c_longlong, _vp, _vp]),
         "conv2d_plan": (_i, [_i] * 12 + [ctypes.POINTER(ConvPlan)]),
+        "conv2d_plan_fused": (_i, [_i] * 17 + [ctypes.POINTER(ConvPlan)]),
         "conv2d_zero_skip_choice": (_i, [_i, _i, ctypes.c_longlong] + [_i] * 9),
         "dmlnn_last_error": (ctypes.c_char_p, []),
     }
@@ -186,6 +190,25 @@ def conv2d_plan(dtype, pass_name, N, C, Hin, Win, F, Hf, Wf, stride, pad, zero_s
     plan = ConvPlan()
     _check("conv2d_plan", load().conv2d_plan(dt, PASSES[pass_name], N, C, Hin, Win, F, Hf, Wf,
                                              stride, pad, int(zero_skip), ctypes.byref(plan)))
+    d = {name: getattr(plan, name) for name, _ in ConvPlan._fields_}
+    d["kernel"] = KERNELS[plan.kernel]
+    return d
+
+
+FORMS = {"plain": 0, "pool_epilogue": 1, "pooled_source": 2, "csr_input": 3, "banks": 4}
+
+
+def conv2d_plan_fused(dtype, pass_name, form, N, C, Hin, Win, F, Hf, Wf, stride, pad,
+                      pool=(0, 0, 0, 0), zero_skip=0) -> dict:
+    """conv2d_plan for a fused call: ``form`` as in ``FORMS``, ``pool`` =
+    (pool_h, pool_w, pool_stride, pool_pad) for the two pool forms."""
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    plan = ConvPlan()
+    ph, pw, ps, pp = pool
+    _check("conv2d_plan_fused",
+           load().conv2d_plan_fused(dt, PASSES[pass_name], FORMS[form], ph, pw, ps, pp, N, C, Hin,
+                                    Win, F, Hf, Wf, stride, pad, int(zero_skip),
+                                    ctypes.byref(plan)))
     d = {name: getattr(plan, name) for name, _ in ConvPlan._fields_}
     d["kernel"] = KERNELS[plan.kernel]
     return d

@@ -111,3 +111,30 @@ def test_zero_skip_choice_follows_density():
         ch("forward", n + 1)
     with pytest.raises(ValueError):
         ch("forward", -1)
+
+
+def test_fused_plan_query():
+    """conv2d_plan_fused reports the kernels the fused calls take, and rejects
+    a form that does not apply to the pass or a pool it cannot fuse."""
+    s = SHAPES["lenet_conv2"]
+    pool = (2, 2, 2, 0)
+    f = dmlnn.conv2d_plan_fused(torch.float64, "forward", "pool_epilogue", *s.args(), pool=pool)
+    assert f["fused"] == 1 and f["kernel"] == "resident"
+    d = dmlnn.conv2d_plan_fused(torch.float64, "backward_data", "pooled_source", *s.args(),
+                                pool=pool)
+    assert d["fused"] == 1 and d["kernel"] == "igemm_dma" and d["zero_skip"] == 0
+    w = dmlnn.conv2d_plan_fused(torch.float64, "backward_filter", "pooled_source", *s.args(),
+                                pool=pool)
+    assert w["kernel"] == dmlnn.conv2d_plan(torch.float64, "backward_filter", *s.args())["kernel"]
+    # a padded pool is not fused: the call runs the plain conv, then the pool
+    u = dmlnn.conv2d_plan_fused(torch.float64, "forward", "pool_epilogue", *s.args(),
+                                pool=(3, 3, 2, 1))
+    assert u["fused"] == 0
+    # the CSR input always takes the register-staged kernel's direct staging
+    c = dmlnn.conv2d_plan_fused(torch.float32, "forward", "csr_input", *s.args())
+    assert c["kernel"] == "igemm_reg" and c["pipelined"] == 0
+    for args in [("forward", "pooled_source", pool), ("backward_data", "pool_epilogue", pool),
+                 ("backward_filter", "csr_input", (0, 0, 0, 0)),
+                 ("backward_data", "pooled_source", (3, 3, 2, 0))]:
+        with pytest.raises(RuntimeError):
+            dmlnn.conv2d_plan_fused(torch.float64, args[0], args[1], *s.args(), pool=args[2])

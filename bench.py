@@ -601,6 +601,56 @@ def cpu_baseline(target_s=12.0):
                       f"images, fp64, {t:.2f} s wall, {cpu}"}
 
 
+def cpu_baselines_lenet(target_s=4.0):
+    """The oracle on bounded samples of the LeNet-scale workloads: the three conv
+    passes of each LeNet layer (fp64 GFLOP/s) and the whole training step
+    (images/s), each on as many images as fit about target_s seconds."""
+    import numpy as np
+    import oracle
+    from oracle import lenet as lenet_oracle
+    from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs, lenet_train_inputs
+
+    cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(cores)
+    res = {}
+    for name in ("lenet_conv1", "lenet_conv2"):
+        s = SHAPES[name]
+        a = (s.C, s.Hin, s.Win, s.Hf, s.Wf, s.stride, s.pad)
+
+        def run(n):
+            X, W, b, _ = conv_layer_inputs(name, N=n)
+            dout = np.random.default_rng(3).standard_normal((n, s.F * s.Hout * s.Wout))
+            t = time.perf_counter()
+            out, _, _ = oracle.conv2d_forward(X, W, b, *a)
+            oracle.conv2d_backward_filter(X, dout, out, *a, s.F)
+            oracle.conv2d_backward_data(W, dout, out, *a)
+            return time.perf_counter() - t
+
+        t1 = run(1)
+        n = int(max(1, min(s.N, round(target_s / max(t1, 1e-3)))))
+        t = run(n) if n > 1 else t1
+        res[name] = {"value": round(3 * 2.0 * n * s.F * s.Hout * s.Wout * s.K / t / 1e9, 3),
+                     "unit": "GFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
+                     "sample": f"fwd+bwd_filter+bwd_data on {n} of {s.N} images, fp64, "
+                               f"{t:.2f} s wall"}
+
+    def step(n):
+        X, Y, params = lenet_train_inputs(n)
+        vel = lenet_oracle.zero_velocities(params)
+        t = time.perf_counter()
+        lenet_oracle.train_step(X, Y, params, vel)
+        return time.perf_counter() - t
+
+    t1 = step(1)
+    n = int(max(1, min(64, round(target_s / max(t1, 1e-3)))))
+    t = step(n) if n > 1 else t1
+    res["lenet_train"] = {"value": round(n / t, 2), "unit": "images/s",
+                          "cores": oracle.get_threads(), "kind": "oracle",
+                          "sample": f"one SGD-momentum training step on {n} of 64 images, fp64, "
+                                    f"{t:.2f} s wall"}
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -695,6 +745,8 @@ def main():
         rec["aux_kernels"] = aux_kernel_timing()
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline()
+        if not args.only_f64:
+            rec["cpu_baselines_lenet"] = cpu_baselines_lenet()
     print(json.dumps(rec), flush=True)
 
 

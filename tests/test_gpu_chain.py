@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-import lenet_oracle
+from oracle import lenet as lenet_oracle
 import oracle
 from gpu_util import assert_close, dev, host
 from paper_1802_04647_amd import dmlnn

@@ -6,7 +6,7 @@ import torch
 
 import oracle
 from gpu_util import assert_close, dev, host, rounded
-from lenet_oracle import forward_probs
+from oracle.lenet import forward_probs
 from paper_1802_04647_amd import dmlnn
 from paper_1802_04647_amd.inputs import lenet_train_inputs, sparse_uniform, streams
 from paper_1802_04647_amd.lenet import LeNetScorer

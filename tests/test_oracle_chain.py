@@ -6,7 +6,7 @@ import numpy as np
 import torch
 import torch.nn.functional as tF
 
-import lenet_oracle
+from oracle import lenet as lenet_oracle
 from paper_1802_04647_amd.inputs import lenet_train_inputs
 
 

@@ -173,7 +173,9 @@ typedef enum {
     DMLNN_KERNEL_SMALL_M = 3,        /* vector-ALU kernel for at most four output rows    */
     DMLNN_KERNEL_RESIDENT = 4,       /* filter-resident forward for small images (fp64)   */
     DMLNN_KERNEL_WGRAD_RING = 5,     /* backward_filter: row ring over the whole k range  */
-    DMLNN_KERNEL_WGRAD_TILES = 6     /* backward_filter: (filter tile, k range) blocks    */
+    DMLNN_KERNEL_WGRAD_TILES = 6,    /* backward_filter: (filter tile, k range) blocks    */
+    DMLNN_KERNEL_WGRAD_POOL_SPARSE = 7 /* backward_filter from a pooled source with at most
+                                          32 filter columns: a sum over the pool windows  */
 } dmlnn_conv_kernel;
 
 typedef struct {

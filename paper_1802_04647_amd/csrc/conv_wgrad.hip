@@ -968,6 +968,176 @@ bool choose_wplan(size_t tsz, const ConvDims &d, WPlan &p, bool &ring)
     return make_wplan(tsz, d, p);
 }
 
+// Pooled source with a short filter row (K = C*Hf*Wf <= kSpK; LeNet conv1: K =
+// 25).  The routed gradient g holds at most one non-zero cell per pool window:
+// the window's argmax, when its pooled value is positive (every other cell of
+// the conv output is zero).  So dW and db are sums over the windows rather
+// than over all pixels (paper, Section 3 "Sparse Operations": an operator that
+// is safe on sparse input does work in proportion to the non-zeros; here the
+// zeros are known from the pool's argmax without looking at them).
+//
+// Block (image group, group of four filters), one wave per filter.  For each
+// image of the group the block stages the zero-padded input image in LDS;
+// each lane then takes windows w, w + 64, ... of its filter's plane (their
+// three pool values loaded kSpB windows at a time) and for a non-zero window
+// adds d * X[n, c, oy*S + i - P, ox*S + j - P] (an LDS read) to its K
+// accumulators and d to the bias one.  The wave's sums are added in a fixed
+// butterfly and written as split `group` of the split workspace, which the
+// same fixed-order reduction as the split kernels completes.
+constexpr int kSpK = 32;
+constexpr int kSpFilters = 4;                 // filters (waves) per block
+constexpr int kSpThreads = kSpFilters * kWave;
+constexpr int kSpB = 2;                       // windows whose pool values load together
+constexpr int kSpStage = 8;                   // image elements a thread loads together
+constexpr size_t kSpLds = 64 * 1024;          // the padded image, at most
+
+// Divisors of the window sum as host magic numbers (every numerator is below
+// 2^16: the staged image holds at most 8192 elements).
+struct SparseMagic {
+    unsigned long long plane, wx, wp;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kSpThreads) void conv_wgrad_pool_sparse_kernel(WgradArgs a,
+                                                                            int groups,
+                                                                            SparseMagic mg)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *s_x = reinterpret_cast<T *>(smem);  // [C][Hin + 2P][Win + 2P], zero borders
+    __shared__ int s_tap[kSpK];
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+    const int nfg = (a.F + kSpFilters - 1) / kSpFilters;
+    const int grp = blockIdx.x / nfg, f = (blockIdx.x - grp * nfg) * kSpFilters + wave;
+    const int n0 = (int)((long long)grp * a.N / groups);
+    const int n1 = (int)((long long)(grp + 1) * a.N / groups);
+    const int Hx = a.Hin + 2 * a.P, Wx = a.Win + 2 * a.P, plane = Hx * Wx;
+    if (tid < kSpK) {  // column k = (c, i, j): its offset from the window origin
+        const int k = min(tid, a.K - 1);
+        const int c = k / a.HfWf, t = k - c * a.HfWf, i = t / a.Wf;
+        s_tap[tid] = c * plane + i * Wx + (t - i * a.Wf);
+    }
+    const PoolSrc &p = a.pool;
+    const T *X = reinterpret_cast<const T *>(a.X);
+    const T *dpool = reinterpret_cast<const T *>(p.dpool);
+    const T *pooled = reinterpret_cast<const T *>(p.pooled);
+    const int nwi = p.Hp * p.Wp;  // windows of one (image, filter) plane
+    const int fc = min(f, a.F - 1);  // waves past the last filter compute and drop
+    T acc[kSpK + 1];
+#pragma unroll
+    for (int k = 0; k <= kSpK; ++k) acc[k] = T(0);
+    for (int n = n0; n < n1; ++n) {
+        __syncthreads();  // the previous image's readers are done
+        const T *xn = X + (size_t)n * a.C * a.Hin * a.Win;
+        // kSpStage loads a thread before any store, so they are in flight together
+        const int tot = a.C * plane;
+        for (int base = 0; base < tot; base += kSpStage * kSpThreads) {
+            T v[kSpStage];
+            bool in[kSpStage];
+#pragma unroll
+            for (int u = 0; u < kSpStage; ++u) {
+                const int e = min(base + u * kSpThreads + tid, tot - 1);
+                const int c = div_magic(e, mg.plane), r = e - c * plane;
+                const int yp = div_magic(r, mg.wx), xp = r - yp * Wx;
+                const int y = yp - a.P, x = xp - a.P;
+                in[u] = y >= 0 && y < a.Hin && x >= 0 && x < a.Win;
+                v[u] = xn[in[u] ? (c * a.Hin + y) * a.Win + x : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < kSpStage; ++u) {
+                const int e = base + u * kSpThreads + tid;
+                if (e < tot) s_x[e] = in[u] ? v[u] : T(0);
+            }
+        }
+        __syncthreads();
+        const size_t pbase = ((size_t)n * a.F + fc) * nwi;
+        for (int w0 = lane; w0 < nwi; w0 += kSpB * kWave) {
+            T pv[kSpB], d[kSpB];
+            int am[kSpB];
+#pragma unroll
+            for (int b = 0; b < kSpB; ++b) {  // clamped: every load issues before any use
+                const size_t o = pbase + min(w0 + b * kWave, nwi - 1);
+                pv[b] = pooled[o];
+                d[b] = dpool[o];
+                am[b] = p.argmax[o];
+            }
+#pragma unroll
+            for (int b = 0; b < kSpB; ++b) {
+                const int w = w0 + b * kWave;
+                const int qa = am[b] - fc * a.Q;  // the argmax cell in the conv output plane
+                const int q = min(max(qa, 0), a.Q - 1);
+                const int oy = div_magic(q, a.magic_wout), ox = q - oy * a.Wout;
+                const int py = div_magic(min(w, nwi - 1), mg.wp), px = w - py * p.Wp;
+                // the cell must lie in its window, as the routing defines it
+                const int ry = oy - py * p.PS, rx = ox - px * p.PS;
+                const bool live = w < nwi && pv[b] > T(0) && qa == q && ry >= 0 && ry < p.PH &&
+                                  rx >= 0 && rx < p.PW;
+                const T de = live ? d[b] : T(0);
+                const T *xw = s_x + oy * a.S * Wx + ox * a.S;  // the window origin
+                // all kSpK columns, no branch: columns past K repeat tap K-1
+                // into accumulators that are never stored
+#pragma unroll
+                for (int k = 0; k < kSpK; ++k) acc[k] += de * xw[s_tap[k]];
+                acc[kSpK] += de;
+            }
+        }
+    }
+    // butterfly over the wave's lanes (fixed order)
+#pragma unroll
+    for (int k = 0; k <= kSpK; ++k) {
+        T v = acc[k];
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+        acc[k] = v;
+    }
+    if (f < a.F && lane == 0) {
+        T *ws = reinterpret_cast<T *>(a.ws);
+#pragma unroll
+        for (int k = 0; k < kSpK; ++k)
+            if (k < a.K) ws[(size_t)grp * a.F * a.K + (size_t)f * a.K + k] = acc[k];
+        ws[(size_t)groups * a.F * a.K + (size_t)grp * a.F + f] = acc[kSpK];
+    }
+}
+
+// Whether a pooled-source backward_filter takes the window sum: short filter
+// rows and a padded input image that fits the block's LDS.
+bool sparse_fits(size_t tsz, const ConvDims &d)
+{
+    return d.C * d.Hf * d.Wf <= kSpK &&
+           tsz * d.C * (size_t)(d.Hin + 2 * d.pad) * (d.Win + 2 * d.pad) <= kSpLds;
+}
+
+size_t sparse_lds(size_t tsz, const ConvDims &d)
+{
+    return tsz * d.C * (size_t)(d.Hin + 2 * d.pad) * (d.Win + 2 * d.pad);
+}
+
+// Image groups of the window sum: one per image up to the workspace's split
+// count (each group is a split of the reduction).
+int sparse_groups(int N, int ws_splits) { return std::max(1, std::min(N, ws_splits)); }
+
+template <typename T>
+hipError_t launch_pool_sparse(WgradArgs a, int groups, size_t lds, void *dW, void *db,
+                              hipStream_t s)
+{
+    a.splits = groups;
+    auto k = conv_wgrad_pool_sparse_kernel<T>;
+    hipError_t e = allow_dynamic_lds(k, lds);
+    if (e != hipSuccess) return e;
+    const int nfg = (a.F + kSpFilters - 1) / kSpFilters;
+    const int Wx = a.Win + 2 * a.P;
+    const SparseMagic mg = {host_magic((a.Hin + 2 * a.P) * Wx), host_magic(Wx),
+                            host_magic(a.pool.Wp)};
+    hipLaunchKernelGGL(k, dim3(nfg * groups), dim3(kSpThreads), lds, s, a, groups, mg);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int FK = a.F * a.K;
+    const int total = FK + (db ? a.F : 0);
+    hipLaunchKernelGGL((conv_wgrad_reduce<T>), dim3((total + 15) / 16), dim3(256), 0, s,
+                       reinterpret_cast<const T *>(a.ws), reinterpret_cast<T *>(dW),
+                       reinterpret_cast<T *>(db), FK, a.F, groups);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 size_t conv_wgrad_workspace_bytes(int dtype, const ConvDims &d)
@@ -986,6 +1156,21 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanIn
     WPlan p;
     bool ring;
     if (!choose_wplan(tsz, d, p, ring)) return hipErrorInvalidValue;
+    if (pool_ps && sparse_fits(tsz, d)) {
+        const int groups = sparse_groups(d.N, p.splits);
+        info.kernel = kWgradPoolSparse;
+        info.tile_m = kSpFilters;
+        info.blocks = (d.F + kSpFilters - 1) / kSpFilters * groups;
+        info.chunk = d.C * d.Hf * d.Wf;
+        info.k_split = 1;
+        info.splits = groups;
+        info.window_width = d.Win + 2 * d.pad;
+        info.window_rows = d.Hin + 2 * d.pad;
+        info.lds = sparse_lds(tsz, d);
+        info.tile_stride = kSpB * kWave;
+        info.fused = 1;
+        return hipSuccess;
+    }
     info.kernel = ring ? kWgradRing : kWgradTiles;
     info.tile_m = kBM;
     info.tile_pixels = p.RQ;
@@ -1056,6 +1241,12 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
         // all-zero fragments: one cell per window holds a value)
         a.pool = *pool;
         a.mask = nullptr;
+        if (sparse_fits(tsz, d)) {  // short filter rows: the sum over the pool windows
+            const int groups = sparse_groups(d.N, p.splits);
+            const size_t lds = sparse_lds(tsz, d);
+            return dtype == 0 ? launch_pool_sparse<double>(a, groups, lds, dW, db, s)
+                              : launch_pool_sparse<float>(a, groups, lds, dW, db, s);
+        }
         // the tiled kernel's register staging holds kMGP windows a thread; more
         // take the direct staging path (one cell at a time)
         if (!ring && kBM * max_regions(p, d, pool->PS) > kThreads * kMGP) a.pipelined = 0;

@@ -22,7 +22,8 @@ enum ConvKernel {
     kConvSmallM = 3,    // vector-ALU kernel for at most four output rows
     kConvResident = 4,  // filter-resident forward for small images (fp64)
     kWgradRing = 5,     // backward_filter, row ring over the whole k range
-    kWgradTiles = 6     // backward_filter, 4-wave (f-tile, k-range, split) blocks
+    kWgradTiles = 6,    // backward_filter, 4-wave (f-tile, k-range, split) blocks
+    kWgradPoolSparse = 7  // backward_filter from a pooled source, small k: the pool windows
 };
 
 // What the plan query reports about one pass (host only, no device access).

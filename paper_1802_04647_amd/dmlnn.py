@@ -51,7 +51,7 @@ class ConvPlan(ctypes.Structure):
 
 
 KERNELS = {1: "igemm_dma", 2: "igemm_reg", 3: "small_m", 4: "resident", 5: "wgrad_ring",
-           6: "wgrad_tiles"}
+           6: "wgrad_tiles", 7: "wgrad_pool_sparse"}
 PASSES = {"forward": 0, "backward_filter": 1, "backward_data": 2}
 _i = ctypes.c_int
 

@@ -1047,10 +1047,65 @@ def model_wgrad_tiles(g, p, tsz, form):
     wgrad_outputs(g, p, tsz, kernel, ranges, NBW, 4, ws_elems)
 
 
+def model_wgrad_pool_sparse(g, p, tsz, form):
+    """The pool-window sum: block (image group, four filters) stages each padded
+    image in LDS; a lane's windows read the K taps around their argmax cell."""
+    kernel = "wgrad_pool_sparse"
+    F, N, K = g["F"], g["N"], g["K"]
+    groups, FW = p["splits"], p["tile_m"]
+    Hx, Wx = g["Hin"] + 2 * g["P"], g["Win"] + 2 * g["P"]
+    plane = Hx * Wx
+    need(form == "pooled_source" and K <= 32 and FW == 4, f"{kernel}: form")
+    need(p["blocks"] == cdiv(F, FW) * groups and 1 <= groups <= N, f"{kernel}: grid")
+    need(p["window_width"] == Wx and p["window_rows"] == Hx, f"{kernel}: staged image")
+    lds = Lds(p["lds_bytes"], kernel)
+    lds.region("image", 0, tsz * g["C"] * plane)
+    ws_elems = p["workspace_bytes"] // tsz
+    need(groups * (F * K + F) <= ws_elems, f"{kernel}: partials exceed the workspace")
+    glob(kernel, "workspace", [(groups - 1) * F * K + (F - 1) * K + K - 1,
+                               groups * F * K + (groups - 1) * F + F - 1], ws_elems)
+    seen = np.zeros(N, dtype=np.int64)
+    for grp in range(groups):
+        n0, n1 = grp * N // groups, (grp + 1) * N // groups
+        need(n1 > n0, f"{kernel}: an empty image group")
+        seen[n0:n1] += 1
+    need(seen == 1, f"{kernel}: images not covered once by the groups")
+    # staging: every padded cell once, from a valid (clamped) input element
+    e = np.arange(g["C"] * plane)
+    c = div_magic(e, plane, f"{kernel} image channel")
+    r = e - c * plane
+    yp = div_magic(r, Wx, f"{kernel} image row")
+    y, x = yp - g["P"], r - yp * Wx - g["P"]
+    inside = (y >= 0) & (y < g["Hin"]) & (x >= 0) & (x < g["Win"])
+    lds.access("image", e, tsz, "image store")
+    glob(kernel, "X", np.where(inside, (c * g["Hin"] + y) * g["Win"] + x, 0),
+         g["C"] * g["Hin"] * g["Win"])
+    # pool arrays of a (image, filter) plane: clamped window indices
+    nwi = g["Hp"] * g["Wp"]
+    w = np.arange(0, cdiv(nwi, 256) * 256)
+    glob(kernel, "pool arrays", ((N - 1) * F + F - 1) * nwi + np.minimum(w, nwi - 1), N * F * nwi)
+    # every cell a window routes (also the clamped cell of dead windows): its
+    # K taps stay in the staged image, and tap k is input (c, oy*S+i-P, ox*S+j-P)
+    div_magic(np.arange(nwi), g["Wp"], f"{kernel} window row")
+    q = np.arange(g["Q"])
+    oy = div_magic(q, g["Wout"], f"{kernel} cell row")
+    ox = q - oy * g["Wout"]
+    k = np.arange(K)
+    HfWf = g["Hf"] * g["Wf"]
+    kc, kt = k // HfWf, k % HfWf
+    tap = kc * plane + (kt // g["Wf"]) * Wx + kt % g["Wf"]
+    idx = (oy * g["S"] * Wx + ox * g["S"])[:, None] + tap[None, :]
+    lds.access("image", idx, tsz, "tap read")
+    yy = (oy[:, None] * g["S"] + kt // g["Wf"]) - g["P"]
+    xx = (ox[:, None] * g["S"] + kt % g["Wf"]) - g["P"]
+    need((idx // plane == kc) & ((idx % plane) // Wx - g["P"] == yy) & ((idx % plane) % Wx - g["P"] == xx),
+         f"{kernel}: a tap reads the wrong input cell")
+
+
 # ================================================================ dispatch
 MODELS = {"igemm_dma": model_igemm_dma, "igemm_reg": model_igemm_reg, "small_m": model_small_m,
           "resident": model_resident, "wgrad_ring": model_wgrad_ring,
-          "wgrad_tiles": model_wgrad_tiles}
+          "wgrad_tiles": model_wgrad_tiles, "wgrad_pool_sparse": model_wgrad_pool_sparse}
 
 
 def check_conv(s, pass_name, dtype, plan, form="plain", pool=None):

@@ -123,6 +123,10 @@ PB_CASES = [
     (ConvShape(2, 12, 16, 16, 40, 3, 3, 2, 1), 2, 2, 2),    # conv stride 2: up-sampled source
     (ConvShape(1, 6, 5, 500, 8, 3, 3, 1, 1), 2, 2, 2),      # wide rows: register-staged kernels
     (ConvShape(2, 3, 9, 70, 10, 3, 3, 1, 1), 1, 1, 1),      # 1x1 pool; rows sliced in backward_filter
+    # backward_filter as a sum over the pool windows (K <= 32)
+    (ConvShape(3, 2, 11, 9, 5, 3, 3, 2, 1), 2, 2, 2),       # conv stride 2
+    (ConvShape(2, 1, 17, 15, 7, 5, 5, 1, 2), 3, 3, 3),      # trailing rows/cols no window covers
+    (ConvShape(4, 3, 8, 8, 40, 3, 3, 1, 0), 2, 3, 3),       # gaps between windows, 40 filters
 ]
 
 

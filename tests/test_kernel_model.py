@@ -112,7 +112,8 @@ def test_every_kernel_and_form_is_modelled():
     for want in [("igemm_dma", "pool_epilogue"), ("resident", "pool_epilogue"),
                  ("igemm_dma", "pooled_source"), ("igemm_reg", "pooled_source"),
                  ("small_m", "pooled_source"), ("wgrad_ring", "pooled_source"),
-                 ("wgrad_tiles", "pooled_source"), ("igemm_reg", "csr_input"),
+                 ("wgrad_tiles", "pooled_source"), ("wgrad_pool_sparse", "pooled_source"),
+                 ("igemm_reg", "csr_input"),
                  ("igemm_dma", "banks")]:
         assert want in kinds, want
 

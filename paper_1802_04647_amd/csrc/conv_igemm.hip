@@ -392,9 +392,16 @@ __global__ __launch_bounds__(kThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
     const int wm = wave & 1, wn = wave >> 1;
-    const int n = blockIdx.x / a.tiles_per_img;
-    const int tile = blockIdx.x - n * a.tiles_per_img;
-    const int m0 = blockIdx.y * kBM;
+    // Consecutive tiles of an image share the halo rows of their source
+    // windows: the blocks are renumbered so that runs of consecutive tiles go
+    // to one XCD, whose L2 then serves the second read of each halo row (dealt
+    // round-robin, neighbours sat on different XCDs and fetched the halo from
+    // HBM again: backward_data read 1.29 GB of HBM for 0.82 GB of operands).
+    const int Lb = xcd_logical_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+    const int bx = Lb % gridDim.x, by = Lb / gridDim.x;
+    const int n = bx / a.tiles_per_img;
+    const int tile = bx - n * a.tiles_per_img;
+    const int m0 = by * kBM;
     const int q0 = tile * a.TS;
     const int qend = min(q0 + a.TS, a.Q);
     const int qy0 = q0 / a.Qw;

@@ -73,6 +73,14 @@ def div_small(n, d, what="reciprocal division"):
     return q
 
 
+def xcd_logical_block(b, n):
+    """The kernels' renumbering of block b of n (runs of consecutive logical
+    blocks on one XCD); must be a permutation of the grid."""
+    b = np.asarray(b, dtype=np.int64)
+    m = n >> 3
+    return np.where(b >= 8 * m, b, (b & 7) * m + (b >> 3))
+
+
 def mfma_row(tsz, lane, r):
     """Output row held by accumulator register r of a 16x16x4 MFMA lane."""
     return (lane >> 4) + 4 * r if tsz == 8 else 4 * (lane >> 4) + r
@@ -255,6 +263,9 @@ def model_igemm_dma(g, p, tsz, form):
     need(c0s[-1] * (M if bwd else 1) * HfWf * tsz <= INT_MAX, f"{kernel}: filter soffset overflows")
     tiles, m_tiles = cdiv(Q, TS), cdiv(M, BM)
     need(p["blocks"] == g["N"] * tiles * m_tiles, f"{kernel}: block count")
+    nblk = p["blocks"]
+    need(np.array_equal(np.sort(xcd_logical_block(np.arange(nblk), nblk)), np.arange(nblk)),
+         f"{kernel}: the block renumbering is not a permutation")
 
     lane = np.arange(WAVE)
     lq, l16 = lane >> 4, lane & 15

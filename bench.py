@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--separate-mask", action="store_true",
+                    help="time the step with both backward passes applying the relu mask "
+                         "(no masked gradient handed from backward_filter to backward_data)")
     ap.add_argument("--zero-skip-probe", action="store_true",
                     help="only run the config 2 zero-skip measurement (for counter runs)")
     ap.add_argument("--only-f64", action="store_true",
@@ -78,7 +81,11 @@ def measured_traffic(pass_name: str):
     return float(m.group(1)) if m else None
 
 
-def conv_step_timing(dtype_name, steps, warmup):
+def conv_step_timing(dtype_name, steps, warmup, emit=True):
+    """The three passes of the ResNet-shaped layer, timed.  emit: backward_filter
+    also writes the relu-masked gradient it stages (conv2d_backward_filter_emit)
+    and backward_data takes it with no mask; else both passes take dout and the
+    mask."""
     import torch
     from paper_1802_04647_amd import dmlnn
     from paper_1802_04647_amd.inputs import SHAPES, conv_layer_inputs
@@ -96,6 +103,7 @@ def conv_step_timing(dtype_name, steps, warmup):
     dX = torch.empty_like(X)
     ws = torch.empty(dmlnn.conv2d_backward_filter_workspace_size(tdt, *s.args()),
                      dtype=torch.uint8, device="cuda")
+    g = torch.empty_like(dout) if emit else None
 
     def step(ev=None):
         if ev is not None:
@@ -103,10 +111,13 @@ def conv_step_timing(dtype_name, steps, warmup):
         dmlnn.conv2d_forward(X, W, b, *a, relu=True, out=out)
         if ev is not None:
             ev[1].record()
-        dmlnn.conv2d_backward_filter(X, dout, out, *a, s.F, workspace=ws, dW=dW, db=db)
+        dmlnn.conv2d_backward_filter(X, dout, out, *a, s.F, workspace=ws, dW=dW, db=db, g_out=g)
         if ev is not None:
             ev[2].record()
-        dmlnn.conv2d_backward_data(W, dout, out, *a, dX=dX)
+        if emit:
+            dmlnn.conv2d_backward_data(W, g, None, *a, dX=dX)
+        else:
+            dmlnn.conv2d_backward_data(W, dout, out, *a, dX=dX)
         if ev is not None:
             ev[3].record()
 
@@ -682,7 +693,7 @@ def main():
         lt = lenet_timing()
         print(json.dumps({"lenet_training": {k: round(v, 4) for k, v in lt.items()}}), flush=True)
         return
-    r = conv_step_timing("f64", args.steps, args.warmup)
+    r = conv_step_timing("f64", args.steps, args.warmup, emit=not args.separate_mask)
     N, F3 = r["N"], 3 * r["flops_per_pass"]
     ms_step = r["wall_s"] * 1e3 / args.steps
     gflops = F3 / (ms_step / 1e3) / 1e9
@@ -705,7 +716,10 @@ def main():
         "data": "synthetic (seeded relu(N(0,1)) activations, He-normal filters, N(0,1) upstream "
                 "gradient)",
         "config": {"workload": "resnet_conv: conv2d 64->64, 56x56, 3x3, stride 1, pad 1, "
-                               "bias_add+relu fused; forward + backward_filter + backward_data",
+                               "bias_add+relu fused; forward + backward_filter + backward_data"
+                               + ("" if args.separate_mask else
+                                  " (backward_filter hands the relu-masked gradient to "
+                                  "backward_data)"),
                    "global_batch": N, "seq_len": None, "parallelism": "single GPU"},
         "pct_of_fp64_mfma_peak": round(100.0 * gflops / 1e3 / PEAK_F64_MFMA, 2),
         "images_per_s": round(N / (ms_step / 1e3), 1),
@@ -719,6 +733,11 @@ def main():
                      "traffic": measured_traffic(dom)},
     }
     rec["hbm_copy"] = copy_calibration()
+    if not args.only_f64 and not args.separate_mask:
+        rs = conv_step_timing("f64", args.steps, args.warmup, emit=False)
+        rec["separate_mask"] = {"ms_per_step": round(rs["wall_s"] * 1e3 / args.steps, 4),
+                                "per_pass_ms": {k: round(v, 4) for k, v in
+                                                rs["per_pass_ms"].items()}}
     if not args.only_f64:
         r32 = conv_step_timing("f32", args.steps, args.warmup)
         ms32 = r32["wall_s"] * 1e3 / args.steps

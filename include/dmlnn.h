@@ -113,6 +113,22 @@ DMLNN_API int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const voi
                            int F, int Hf, int Wf, int stride, int pad,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* conv2d_backward_filter that also writes the masked gradient it stages,
+ *   g_out[n,f,oh,ow] = g[n,f,oh,ow]   (g as in conv2d_backward_filter),
+ * so that conv2d_backward_data can take g_out as its dout with out_fwd = NULL
+ * and skip the mask (paper, Section "Future Work": vertical fusion across the
+ * layer's two backward functions; the relu mask is applied once).  g_out is a
+ * caller-owned N x (F*Hout*Wout) device buffer; it may be dout itself (masked
+ * in place: each element is read and written by the one thread that stages
+ * it), but must not overlap X, dW, db, the workspace or a distinct out_fwd
+ * (DMLNN_ERR_ARG).  Otherwise as conv2d_backward_filter: same workspace, same
+ * results bit for bit. */
+DMLNN_API int conv2d_backward_filter_emit(dmlnn_dtype dtype, const void *X, const void *dout,
+                                          const void *out_fwd, void *dW, void *db, void *g_out,
+                                          int N, int C, int Hin, int Win, int F, int Hf, int Wf,
+                                          int stride, int pad, void *workspace,
+                                          size_t workspace_bytes, void *stream);
+
 /* conv2d_backward_filter for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): the same computation, plan and result — bitwise equal to

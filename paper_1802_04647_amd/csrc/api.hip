@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
 #include <mutex>
 
@@ -207,6 +208,46 @@ int conv2d_backward_filter(dmlnn_dtype dtype, const void *X, const void *dout, c
     return launched(dmlnn::launch_conv_backward_filter(dtype, X, dout, out_fwd, dW, db, d, workspace,
                                                        zero_skip_mode(), (hipStream_t)stream),
                     "conv2d_backward_filter");
+}
+
+// Whether the byte ranges [a, a + na) and [b, b + nb) share a byte.
+static bool overlaps(const void *a, size_t na, const void *b, size_t nb)
+{
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+int conv2d_backward_filter_emit(dmlnn_dtype dtype, const void *X, const void *dout,
+                                const void *out_fwd, void *dW, void *db, void *g_out, int N,
+                                int C, int Hin, int Win, int F, int Hf, int Wf, int stride,
+                                int pad, void *workspace, size_t workspace_bytes, void *stream)
+{
+    const char *name = "conv2d_backward_filter_emit";
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "%s: bad dtype %d", name, (int)dtype);
+    if (!X || !dout || !dW || !g_out)
+        return fail(DMLNN_ERR_NULL, "%s: X, dout, dW and g_out are required", name);
+    dmlnn::ConvDims d;
+    if (int r = conv_dims(d, N, C, Hin, Win, F, Hf, Wf, stride, pad)) return r;
+    const size_t need = dmlnn::conv_wgrad_workspace_bytes(dtype, d);
+    if (need == 0) return fail(DMLNN_ERR_ARG, "%s: no tiling fits these sizes", name);
+    if (!workspace || workspace_bytes < need)
+        return fail(DMLNN_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name,
+                    need, workspace ? workspace_bytes : (size_t)0);
+    // g_out may be dout itself (each element is read and written by one
+    // thread, and masking is idempotent), but no other operand
+    const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
+    const size_t gbytes = (size_t)N * F * d.Hout * d.Wout * esz;
+    const size_t xbytes = (size_t)N * C * Hin * Win * esz, wbytes = (size_t)F * C * Hf * Wf * esz;
+    if (overlaps(g_out, gbytes, X, xbytes) || overlaps(g_out, gbytes, dW, wbytes) ||
+        (db && overlaps(g_out, gbytes, db, (size_t)F * esz)) ||
+        overlaps(g_out, gbytes, workspace, workspace_bytes) ||
+        (out_fwd && out_fwd != dout && overlaps(g_out, gbytes, out_fwd, gbytes)))
+        return fail(DMLNN_ERR_ARG, "%s: g_out overlaps another operand", name);
+    if (int r = device_check()) return r;
+    return launched(dmlnn::launch_conv_backward_filter(dtype, X, dout, out_fwd, dW, db, d, workspace,
+                                                       zero_skip_mode(), (hipStream_t)stream,
+                                                       nullptr, g_out),
+                    name);
 }
 
 int conv2d_backward_filter_noalloc(dmlnn_dtype dtype, const void *X, const void *dout,

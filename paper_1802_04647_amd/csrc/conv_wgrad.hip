@@ -61,6 +61,8 @@ struct WgradArgs {
     int spr;        // 0: tiles are runs of whole output rows; else slices per output row
     unsigned long long magic_rq, magic_wpad, magic_ch, magic_wout, magic_hwf, magic_wf;
     PoolSrc pool;   // PB kernels: g comes from a following max-pool's backward
+    void *g_out;    // or null: g (dout masked to out_fwd > 0) is also written here
+                    // (by the k-range-0 blocks, each element once)
 };
 
 template <typename T, int NBW, bool ZSKIP, bool PB>
@@ -256,12 +258,17 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
                 s_g[r * a.SG + len + (e - r * tail)] = T(0);
             }
         } else {
+        T *gout = (a.g_out && kr == 0) ? reinterpret_cast<T *>(a.g_out) : nullptr;
+        const size_t gbase = ((size_t)g.n * a.F + ft * kBM) * a.Q;
 #pragma unroll
         for (int it = 0; it < kMG; ++it) {
             const int e = tid + kThreads * it;
             if (e < tot_g) {
                 const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
-                s_g[r * a.SG + u] = (vm[it] > T(0)) ? vg[it] : T(0);
+                const T v = (vm[it] > T(0)) ? vg[it] : T(0);
+                s_g[r * a.SG + u] = v;
+                if (gout && ft * kBM + r < a.F && g.q0 + u < g.qend)
+                    gout[gbase + (size_t)r * a.Q + g.q0 + u] = v;
             }
         }
         }
@@ -286,6 +293,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_wgrad_kernel(WgradArgs a)
                     } else {
                         v = dout[goff + q];
                         if (mask && !(mask[goff + q] > T(0))) v = T(0);
+                        if (a.g_out && kr == 0) reinterpret_cast<T *>(a.g_out)[goff + q] = v;
                     }
                 }
                 s_g[r * a.SG + u] = v;
@@ -544,9 +552,10 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             vm[it] = mv;
         }
     };
-    auto store_g = [&](int oh) {
+    auto store_g = [&](int n, int oh) {
         const int tid = opaque(threadIdx.x);
         if constexpr (PB) {
+            (void)n;
             const int py = div_magic(oh, a.pool.magic_ps);
 #pragma unroll
             for (int it = 0; it < kRGP; ++it) {
@@ -564,12 +573,32 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             }
             return;
         }
+        (void)n;
 #pragma unroll
         for (int it = 0; it < NG; ++it) {
             const int e = tid + kRingThreads * it;
             if (e < kBM * a.RQ) {
                 const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
                 s_g[r * a.SG + u] = (vm[it] > T(0)) ? vg[it] : T(0);
+            }
+        }
+    };
+    // The staged tile's masked gradient to g_out (k-range 0 only): issued after
+    // the barrier that ends the staging phase, from the registers the tile was
+    // loaded into (before the next tile's loads reuse them), so the stores
+    // leave the phase in which the matrix pipe idles.
+    T *const gout = (!PB && a.g_out && kr == 0) ? reinterpret_cast<T *>(a.g_out) : nullptr;
+    auto emit_g = [&](int n, int oh) {
+        if (PB || !gout) return;
+        const int tid = opaque(threadIdx.x);
+#pragma unroll
+        for (int it = 0; it < NG; ++it) {
+            const int e = tid + kRingThreads * it;
+            if (e < kBM * a.RQ) {
+                const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
+                if (u < a.Wout && ft * kBM + r < a.F)
+                    gout[((size_t)n * a.F + ft * kBM + r) * a.Q + (size_t)oh * a.Wout + u] =
+                        (vm[it] > T(0)) ? vg[it] : T(0);
             }
         }
     };
@@ -635,9 +664,10 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
                 s_g[r * a.SG + a.Wout + (e - r * tail)] = T(0);
             }
         }
-        store_g(oh0);
+        store_g(n0, oh0);
         stage_x_full(n0, oh0);
         __syncthreads();
+        emit_g(n0, oh0);
         if (t_begin + 1 < t_end) {
             const long long t1 = t_begin + 1;
             const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
@@ -693,12 +723,13 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
 
         if (tt + 1 < t_end) {
             __syncthreads();
-            store_g(oh1);
+            store_g(n1, oh1);
             if (oh1 != 0)
                 store_x(oh1);
             else
                 stage_x_full(n1, oh1);
             __syncthreads();
+            emit_g(n1, oh1);
             if (tt + 2 < t_end) {
                 const int n2 = oh1 + 1 < a.Hout ? n1 : n1 + 1, oh2 = oh1 + 1 < a.Hout ? oh1 + 1 : 0;
                 load_g(n2, oh2);
@@ -1193,7 +1224,7 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanIn
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
                                        const void *out_fwd, void *dW, void *db,
                                        const ConvDims &d, void *ws, int zero_skip,
-                                       hipStream_t s, const PoolSrc *pool)
+                                       hipStream_t s, const PoolSrc *pool, void *g_out)
 {
     const size_t tsz = dtype == 0 ? sizeof(double) : sizeof(float);
     WPlan p;
@@ -1236,6 +1267,7 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.magic_wout = host_magic(d.Wout);
     a.magic_hwf = host_magic(a.HfWf);
     a.magic_wf = host_magic(d.Wf);
+    a.g_out = pool ? nullptr : g_out;
     if (pool) {
         // the pooled source has no zero-skip form (its routed gradient has no
         // all-zero fragments: one cell per window holds a value)

@@ -89,7 +89,8 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanIn
 hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dout,
                                        const void *out_fwd, void *dW, void *db,
                                        const ConvDims &d, void *ws, int zero_skip,
-                                       hipStream_t s, const PoolSrc *pool = nullptr);
+                                       hipStream_t s, const PoolSrc *pool = nullptr,
+                                       void *g_out = nullptr);
 
 // ----------------------------------------------------------------- others ----
 hipError_t launch_bias_add_relu(int dtype, const void *X, const void *b, void *out, int N, int C,

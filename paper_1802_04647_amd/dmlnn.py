@@ -74,6 +74,8 @@ def load():
         "conv2d_backward_filter_workspace_size": (ctypes.c_size_t, [_i] * 10),
         "conv2d_backward_filter": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9
                                    + [_vp, ctypes.c_size_t, _vp]),
+        "conv2d_backward_filter_emit": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 9
+                                        + [_vp, ctypes.c_size_t, _vp]),
         "conv2d_backward_data": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
         "conv2d_backward_filter_noalloc": (_i, [_i, _vp, _vp, _vp, _vp, _vp] + [_i] * 9 + [_vp]),
         "conv2d_backward_filter_pooled": (_i, [_i] + [_vp] * 6 + [_i] * 13
@@ -250,9 +252,12 @@ def conv2d_backward_filter_workspace_size(dtype, N, C, Hin, Win, F, Hf, Wf, stri
 
 
 def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F,
-                           want_db=True, workspace=None, dW=None, db=None):
-    """Returns (dW F x C*Hf*Wf, db F or None); out_fwd None means no relu mask."""
-    dt = _dtype(X, dout, out_fwd, dW, db)
+                           want_db=True, workspace=None, dW=None, db=None, g_out=None):
+    """Returns (dW F x C*Hf*Wf, db F or None); out_fwd None means no relu mask.
+    With g_out (an N x F*Hout*Wout buffer, possibly dout itself) the masked
+    gradient is written there too (conv2d_backward_filter_emit), ready to be
+    conv2d_backward_data's dout with out_fwd None."""
+    dt = _dtype(X, dout, out_fwd, dW, db, g_out)
     N = X.shape[0]
     need = conv2d_backward_filter_workspace_size(dt, N, C, Hin, Win, F, Hf, Wf, stride, pad)
     if workspace is None:
@@ -267,6 +272,13 @@ def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F
     _need(out_fwd, N * F * max(Hout, 0) * max(Wout, 0), "out_fwd")
     _need(dW, F * C * Hf * Wf, "dW")
     _need(db, F, "db")
+    if g_out is not None:
+        _need(g_out, N * F * max(Hout, 0) * max(Wout, 0), "g_out")
+        _check("conv2d_backward_filter_emit", load().conv2d_backward_filter_emit(
+            dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), _p(g_out), N, C, Hin, Win, F, Hf,
+            Wf, stride, pad, _p(workspace), workspace.numel() * workspace.element_size(),
+            _stream()))
+        return dW, db
     _check("conv2d_backward_filter", load().conv2d_backward_filter(
         dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
         stride, pad, _p(workspace), workspace.numel() * workspace.element_size(), _stream()))

@@ -936,6 +936,12 @@ def model_wgrad_ring(g, p, tsz, form):
                     lds.access("g", (l16 + 16 * mb) * SG + lq + qq, tsz, "g fragment read")
     tid = np.arange(768)
     lds.access("g", (tid // 12) * SG + RQ - 1, tsz, "db read")
+    # the emitted masked gradient: (n, f, oh, u) for f < F, u < Wout
+    f = np.arange(cdiv(g["F"], BM) * BM)[:, None]
+    u = np.arange(RQ)[None, :]
+    ok = (f < g["F"]) & (u < Wout)
+    for n, oh in ((0, 0), (g["N"] - 1, g["Hout"] - 1)):
+        glob(kernel, "g_out", ((n * g["F"] + f) * g["Q"] + oh * Wout + u)[ok], g["N"] * g["F"] * g["Q"])
     ring_contents_ok(g, kernel, g["N"] * g["Hout"], p["splits"])
     ring_contents_ok(g, kernel, g["N"] * g["Hout"], 1)
     wgrad_outputs(g, p, tsz, kernel, ranges, NBW, 12, ws_elems)
@@ -1055,6 +1061,15 @@ def model_wgrad_tiles(g, p, tsz, form):
                 lds.access("all", (l16 + 16 * mb) * SG + lq + qq, tsz, "g fragment read")
     tid = np.arange(256)
     lds.access("g", (tid >> 2) * SG + RQ - 1, tsz, "db read")
+    # the emitted masked gradient of the last image's last tile and filter tile
+    ft = cdiv(g["F"], BM) - 1
+    r = np.arange(BM)[:, None]
+    u = np.arange(RQ)[None, :]
+    q0 = Q - (Q - 1) % RQ - 1 if not spr else (g["Hout"] - 1) * Wout + (spr - 1) * RQ
+    qend = Q
+    ok = (ft * BM + r < g["F"]) & (q0 + u < qend)
+    glob(kernel, "g_out", (((g["N"] - 1) * g["F"] + ft * BM) * Q + r * Q + q0 + u)[ok],
+         g["N"] * g["F"] * Q)
     wgrad_outputs(g, p, tsz, kernel, ranges, NBW, 4, ws_elems)
 
 

@@ -83,6 +83,18 @@ def test_conv_backward_validation(lib):
               None) == ERR_NULL
     assert bf(5, FAKE, FAKE, None, FAKE, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, FAKE, need,
               None) == ERR_DTYPE
+    # the masked-gradient form: g_out is required and may not overlap X, dW,
+    # db or the workspace (dout itself is allowed); each call fails validation
+    be = lib.conv2d_backward_filter_emit
+    X, dout, dW, g, ws = 0x10000, 0x20000, 0x30000, 0x40000, 0x50000
+    args = (2, 1, 8, 8, 2, 3, 3, 1, 1)
+    assert be(0, X, dout, None, dW, None, None, *args, ws, need, None) == ERR_NULL
+    assert be(0, X, dout, None, dW, None, X + 8, *args, ws, need, None) == ERR_ARG
+    assert "overlaps" in dmlnn.last_error()
+    assert be(0, X, dout, None, dW, None, dW, *args, ws, need, None) == ERR_ARG
+    assert be(0, X, dout, None, dW, None, ws + 64, *args, ws, need, None) == ERR_ARG
+    assert be(0, X, dout, None, dW, None, g, *args, ws, need - 1, None) == ERR_WS
+    assert be(0, X, dout, None, dW, None, g, 2, 1, 8, 8, 2, 3, 3, 0, 1, ws, need, None) == ERR_ARG
     bd = lib.conv2d_backward_data
     assert bd(0, FAKE, FAKE, None, None, 2, 1, 8, 8, 2, 3, 3, 1, 1, None) == ERR_NULL
     assert bd(0, FAKE, FAKE, None, FAKE, 2, 1, 8, 8, 2, 3, 3, 0, 1, None) == ERR_ARG

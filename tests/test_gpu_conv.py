@@ -326,3 +326,43 @@ def test_identity_filter_is_exact():
                                      1, 1)
     exp = np.maximum(X.reshape(3, C, 100) + b[None, :, None], 0.0).reshape(3, -1)
     assert np.array_equal(host(out), exp)
+
+
+# backward_filter that also writes the masked gradient it stages, which
+# backward_data then takes with no mask: the row-ring kernel (one and two k
+# ranges), the tiled kernel (register and direct staging, several k ranges,
+# rows cut into slices), both dtypes
+EMIT_CASES = [
+    ConvShape(2, 40, 12, 12, 48, 3, 3, 1, 1),
+    ConvShape(1, 128, 3, 12, 2, 3, 3, 1, 1),
+    ConvShape(3, 20, 9, 9, 70, 5, 5, 2, 2),
+    ConvShape(4, 16, 16, 16, 40, 3, 3, 2, 1),
+    ConvShape(1, 6, 5, 500, 8, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("s", EMIT_CASES, ids=str)
+def test_backward_filter_emits_masked_gradient(s, dt):
+    X0, W0, b0, dout0 = random_conv_case(71, s, zero_frac=0.3)
+    X, W, b, dout = (rounded(v, dt) for v in (X0, W0, b0, dout0))
+    a = _args(s)
+    print(f"\n[gpu] backward_filter emit {s} {dt}", flush=True)
+    out, _, _ = dmlnn.conv2d_forward(dev(X, dt), dev(W, dt), dev(b, dt), *a, relu=True)
+    Xd, dd = dev(X, dt), dev(dout, dt)
+    dW0, db0 = dmlnn.conv2d_backward_filter(Xd, dd, out, *a, s.F)
+    dX0 = dmlnn.conv2d_backward_data(dev(W, dt), dd, out, *a)
+    g = torch.full_like(dd, float("nan"))
+    dW1, db1 = dmlnn.conv2d_backward_filter(Xd, dd, out, *a, s.F, g_out=g)
+    dX1 = dmlnn.conv2d_backward_data(dev(W, dt), g, None, *a)
+    # in place: dout itself receives the masked gradient
+    dd2 = dd.clone()
+    dW2, db2 = dmlnn.conv2d_backward_filter(Xd, dd2, out, *a, s.F, g_out=dd2)
+    torch.cuda.synchronize()
+    want_g = torch.where(out > 0, dd, torch.zeros_like(dd))
+    assert torch.equal(g, want_g) and torch.equal(dd2, want_g)
+    for x0, x1 in ((dW0, dW1), (db0, db1), (dX0, dX1), (dW0, dW2), (db0, db2)):
+        assert torch.equal(x0, x1)
+    ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, host(out), *a, s.F)
+    assert_close(host(dW1), ref_dW, dt, "dW")
+    assert_close(host(db1), ref_db, dt, "db")

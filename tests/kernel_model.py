@@ -18,6 +18,10 @@ on one side), every k-step is taken once and every output element written once.
 A kernel change that moves an index without the matching plan change shows up
 here, on the CPU, before any GPU run.  The model restates the kernels' index
 expressions; it shares no code with them or with the oracle.
+
+Launches of more than MAX_TILES tiles (or k ranges) are checked on a fixed
+sample: the first and last 32 and an even spread between (a tile's index math
+depends on its position only), without the whole-output coverage count.
 """
 from __future__ import annotations
 
@@ -31,6 +35,27 @@ INT_MAX = (1 << 31) - 1
 
 class ModelError(AssertionError):
     pass
+
+
+MAX_TILES = 256
+
+
+def sample(n, k=MAX_TILES):
+    """All of range(n), or the fixed sample of a large launch: the first and
+    last k/8 and an even spread, k in all."""
+    if n <= k:
+        return list(range(n))
+    e = max(1, k // 8)
+    return sorted(set(range(e)) | set(range(n - e, n)) |
+                  set(int(v) for v in np.linspace(0, n - 1, k - 2 * e)))
+
+
+def sample_pairs(m_tiles, tiles):
+    """(row tile, pixel tile) pairs of a launch, sampled to about MAX_TILES."""
+    if m_tiles * tiles <= MAX_TILES:
+        return [(mt, t) for mt in range(m_tiles) for t in range(tiles)]
+    km = min(m_tiles, 4)
+    return [(mt, t) for mt in sample(m_tiles, km) for t in sample(tiles, max(MAX_TILES // km, 8))]
 
 
 def need(cond, what):
@@ -319,89 +344,94 @@ def model_igemm_dma(g, p, tsz, form):
             taken += wave_form(w)[2][1]
     need(sorted(taken) == list(range(0, KCK, 4)), f"{kernel}: k-steps of a chunk not taken once")
 
-    cover = out_coverage(kernel, g)
-    for mt in range(m_tiles):
+    pairs = sample_pairs(m_tiles, tiles)
+    cover = out_coverage(kernel, g) if len(pairs) == m_tiles * tiles else None
+    slots_of = {}
+    for mt, t in pairs:
         m0 = mt * BM
-        slots = a_slots(m0)
-        for t in range(tiles):
-            q0 = t * TS
-            qend = min(q0 + TS, Q)
-            qy0 = q0 // Qw
-            rows_need = tile_rows(q0, qend, Qw, S, Hf)
-            need(rows_need <= rows_max, f"{kernel}: tile {t} needs {rows_need} window rows")
-            ybase = qy0 * S - g["Ph"]
-            CHn = rows_need * Wpad
-            Ds = KC * CHn * dpe
-            NIs = cdiv(Ds, WAVE)
-            need(cdiv(NIs, 4) <= 12, f"{kernel}: window DMA needs {NIs} instructions, 48 offsets")
-            lds.access("src0", np.arange(NIs * WAVE * 4 // tsz), tsz, "window DMA")
-            # window cell of every staged element (chunk 0), as the DMA offsets give it
-            e = np.arange(Ds) // dpe
-            r = div_magic(e, Wpad, f"{kernel} window row")
-            x = e - r * Wpad
-            c = div_small(r, rows_need, f"{kernel} window channel")
-            cells = source_cell(dict(g, Cs=g["Cs"] + KC), c, ybase + r - c * rows_need, x - g["Pw"])
-            need(np.where(cells >= 0, cells * tsz + tsz <= INT_MAX, True), f"{kernel}: window voffset")
-            win = np.full(KC * CHn, -2, dtype=np.int64)
-            win[e] = cells
-            if pb:
-                model_dma_pooled_source(g, p, tsz, lds, kernel, KC, CHn, rows_need, ybase, win)
-            qx0 = q0 - qy0 * Qw
+        if mt not in slots_of:
+            slots_of = {mt: a_slots(m0)}
+        slots = slots_of[mt]
+        q0 = t * TS
+        qend = min(q0 + TS, Q)
+        qy0 = q0 // Qw
+        rows_need = tile_rows(q0, qend, Qw, S, Hf)
+        need(rows_need <= rows_max, f"{kernel}: tile {t} needs {rows_need} window rows")
+        ybase = qy0 * S - g["Ph"]
+        CHn = rows_need * Wpad
+        Ds = KC * CHn * dpe
+        NIs = cdiv(Ds, WAVE)
+        need(cdiv(NIs, 4) <= 12, f"{kernel}: window DMA needs {NIs} instructions, 48 offsets")
+        lds.access("src0", np.arange(NIs * WAVE * 4 // tsz), tsz, "window DMA")
+        # window cell of every staged element (chunk 0), as the DMA offsets give it
+        e = np.arange(Ds) // dpe
+        r = div_magic(e, Wpad, f"{kernel} window row")
+        x = e - r * Wpad
+        c = div_small(r, rows_need, f"{kernel} window channel")
+        cells = source_cell(dict(g, Cs=g["Cs"] + KC), c, ybase + r - c * rows_need, x - g["Pw"])
+        need(np.where(cells >= 0, cells * tsz + tsz <= INT_MAX, True), f"{kernel}: window voffset")
+        win = np.full(KC * CHn, -2, dtype=np.int64)
+        win[e] = cells
+        if pb:
+            model_dma_pooled_source(g, p, tsz, lds, kernel, KC, CHn, rows_need, ybase, win)
+        qx0 = q0 - qy0 * Qw
 
-            def pix_off(u):
-                v = qx0 + u
-                dy = div_magic(v, Qw, f"{kernel} pixel row")
-                return np.where(q0 + u < qend, dy * S * Wpad + (v - dy * Qw) * S, 0)
+        def pix_off(u):
+            v = qx0 + u
+            dy = div_magic(v, Qw, f"{kernel} pixel row")
+            return np.where(q0 + u < qend, dy * S * Wpad + (v - dy * Qw) * S, 0)
 
-            for w in range(4):
-                rows_blk, us, (reads, used) = wave_form(w)
-                offs = [pix_off(u) for u in us]
-                for kk in reads:
-                    kcol = kk + lq
-                    kc = np.minimum(kcol, KCv - 1)
-                    cc = div_magic(kc, HfWf, f"{kernel} tap channel")
-                    tp = kc - cc * HfWf
-                    ii = div_magic(tp, Wf, f"{kernel} tap row")
-                    ko = cc * CHn + ii * Wpad + (tp - ii * Wf)
-                    for rr in rows_blk:
-                        lds.access("a0", rr * SA + kcol, tsz, "filter fragment read")
-                    for off in offs:
-                        lds.access("src0", ko + off, tsz, "patch fragment read")
-                    if kk not in used:
-                        continue
-                    for c0 in sorted({c0s[0], c0s[-1]}):
-                        ach = a_chunk(slots, c0)
-                        for rr in rows_blk:
-                            ai = rr * SA + kcol
-                            a_val = np.where(ai < ach.size, ach[np.minimum(ai, ach.size - 1)], -2)
-                            for u, off in zip(us, offs):
-                                bcell = win[ko + off]
-                                b_val = np.where(bcell >= 0, bcell + c0 * plane, bcell)
-                                b_val = np.where(b_val >= Cs * plane, -1, b_val)
-                                check_operands(g, kernel, m0 + rr, c0 * HfWf + kcol, kcol < KCv,
-                                               a_val, np.where(q0 + u < qend, q0 + u, Q), b_val)
-            # epilogue buffers reuse the stages
-            if K4:
-                lds.region("partials", 0, p["lds_bytes"])
-                lds.access("partials", (3 * 64 + 16 * K4 - 1) * 32 + 31, tsz, "k-split partials")
-            if KS:
-                lds.region("handover", 0, p["lds_bytes"])
-                lds.access("handover", 1024 * NB - 1, tsz, "k-split hand-over")
-            for w in range(4):
-                wm, wn = w & 1, w >> 1
-                if KS and wm == 1:
+        for w in range(4):
+            rows_blk, us, (reads, used) = wave_form(w)
+            offs = [pix_off(u) for u in us]
+            for kk in reads:
+                kcol = kk + lq
+                kc = np.minimum(kcol, KCv - 1)
+                cc = div_magic(kc, HfWf, f"{kernel} tap channel")
+                tp = kc - cc * HfWf
+                ii = div_magic(tp, Wf, f"{kernel} tap row")
+                ko = cc * CHn + ii * Wpad + (tp - ii * Wf)
+                for rr in rows_blk:
+                    lds.access("a0", rr * SA + kcol, tsz, "filter fragment read")
+                for off in offs:
+                    lds.access("src0", ko + off, tsz, "patch fragment read")
+                if kk not in used:
                     continue
-                mbase = m0 + (0 if KS else wm * 32)
-                for x in range(2):
-                    for r4 in range(4):
-                        m = mbase + x * 16 + mfma_row(tsz, lane, r4)
-                        for y in range(NB):
-                            q = q0 + (wn * NB + y) * 16 + l16
-                            ok = (m < M) & (q < qend)
+                for c0 in sorted({c0s[0], c0s[-1]}):
+                    ach = a_chunk(slots, c0)
+                    for rr in rows_blk:
+                        ai = rr * SA + kcol
+                        a_val = np.where(ai < ach.size, ach[np.minimum(ai, ach.size - 1)], -2)
+                        for u, off in zip(us, offs):
+                            bcell = win[ko + off]
+                            b_val = np.where(bcell >= 0, bcell + c0 * plane, bcell)
+                            b_val = np.where(b_val >= Cs * plane, -1, b_val)
+                            check_operands(g, kernel, m0 + rr, c0 * HfWf + kcol, kcol < KCv,
+                                           a_val, np.where(q0 + u < qend, q0 + u, Q), b_val)
+        # epilogue buffers reuse the stages
+        if K4:
+            lds.region("partials", 0, p["lds_bytes"])
+            lds.access("partials", (3 * 64 + 16 * K4 - 1) * 32 + 31, tsz, "k-split partials")
+        if KS:
+            lds.region("handover", 0, p["lds_bytes"])
+            lds.access("handover", 1024 * NB - 1, tsz, "k-split hand-over")
+        for w in range(4):
+            wm, wn = w & 1, w >> 1
+            if KS and wm == 1:
+                continue
+            mbase = m0 + (0 if KS else wm * 32)
+            for x in range(2):
+                for r4 in range(4):
+                    m = mbase + x * 16 + mfma_row(tsz, lane, r4)
+                    for y in range(NB):
+                        q = q0 + (wn * NB + y) * 16 + l16
+                        ok = (m < M) & (q < qend)
+                        if cover:
                             cover.add((m * Q + q)[ok])
-            if pool:
-                model_pool_epilogue(g, p, tsz, lds, kernel, q0, qend, NB)
-    cover.check()
+        if pool:
+            model_pool_epilogue(g, p, tsz, lds, kernel, q0, qend, NB)
+    if cover:
+        cover.check()
 
 
 def model_dma_pooled_source(g, p, tsz, lds, kernel, KC, CHn, rows_need, ybase, win):
@@ -513,7 +543,8 @@ def model_igemm_reg(g, p, tsz, form):
     lane = np.arange(WAVE)
     lq, l16 = lane >> 4, lane & 15
     ncg = cdiv(Wpad, WAVE)
-    cover = out_coverage(kernel, g)
+    pairs = sample_pairs(m_tiles, tiles)
+    cover = out_coverage(kernel, g) if len(pairs) == m_tiles * tiles else None
     c0s = sorted({0, (Cs - 1) // KC * KC})
     # filter slice: element e = (m, kk) of the 64 x KCK slice goes to slot
     # e + e / KCK (pipelined) or m * SA + kk (direct)
@@ -527,65 +558,68 @@ def model_igemm_reg(g, p, tsz, form):
         sidx = m * SA + (e - m * KCK)
     kk = e - m * KCK
     lds.access("slice", sidx, tsz, "slice store")
-    for mt in range(m_tiles):
+    slot_mt = None
+    for mt, t in pairs:
         m0 = mt * BM
-        slot = {}
-        for c0 in c0s:
-            ok = (m0 + m < M) & (kk < KCv) & (c0 + kk // HfWf < Cs)
-            sl = np.full(BM * SA, -2, dtype=np.int64)
-            sl[sidx] = np.where(ok, a_element(g, np.minimum(m0 + m, M - 1),
-                                              np.minimum(c0 * HfWf + kk, Cs * HfWf - 1)), -1)
-            slot[c0] = sl
-        for t in range(tiles):
-            q0 = t * TS
-            qend = min(q0 + TS, Q)
-            qy0 = q0 // Qw
-            rows_need = tile_rows(q0, qend, Qw, S, Hf)
-            need(rows_need <= rows_max, f"{kernel}: tile {t} needs {rows_need} window rows")
-            ybase = qy0 * S - g["Ph"]
-            CHn = rows_need * Wpad
-            nrows = KC * rows_need
-            kv = np.arange(KCK)
-            c_, t_ = kv // HfWf, kv % HfWf
-            koff = np.where(kv < KCv, c_ * CHn + (t_ // Wf) * Wpad + t_ % Wf, 0)
-            lds.access("koff", kv, 4, "tap offsets")
-            if pipelined:
-                need(nrows * ncg <= 4 * 8, f"{kernel}: {nrows * ncg} window row slots, 32 staged")
-            rr = np.arange(nrows)[:, None]
-            u = np.arange(Wpad)[None, :]
-            lds.access("window", rr * Wpad + u, tsz, "window store")
-            if csr:
-                xlim = min(g["Sw"], Wpad - g["Pw"])
-                need(xlim - 1 + g["Pw"] < Wpad, f"{kernel}: CSR scatter past the staged row")
-            win = source_cell(dict(g, Cs=Cs + KC), rr // rows_need, ybase + rr % rows_need,
-                              u - g["Pw"]).ravel()
-            # all (wave, pixel block) lanes at once: q and lbase of shape (4 * NB, 64)
-            wv = np.repeat(np.arange(4), NB)[:, None]
-            yv = np.tile(np.arange(NB), 4)[:, None]
-            q = q0 + ((wv >> 1) * NB + yv) * 16 + l16
-            lb = np.where(q < qend, (q // Qw - qy0) * S * Wpad + (q % Qw) * S, 0)
-            for k4 in range(0, KCK, 4):
-                kcol = k4 + lq
-                bi = koff[kcol] + lb
-                lds.access("window", bi, tsz, "patch fragment read")
-                for half in (0, 16):
-                    rblk = (wv & 1) * 32 + half + l16
-                    ai = rblk * SA + kcol
-                    lds.access("slice", ai, tsz, "filter fragment read")
-                    for c0 in c0s:
-                        check_operands(g, kernel, m0 + rblk, c0 * HfWf + kcol, kcol < KCv,
-                                       slot[c0][ai], np.where(q < qend, q, Q),
-                                       shifted(win[bi], c0, plane, Cs * plane))
-            for w in range(4):
-                wm, wn = w & 1, w >> 1
-                for x in range(2):
-                    for r4 in range(4):
-                        mm = m0 + wm * 32 + x * 16 + mfma_row(tsz, lane, r4)
-                        for y in range(NB):
-                            qq = q0 + (wn * NB + y) * 16 + l16
-                            ok = (mm < M) & (qq < qend)
+        if slot_mt != mt:
+            slot_mt, slot = mt, {}
+            for c0 in c0s:
+                ok = (m0 + m < M) & (kk < KCv) & (c0 + kk // HfWf < Cs)
+                sl = np.full(BM * SA, -2, dtype=np.int64)
+                sl[sidx] = np.where(ok, a_element(g, np.minimum(m0 + m, M - 1),
+                                                  np.minimum(c0 * HfWf + kk, Cs * HfWf - 1)), -1)
+                slot[c0] = sl
+        q0 = t * TS
+        qend = min(q0 + TS, Q)
+        qy0 = q0 // Qw
+        rows_need = tile_rows(q0, qend, Qw, S, Hf)
+        need(rows_need <= rows_max, f"{kernel}: tile {t} needs {rows_need} window rows")
+        ybase = qy0 * S - g["Ph"]
+        CHn = rows_need * Wpad
+        nrows = KC * rows_need
+        kv = np.arange(KCK)
+        c_, t_ = kv // HfWf, kv % HfWf
+        koff = np.where(kv < KCv, c_ * CHn + (t_ // Wf) * Wpad + t_ % Wf, 0)
+        lds.access("koff", kv, 4, "tap offsets")
+        if pipelined:
+            need(nrows * ncg <= 4 * 8, f"{kernel}: {nrows * ncg} window row slots, 32 staged")
+        rr = np.arange(nrows)[:, None]
+        u = np.arange(Wpad)[None, :]
+        lds.access("window", rr * Wpad + u, tsz, "window store")
+        if csr:
+            xlim = min(g["Sw"], Wpad - g["Pw"])
+            need(xlim - 1 + g["Pw"] < Wpad, f"{kernel}: CSR scatter past the staged row")
+        win = source_cell(dict(g, Cs=Cs + KC), rr // rows_need, ybase + rr % rows_need,
+                          u - g["Pw"]).ravel()
+        # all (wave, pixel block) lanes at once: q and lbase of shape (4 * NB, 64)
+        wv = np.repeat(np.arange(4), NB)[:, None]
+        yv = np.tile(np.arange(NB), 4)[:, None]
+        q = q0 + ((wv >> 1) * NB + yv) * 16 + l16
+        lb = np.where(q < qend, (q // Qw - qy0) * S * Wpad + (q % Qw) * S, 0)
+        for k4 in range(0, KCK, 4):
+            kcol = k4 + lq
+            bi = koff[kcol] + lb
+            lds.access("window", bi, tsz, "patch fragment read")
+            for half in (0, 16):
+                rblk = (wv & 1) * 32 + half + l16
+                ai = rblk * SA + kcol
+                lds.access("slice", ai, tsz, "filter fragment read")
+                for c0 in c0s:
+                    check_operands(g, kernel, m0 + rblk, c0 * HfWf + kcol, kcol < KCv,
+                                   slot[c0][ai], np.where(q < qend, q, Q),
+                                   shifted(win[bi], c0, plane, Cs * plane))
+        for w in range(4):
+            wm, wn = w & 1, w >> 1
+            for x in range(2):
+                for r4 in range(4):
+                    mm = m0 + wm * 32 + x * 16 + mfma_row(tsz, lane, r4)
+                    for y in range(NB):
+                        qq = q0 + (wn * NB + y) * 16 + l16
+                        ok = (mm < M) & (qq < qend)
+                        if cover:
                             cover.add((mm * Q + qq)[ok])
-    cover.check()
+    if cover:
+        cover.check()
 
 
 # ==================================================== small-M vector kernel
@@ -606,7 +640,7 @@ def model_small_m(g, p, tsz, form):
     lds.disjoint("window", "filter")
     lds.region("reduction", 0, tsz * 16 * 64)
     lane = np.arange(64)
-    cover = out_coverage(kernel, g)
+    cover = out_coverage(kernel, g) if cdiv(Q, 64) <= MAX_TILES else None
     # every (channel, tap) of a chunk at once: arrays of shape (kc * HfWf, 64)
     for c0 in sorted({0, (Cs - 1) // KC * KC}):
         kc = min(KC, Cs - c0)
@@ -619,7 +653,7 @@ def model_small_m(g, p, tsz, form):
         kt = np.arange(kc * HfWf)[:, None]
         cc, tt = kt // HfWf, kt % HfWf
         ii, jj = tt // Wf, tt % Wf
-        for q0 in range(0, Q, 64):
+        for q0 in [64 * t for t in sample(cdiv(Q, 64))]:
             qend = min(q0 + 64, Q)
             qy0 = q0 // Qw
             rows = tile_rows(q0, qend, Qw, S, Hf)
@@ -653,8 +687,10 @@ def model_small_m(g, p, tsz, form):
             if c0 == 0:
                 for m_ in range(M):
                     lds.access("reduction", (3 * 4 + m_) * 64 + lane, tsz, "partial sums")
-                    cover.add((m_ * Q + q)[act])
-    cover.check()
+                    if cover:
+                        cover.add((m_ * Q + q)[act])
+    if cover:
+        cover.check()
 
 
 # =================================================== filter-resident forward
@@ -800,23 +836,25 @@ def wgrad_common(g, p, tsz, kernel, threads):
 
 
 def wgrad_outputs(g, p, tsz, kernel, ranges, NBW, nwaves, ws_elems):
-    """Partial dW / db stores of every split, and the split reduction's reads."""
+    """Partial dW / db stores of a split (the first and the last), and the
+    split reduction's reads: every (f, k) written once per split."""
     F, K = g["F"], g["K"]
     lane = np.arange(64)
+    w = np.arange(nwaves)[:, None, None, None, None]
+    mb = np.arange(4)[None, :, None, None, None]
+    nb = np.arange(NBW)[None, None, :, None, None]
+    r4 = np.arange(4)[None, None, None, :, None]
+    ln = lane[None, None, None, None, :]
     for split in sorted({0, p["splits"] - 1}):
         cover = Coverage(F * K, f"{kernel} partial dW of a split")
         for ft in range(cdiv(F, BM)):
+            f = ft * BM + mb * 16 + mfma_row(tsz, ln, r4)
             for kbeg, kend, _, _ in ranges:
-                for w in range(nwaves):
-                    for mb in range(4):
-                        for nb in range(NBW):
-                            for r4 in range(4):
-                                f = ft * BM + mb * 16 + mfma_row(tsz, lane, r4)
-                                k = kbeg + (w * NBW + nb) * 16 + (lane & 15)
-                                ok = (f < F) & (k < kend)
-                                idx = (f * K + k)[ok]
-                                glob(kernel, "workspace", split * F * K + idx, ws_elems)
-                                cover.add(idx)
+                k = kbeg + (w * NBW + nb) * 16 + (ln & 15)
+                ok = (f < F) & (k < kend)
+                idx = np.broadcast_to(f * K + k, ok.shape)[ok]
+                glob(kernel, "workspace", split * F * K + idx, ws_elems)
+                cover.add(idx)
         cover.check()
         glob(kernel, "workspace (db)", p["splits"] * F * K + split * F + np.arange(F), ws_elems)
 
@@ -969,7 +1007,13 @@ def model_wgrad_tiles(g, p, tsz, form):
     e = np.arange(BM * RQ)
     r = div_magic(e, RQ, f"{kernel} g row")
     lds.access("g", r * SG + e - r * RQ, tsz, "g tile store")
-    for t in range(tiles_per_img):
+    nr_ = len(ranges)
+    if tiles_per_img * nr_ <= MAX_TILES:
+        t_pick, r_pick = list(range(tiles_per_img)), list(range(nr_))
+    else:
+        r_pick = sample(nr_, min(nr_, 4))
+        t_pick = sample(tiles_per_img, max(MAX_TILES // len(r_pick), 8))
+    for t in t_pick:
         if spr:
             oh = t // spr
             ow0 = (t - oh * spr) * RQ
@@ -1022,7 +1066,7 @@ def model_wgrad_tiles(g, p, tsz, form):
                 qs = np.arange(q0, qend)
                 div_magic(qs // Wout, PS, f"{kernel} pooled-source row")
                 div_magic(qs % Wout, PS, f"{kernel} pooled-source column")
-        for kbeg, kend, c_lo, nch in ranges:
+        for kbeg, kend, c_lo, nch in [ranges[i] for i in r_pick]:
             tot_x = nch * CH
             e = np.arange(tot_x)
             if pipelined:

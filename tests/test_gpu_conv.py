@@ -366,3 +366,49 @@ def test_backward_filter_emits_masked_gradient(s, dt):
     ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, host(out), *a, s.F)
     assert_close(host(dW1), ref_dW, dt, "dW")
     assert_close(host(db1), ref_db, dt, "db")
+
+
+def test_images_of_2gib_register_path():
+    """The largest image class: a per-image X of 2.1 GB (fp64), beyond the 32-bit
+    byte offsets of the LDS-DMA kernels, takes the register-staged forward and
+    a row-sliced backward_filter; checked at sampled outputs against the
+    oracle's element functions (the full oracle would take hours)."""
+    s = ConvShape(1, 4096, 256, 256, 16, 3, 3, 1, 1)
+    assert s.C * s.Hin * s.Win * 8 >= 2 ** 31
+    assert dmlnn.conv2d_plan(torch.float64, "forward", *s.args())["kernel"] == "igemm_reg"
+    r = np.random.default_rng(2 ** 31)
+    X = np.maximum(r.standard_normal((1, s.C * s.Hin * s.Win)), 0.0)
+    W = r.standard_normal((s.F, s.K)) * np.sqrt(2.0 / s.K)
+    b = r.standard_normal(s.F) * 0.1
+    dout = r.standard_normal((1, s.F * s.Hout * s.Wout))
+    a = _args(s)
+    print(f"\n[gpu] 2 GiB image {s} f64", flush=True)
+    Xd = torch.from_numpy(X).cuda()
+    out, _, _ = dmlnn.conv2d_forward(Xd, dev(W, "f64"), dev(b, "f64"), *a, relu=True)
+    dW, db = dmlnn.conv2d_backward_filter(Xd, dev(dout, "f64"), out, *a, s.F)
+    dX = dmlnn.conv2d_backward_data(dev(W, "f64"), dev(dout, "f64"), out, *a)
+    torch.cuda.synchronize()
+    out_h, dW_h, db_h = host(out), host(dW), host(db)
+    pick = np.random.default_rng(7)
+    got, ref = [], []
+    for _ in range(96):
+        f, oh, ow = (int(pick.integers(v)) for v in (s.F, s.Hout, s.Wout))
+        got.append(out_h[0, (f * s.Hout + oh) * s.Wout + ow])
+        ref.append(max(oracle.conv2d_forward_pre_elem(X, W, b, *a, 0, f, oh, ow), 0.0))
+    assert_close(np.array(got), np.array(ref), "f64", "out (sampled)")
+    got, ref = [], []
+    for _ in range(24):
+        f, c, i, j = (int(pick.integers(v)) for v in (s.F, s.C, s.Hf, s.Wf))
+        got.append(dW_h[f, (c * s.Hf + i) * s.Wf + j])
+        ref.append(oracle.conv2d_backward_filter_elem(X, dout, out_h, 1, s.C, s.Hin, s.Win, s.F,
+                                                      s.Hf, s.Wf, s.stride, s.pad, f, c, i, j))
+    assert_close(np.array(got), np.array(ref), "f64", "dW (sampled)")
+    ref_db = [oracle.conv2d_backward_bias_elem(dout, out_h, 1, s.F, s.Hout, s.Wout, f)
+              for f in range(s.F)]
+    assert_close(db_h, np.array(ref_db), "f64", "db")
+    idx = [tuple(int(pick.integers(v)) for v in (s.C, s.Hin, s.Win)) for _ in range(96)]
+    flat = torch.tensor([(c * s.Hin + h) * s.Win + w for c, h, w in idx], device="cuda")
+    got = dX[0, flat].cpu().numpy()
+    ref = [oracle.conv2d_backward_data_elem(W, dout, out_h, s.C, s.Hin, s.Win, s.F, s.Hf, s.Wf,
+                                            s.stride, s.pad, 0, c, h, w) for c, h, w in idx]
+    assert_close(got, np.array(ref), "f64", "dX (sampled)")

@@ -260,8 +260,9 @@ DMLNN_API int conv2d_plan_fused(dmlnn_dtype dtype, int pass, int form, int pool_
  * operand a pass stages — X for DMLNN_PASS_FORWARD and
  * DMLNN_PASS_BACKWARD_FILTER, the gradient dout for DMLNN_PASS_BACKWARD_DATA —
  * for instance read back from count_nonzero, returns the zero-skip mode worth
- * setting with dmlnn_set_zero_skip: 1 when the pass's kernel has a skip form
- * and, with the zeros spread independently at that density, at least 5% of its
+ * setting with dmlnn_set_zero_skip: 1 when the kernel the pass takes in the
+ * dense mode has a skip form and, with the zeros spread independently at that
+ * density, at least 5% of its
  * 64-value input fragments are expected to be all zero ((1 - density)^64 >=
  * 0.05, i.e. density <= 4.6%); else 0.  Structured zeros (zero borders, dead
  * channels) skip more than this estimate: a caller that knows its data may set

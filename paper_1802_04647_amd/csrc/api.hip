@@ -340,7 +340,8 @@ static int plan_query(const char *name, dmlnn_dtype dtype, int pass, int form, i
     memset(plan, 0, sizeof(*plan));
     plan->kernel = info.kernel;
     plan->zero_skip = zero_skip && info.kernel != dmlnn::kConvSmallM &&
-                      info.kernel != dmlnn::kConvResident && form != DMLNN_FORM_POOLED_SOURCE;
+                      info.kernel != dmlnn::kConvResident &&
+                      info.kernel != dmlnn::kWgradPoolSparse && form != DMLNN_FORM_POOLED_SOURCE;
     plan->tile_m = info.tile_m;
     plan->tile_pixels = info.tile_pixels;
     plan->blocks = info.blocks;
@@ -391,9 +392,12 @@ int conv2d_zero_skip_choice(dmlnn_dtype dtype, int pass, long long nnz, int N, i
     const long long n = pass == DMLNN_PASS_BACKWARD_DATA ? (long long)N * F * d.Hout * d.Wout
                                                          : (long long)N * C * Hin * Win;
     if (nnz < 0 || nnz > n) return -1;
+    // the kernel the pass takes in the dense mode: when it has no skip form (the
+    // vector-ALU small-M kernel, the filter-resident forward), the skip mode
+    // would swap it for a different kernel, not skip its work
     dmlnn::ConvPlanInfo info;
-    if (dmlnn::conv_plan_info(dtype, pass, d, 1, 0, 0, 0, 0, 0, info) != hipSuccess) return -1;
-    if (info.kernel == dmlnn::kConvSmallM) return 0;  // no skip form
+    if (dmlnn::conv_plan_info(dtype, pass, d, 0, 0, 0, 0, 0, 0, info) != hipSuccess) return -1;
+    if (info.kernel == dmlnn::kConvSmallM || info.kernel == dmlnn::kConvResident) return 0;
     // expected share of all-zero 64-value fragments under independent zeros
     const double density = (double)nnz / (double)n;
     return pow(1.0 - density, 64.0) >= 0.05 ? 1 : 0;

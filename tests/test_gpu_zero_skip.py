@@ -142,23 +142,31 @@ def test_fused_pool_skip_matches_oracle(dt):
 def test_mode_chosen_from_count_nonzero():
     """The nnz-driven choice end to end: count the non-zeros of a 1%-dense
     LeNet-shaped input on the GPU, let the library's rule pick the mode from
-    that count (the skip), and run the forward pass in it against the oracle."""
+    that count, and run backward_filter (which stages X) in it against the
+    oracle; the forward (the LDS-DMA kernel here) takes the skip as well, and
+    a layer whose dense forward has no skip form (the filter-resident kernel of
+    LeNet conv2) stays dense."""
     from paper_1802_04647_amd.inputs import rng, sparse_uniform
     s = SHAPES["lenet_conv1"]
-    _, W, b, _ = conv_layer_inputs("lenet_conv1")
+    _, W, b, dout = conv_layer_inputs("lenet_conv1")
     X = sparse_uniform(rng(71), rng(72), (s.N, s.C * s.Hin * s.Win), keep=0.01)
     Xd = dev(X, "f64")
     nnz = int(dmlnn.count_nonzero(Xd).item())
     assert nnz == np.count_nonzero(X)
-    mode = dmlnn.conv2d_zero_skip_choice(torch.float64, "forward", nnz, *s.args())
+    assert dmlnn.conv2d_zero_skip_choice(torch.float64, "forward", nnz, *s.args()) == 1
+    assert dmlnn.conv2d_zero_skip_choice(torch.float64, "forward", 0,
+                                         *SHAPES["lenet_conv2"].args()) == 0
+    mode = dmlnn.conv2d_zero_skip_choice(torch.float64, "backward_filter", nnz, *s.args())
     assert mode == 1
-    dense = dmlnn.conv2d_zero_skip_choice(torch.float64, "forward", int(0.2 * X.size), *s.args())
+    dense = dmlnn.conv2d_zero_skip_choice(torch.float64, "backward_filter", int(0.2 * X.size),
+                                          *s.args())
     assert dense == 0
     prev = dmlnn.set_zero_skip(mode)
     try:
-        out, _, _ = dmlnn.conv2d_forward(Xd, dev(W, "f64"), dev(b, "f64"), *_args(s))
+        dW, db = dmlnn.conv2d_backward_filter(Xd, dev(dout, "f64"), None, *_args(s), s.F)
         torch.cuda.synchronize()
     finally:
         dmlnn.set_zero_skip(prev)
-    ref, _, _ = oracle.conv2d_forward(X, W, b, *_args(s), relu=True)
-    assert_close(host(out), ref, "f64", "forward")
+    ref_dW, ref_db = oracle.conv2d_backward_filter(X, dout, None, *_args(s), s.F)
+    assert_close(host(dW), ref_dW, "f64", "dW")
+    assert_close(host(db), ref_db, "f64", "db")

@@ -97,16 +97,21 @@ def test_plan_validation():
 
 
 def test_zero_skip_choice_follows_density():
-    s = SHAPES["lenet_conv1"]
+    s = SHAPES["resnet_conv"]
     n = s.N * s.C * s.Hin * s.Win
-    ch = lambda p, nnz: dmlnn.conv2d_zero_skip_choice(torch.float64, p, nnz, *s.args())  # noqa
-    assert ch("forward", int(0.2 * n)) == 0        # the config's 20% density: no fragment skips
+    ch = lambda p, nnz, s=s: dmlnn.conv2d_zero_skip_choice(torch.float64, p, nnz, *s.args())  # noqa
+    assert ch("forward", int(0.5 * n)) == 0        # the config's 50% density: no fragment skips
     assert ch("forward", int(0.01 * n)) == 1       # (0.99)^64 = 0.53 of fragments all zero
     assert ch("forward", 0) == 1
     assert ch("forward", int(0.045 * n)) == 1 and ch("forward", int(0.047 * n)) == 0
     assert ch("backward_filter", int(0.01 * n)) == 1
-    # backward_data of a one-channel layer runs the small-M kernel: no skip form
-    assert ch("backward_data", 0) == 0
+    # kernels with no skip form in the dense mode: never the skip mode
+    s1, s2 = SHAPES["lenet_conv1"], SHAPES["lenet_conv2"]
+    n1 = s1.N * s1.C * s1.Hin * s1.Win
+    assert ch("forward", 0, s1) == 1            # LDS-DMA forward: a skip form
+    assert ch("backward_data", 0, s1) == 0      # small-M vector backward_data (one channel)
+    assert ch("backward_filter", int(0.01 * n1), s1) == 1
+    assert ch("forward", 0, s2) == 0            # filter-resident forward
     with pytest.raises(ValueError):
         ch("forward", n + 1)
     with pytest.raises(ValueError):

@@ -542,11 +542,14 @@ def aux_kernel_timing():
     oa = torch.empty((64, 512), dtype=f64, device="cuda")
     dA, dWa, dba = torch.empty_like(A), torch.empty_like(Wa), torch.empty_like(ba)
     go = torch.randn((64, 512), dtype=f64, device="cuda", generator=g)
-    dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa)
-    for nm, fn, fl in (("affine_fwd", lambda: dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa),
+    wsa = torch.empty(dmlnn.affine_workspace_size(f64, 64, 3136, 512), dtype=torch.uint8,
+                      device="cuda")
+    dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa, workspace=wsa)
+    for nm, fn, fl in (("affine_fwd", lambda: dmlnn.affine_fwd(A, Wa, ba, relu=True, out=oa,
+                                                               workspace=wsa),
                         2 * 64 * 3136 * 512),
                        ("affine_bwd", lambda: dmlnn.affine_bwd(go, A, Wa, out_fwd=oa, dX=dA,
-                                                               dW=dWa, db=dba),
+                                                               dW=dWa, db=dba, workspace=wsa),
                         2 * 2 * 64 * 3136 * 512)):
         ms = _median_ms(fn)
         tf = fl / (ms / 1e3) / 1e12

@@ -392,19 +392,43 @@ DMLNN_API int conv2d_backward_data_pooled(dmlnn_dtype dtype, const void *W, cons
 
 /* ----------------------------------------------------------------- affine ----
  * Paper: Section 2 (the affine layer of the softmax-classifier example: the
- * product X W plus a bias row; its backward returns dX, dW, db in that order).  X is N x D, W is D x M, b is 1 x M, out is N x M.
- *   out = X W + b, then max(., 0) if relu.  b may be NULL. */
+ * product X W plus a bias row; its backward returns dX, dW, db in that order).
+ * X is N x D, W is D x M, b is 1 x M, out is N x M, all row-major.
+ *
+ * Workspace (both calls): optional.  Products too small to fill the GPU by
+ * their output tiles alone (few output rows and columns, a long reduction,
+ * e.g. a batch-64 forward with D = 3136, M = 512) split the reduction over
+ * blocks and add the partial products in a second, fixed-order pass; the
+ * partials need up to affine_workspace_size(...) bytes.  With NULL (or fewer
+ * bytes) the call splits less (at most what fits) and is still correct.  The
+ * result is deterministic for a given workspace size: the split count, and so
+ * the order of the additions, depends only on the sizes and workspace_bytes.
+ * The workspace must be element aligned and must not overlap the call's
+ * tensors (DMLNN_ERR_ARG); its contents on entry are ignored and on return are
+ * undefined.  Calls that may run at the same time need separate workspaces.
+ * Returns 0 for invalid arguments. */
+DMLNN_API size_t affine_workspace_size(dmlnn_dtype dtype, int N, int D, int M);
+
+/* out = X W + b, then max(., 0) if relu.  b may be NULL. */
 DMLNN_API int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
-               int N, int D, int M, int relu, void *stream);
+                         int N, int D, int M, int relu, void *workspace,
+                         size_t workspace_bytes, void *stream);
 
 /* g = dout (masked to out_fwd > 0 when out_fwd != NULL);
  *   dX = g W^T (N x D), dW = X^T g (D x M), db = column sums of g (1 x M).
+ * relu_input = 1 when X is the output of a relu: dX is then also multiplied
+ * by (X > 0), the relu backward of the layer below folded into the product
+ * (paper, Section "Future Work": vertical fusion across layers), so that
+ * layer's backward can take dX with out_fwd = NULL and read no mask; dX may
+ * then not overlap X.  relu_input = 0: dX as above.
  * Each output may be NULL (not computed), but not all three: the products are
  * independent, so a caller may compute them in separate calls on separate
- * streams.  DMLNN_ERR_NULL when dout, X or W is NULL or no output is given. */
+ * streams (each with its own workspace).  The products of one call run one
+ * after another on `stream` and share the workspace.  DMLNN_ERR_NULL when
+ * dout, X or W is NULL or no output is given. */
 DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W,
-               const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M,
-               void *stream);
+                         const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M,
+                         int relu_input, void *workspace, size_t workspace_bytes, void *stream);
 
 /* ----------------------------------------------------------- softmax_xent ----
  * Paper: Section 2 (the softmax-classifier example chains the softmax

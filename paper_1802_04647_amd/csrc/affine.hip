@@ -7,52 +7,39 @@
 //   forward  out = X W + b        (A = X,        B = W)
 //   dX = g W^T                    (A = g,        B = W viewed transposed)
 //   dW = X^T g                    (A = X viewed transposed, B = g)
-// where g = dout masked to out_fwd > 0 when a relu mask is given.  A block
-// owns a 16 x 16 output tile and up to 16 waves that split K (one MFMA per
-// 4-deep k-step); their partial tiles are added in wave order
-// (deterministic).  Column sums of g (db) use a separate fixed-order kernel.
+// where g = dout masked to out_fwd > 0 when a relu mask is given.  Column sums
+// of g (db) use a separate fixed-order kernel.
+#include <algorithm>
+
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace dmlnn {
 namespace {
 
-constexpr int kTJ = 16;      // output tile columns
-constexpr int kMaxKW = 16;   // waves splitting K inside a block
+constexpr int kMaxNK = 8;    // waves per block of the small-product kernel, each a k range
 
 struct GemmArgs {
     const void *A, *Amask;  // A(i,k) = A[i*sAm + k*sAk]; mask has the same strides
     const void *B, *Bmask;  // B(k,j) = B[k*sBk + j*sBn]
     const void *bias;       // per column j, or null
     void *C;                // C[i*ldc + j]
+    void *part;             // [splits][M][N] partial products when splits > 1
+    const void *xmask;      // C is zeroed where xmask[i*ldc + j] <= 0 (or null)
     long long sAm, sAk, sBk, sBn, ldc;
     int M, N, K, relu;
-    int kw_len;             // k per wave (a multiple of 16)
 };
 
-// A block owns a 16 x 16 output tile; its waves split K into contiguous
-// ranges of kw_len (a multiple of 16) and read their MFMA fragments straight
-// from global memory (the products here have at most a few MB of operands,
-// which stay in L2).
-//
-// k is walked in groups of 16 (four MFMA k-steps).  Inside a group the k
-// order is permuted so that an operand stored with k contiguous (X for the
-// forward product, g and W for dX) is read with 16-byte vector loads: lane
-// quarter q holds k = 2q, 2q+1, 8+2q, 9+2q of the group in its four steps
-// (fp64; for fp32 k = 4q..4q+3).  Each step still covers four distinct k, the
-// four steps cover the group, and both operands use the same order, so the
-// products are unchanged.  A 16-row fragment then reads 64 contiguous bytes
-// per row per load instead of 32, which halves the L1 cache accesses that
-// bound these loads.  Operands with rows contiguous keep per-step loads.
-//
-// These products are small, so a wave's time is load latency: groups are
-// loaded two at a time, one batch ahead (two register sets), so one batch's
-// loads are in flight while the previous batch's MFMAs issue.  Rows and
-// columns past the matrix edge read a clamped (valid) row or column; they only
-// feed outputs that are not stored.  A partial last group (K not a multiple
-// of 16) reads clamped k and zeroes B past the range.  A relu mask is loaded
-// beside its operand and applied just before the MFMA.  The per-wave partial
-// tiles are added in wave order (deterministic).
+// The k order of an MFMA fragment.  k is walked in groups of 16 (four MFMA
+// k-steps).  Inside a group the k order is permuted so that an operand stored
+// with k contiguous (X for the forward product, g and W for dX) is read with
+// 16-byte vector loads: lane quarter q holds k = 2q, 2q+1, 8+2q, 9+2q of the
+// group in its four steps (fp64; for fp32 k = 4q..4q+3).  Each step still
+// covers four distinct k, the four steps cover the group, and both operands
+// use the same order, so the products are unchanged.  A 16-row fragment then
+// reads 64 contiguous bytes per row per load instead of 32, which halves the
+// L1 cache accesses that bound these loads.  Operands with rows contiguous
+// keep per-step loads (16 lanes read one 16-element row piece).
 template <typename T>
 struct GemmFrag {
     // position in the group of k-step u for lane quarter q
@@ -81,105 +68,152 @@ struct GemmFrag {
     }
 };
 
-// Waves per block at most: the masked fp64 forms hold two register sets of
-// operands and masks, more than the 128 registers a 16-wave block leaves.
-template <typename T, bool MA, bool MB>
-constexpr int gemm_max_waves() { return (sizeof(T) == 8 && (MA || MB)) ? 8 : kMaxKW; }
-
-template <typename T, bool MA, bool MB, bool VA, bool VB>
-__global__ __launch_bounds__((gemm_max_waves<T, MA, MB>() * kWave)) void gemm_kernel(GemmArgs g)
+// A block owns one output tile of WT x WT MFMA tiles (16 x 16 each) and
+// `nk` waves; the waves of the tile's `splits` blocks walk contiguous,
+// balanced ranges of whole 16-k groups, in (block, wave) order, reading their
+// MFMA fragments straight from global memory.  WT = 2 (32 x 32 per wave: two
+// A and two B fragments feed four MFMAs per k-step) halves the operand
+// fetches per MFMA against WT = 1 for products with long K; WT = 1 keeps more
+// blocks for short K or a narrow output.  The waves of a block add their
+// partial tiles through LDS in wave order; with splits > 1 each block writes
+// its sum to its own slice of the workspace and a second kernel adds the
+// slices in split order, so the result is deterministic for a given split
+// count.  The products of a LeNet-sized step are too small to fill the GPU by
+// tiles alone (the 64 x 512 forward from K = 3136 has 32 tiles of 32 x 32):
+// the k split over blocks is what lets most CUs take part.
+//
+// These products are bound by the latency and the CU's fetch rate of their
+// operand loads, not by the matrix cores, so groups are loaded BATCH at a
+// time, one batch ahead (two register sets), so one batch's loads are in
+// flight while the previous batch's MFMAs issue.  Rows and columns past the
+// matrix edge read a clamped (valid) row or column; they only feed outputs
+// that are not stored.  A partial last group (K not a multiple of 16) reads
+// clamped k and zeroes both operands past K.  A relu mask is loaded beside its
+// operand and applied just before the MFMA.  With `xmask`, each output (i, j)
+// is multiplied by (xmask[i, j] > 0) before it is stored (the relu backward
+// of the layer below, folded into dX).
+template <typename T, bool MA, bool MB, bool VA, bool VB, int BATCH, int WT>
+__global__ __launch_bounds__(kMaxNK * kWave) void gemm_kernel(GemmArgs g)
 {
     using MF = Mfma<T>;
     using FR = GemmFrag<T>;
+    constexpr int TE = 16 * WT;  // tile edge
     extern __shared__ __align__(16) unsigned char smem[];
-    T *s_red = reinterpret_cast<T *>(smem);  // [wave][16 * kTJ]
+    T *s_red = reinterpret_cast<T *>(smem);  // [wave][TE * TE]
 
-    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-    const int nw = blockDim.x / kWave;
-    // Blocks are dealt to the 8 XCDs round-robin (block b to XCD b mod 8), and
-    // each XCD has its own L2.  Tile t = (ti, tj), ti fastest, is renumbered so
-    // that every XCD owns a contiguous run of tiles: the row tiles of a column
-    // strip then share one L2 copy of that strip of B (for the LeNet products
-    // B is a 12.8 MB weight matrix, larger than one L2).
-    const int ntile = gridDim.x * gridDim.y, bl = blockIdx.x + gridDim.x * blockIdx.y;
-    const int per = ntile / 8, rem = ntile % 8, xcd = bl % 8;
-    const int t = xcd * per + min(xcd, rem) + bl / 8;
-    const int i0 = (t % gridDim.x) * 16, j0 = (t / gridDim.x) * kTJ;
-    const int kbeg = wave * g.kw_len, kend = min(g.K, kbeg + g.kw_len);
-    const int ngrp = kend > kbeg ? (kend - kbeg + 15) / 16 : 0;
-    const bool ragged = ((kend - kbeg) & 15) != 0;  // the last group is partial
+    const int lane = lane_id(), wave = wave_id();
+    const int nk = blockDim.x / kWave;
+    const int tm = (g.M + TE - 1) / TE;
+    const int ntile = gridDim.x, splits = gridDim.y;
+    // Blocks are dealt to the 8 XCDs round-robin and each XCD has its own L2:
+    // renumber (tile, split), tile fastest with row tiles first, so that each
+    // XCD owns a contiguous run and the row tiles of a column strip share one
+    // L2 copy of that strip of B (for the LeNet forward a 12.8 MB weight).
+    const int t = xcd_logical_block(blockIdx.x + ntile * blockIdx.y, ntile * splits);
+    const int tile = t % ntile, split = t / ntile;
+    const int i0 = (tile % tm) * TE, j0 = (tile / tm) * TE;
+    const int G = (g.K + 15) / 16;
+    const long long R = (long long)splits * nk, r = (long long)split * nk + wave;
+    const int g_lo = (int)(r * G / R), g_hi = (int)((r + 1) * G / R);
+    const int ngrp = g_hi - g_lo;
+    const bool ragged = (g.K & 15) != 0 && g_hi == G;  // this range holds the partial group
     const T *A = reinterpret_cast<const T *>(g.A);
     const T *Am = reinterpret_cast<const T *>(g.Amask);
     const T *B = reinterpret_cast<const T *>(g.B);
     const T *Bm = reinterpret_cast<const T *>(g.Bmask);
     const int li = lane & 15, q = lane >> 4;
-    const long long arow = (long long)min(i0 + li, g.M - 1) * g.sAm;
-    const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
+    long long arow[WT], bcol[WT];
+#pragma unroll
+    for (int x = 0; x < WT; ++x) {
+        arow[x] = (long long)min(i0 + 16 * x + li, g.M - 1) * g.sAm;
+        bcol[x] = (long long)min(j0 + 16 * x + li, g.N - 1) * g.sBn;
+    }
 
     struct Grp {
-        T a[4], b[4];
-        T am[4], bm[4];  // used only with a mask (MA / MB)
+        T a[WT][4], b[WT][4];
+        T am[WT][4], bm[WT][4];  // used only with a mask (MA / MB)
     };
-    // one group of 16 k from k0; `part`: the wave's partial last group
+    // one group of 16 k from k0; `part`: the partial last group of K
     auto load_grp = [&](int k0, bool part, Grp &f) {
         if (part) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int k = k0 + FR::kpos(q, u), kc = min(k, kend - 1);
-                const long long oa = arow + (long long)kc * g.sAk;
-                const long long ob = (long long)kc * g.sBk + bcol;
-                f.a[u] = A[oa];
-                if (MA) f.am[u] = Am[oa];
-                const T bv = B[ob];
-                f.b[u] = k < kend ? bv : T(0);
-                if (MB) f.bm[u] = Bm[ob];
+                const int k = k0 + FR::kpos(q, u), kc = min(k, g.K - 1);
+                const bool in = k < g.K;
+#pragma unroll
+                for (int x = 0; x < WT; ++x) {
+                    const long long oa = arow[x] + (long long)kc * g.sAk;
+                    const T av = A[oa];
+                    f.a[x][u] = in ? av : T(0);
+                    if (MA) f.am[x][u] = Am[oa];
+                    const long long ob = (long long)kc * g.sBk + bcol[x];
+                    const T bv = B[ob];
+                    f.b[x][u] = in ? bv : T(0);
+                    if (MB) f.bm[x][u] = Bm[ob];
+                }
             }
             return;
         }
-        if constexpr (VA) {
-            FR::vload(A + arow + k0, q, f.a);
-            if constexpr (MA) FR::vload(Am + arow + k0, q, f.am);
-        } else {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const long long oa = arow + (long long)(k0 + FR::kpos(q, u)) * g.sAk;
-                f.a[u] = A[oa];
-                if (MA) f.am[u] = Am[oa];
+        for (int x = 0; x < WT; ++x) {
+            if constexpr (VA) {
+                FR::vload(A + arow[x] + k0, q, f.a[x]);
+                if constexpr (MA) FR::vload(Am + arow[x] + k0, q, f.am[x]);
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const long long oa = arow[x] + (long long)(k0 + FR::kpos(q, u)) * g.sAk;
+                    f.a[x][u] = A[oa];
+                    if (MA) f.am[x][u] = Am[oa];
+                }
             }
-        }
-        if constexpr (VB) {
-            FR::vload(B + bcol + k0, q, f.b);
-            if constexpr (MB) FR::vload(Bm + bcol + k0, q, f.bm);
-        } else {
+            if constexpr (VB) {
+                FR::vload(B + bcol[x] + k0, q, f.b[x]);
+                if constexpr (MB) FR::vload(Bm + bcol[x] + k0, q, f.bm[x]);
+            } else {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const long long ob = (long long)(k0 + FR::kpos(q, u)) * g.sBk + bcol;
-                f.b[u] = B[ob];
-                if (MB) f.bm[u] = Bm[ob];
+                for (int u = 0; u < 4; ++u) {
+                    const long long ob = (long long)(k0 + FR::kpos(q, u)) * g.sBk + bcol[x];
+                    f.b[x][u] = B[ob];
+                    if (MB) f.bm[x][u] = Bm[ob];
+                }
             }
         }
     };
-    typename MF::acc_t acc = MF::zero();
+    typename MF::acc_t acc[WT][WT];
+#pragma unroll
+    for (int x = 0; x < WT; ++x)
+#pragma unroll
+        for (int y = 0; y < WT; ++y) acc[x][y] = MF::zero();
     auto mma_grp = [&](const Grp &f) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const T av = MA ? (f.am[u] > T(0) ? f.a[u] : T(0)) : f.a[u];
-            const T bv = MB ? (f.bm[u] > T(0) ? f.b[u] : T(0)) : f.b[u];
-            acc = MF::mma(av, bv, acc);
+            T av[WT], bv[WT];
+#pragma unroll
+            for (int x = 0; x < WT; ++x) {
+                av[x] = MA ? (f.am[x][u] > T(0) ? f.a[x][u] : T(0)) : f.a[x][u];
+                bv[x] = MB ? (f.bm[x][u] > T(0) ? f.b[x][u] : T(0)) : f.b[x][u];
+            }
+#pragma unroll
+            for (int x = 0; x < WT; ++x)
+#pragma unroll
+                for (int y = 0; y < WT; ++y) acc[x][y] = MF::mma(av[x], bv[y], acc[x][y]);
         }
     };
-    // batch b = groups 2b and 2b + 1 (the second may not exist)
-    auto load_batch = [&](int b, Grp (&f)[2]) {
-        const int g0 = 2 * b;
-        load_grp(kbeg + 16 * g0, ragged && g0 == ngrp - 1, f[0]);
-        if (g0 + 1 < ngrp) load_grp(kbeg + 16 * g0 + 16, ragged && g0 + 1 == ngrp - 1, f[1]);
+    auto load_batch = [&](int b, Grp (&f)[BATCH]) {
+#pragma unroll
+        for (int c = 0; c < BATCH; ++c) {
+            const int gi = b * BATCH + c;
+            if (gi < ngrp) load_grp((g_lo + gi) * 16, ragged && gi == ngrp - 1, f[c]);
+        }
     };
-    auto mma_batch = [&](int b, const Grp (&f)[2]) {
-        mma_grp(f[0]);
-        if (2 * b + 1 < ngrp) mma_grp(f[1]);
+    auto mma_batch = [&](int b, const Grp (&f)[BATCH]) {
+#pragma unroll
+        for (int c = 0; c < BATCH; ++c)
+            if (b * BATCH + c < ngrp) mma_grp(f[c]);
     };
-    const int nbatch = (ngrp + 1) / 2;
-    Grp f0[2], f1[2];
+    const int nbatch = (ngrp + BATCH - 1) / BATCH;
+    Grp f0[BATCH], f1[BATCH];
     if (nbatch > 0) load_batch(0, f0);
     int i = 0;
     for (; i + 1 < nbatch; i += 2) {
@@ -191,163 +225,63 @@ __global__ __launch_bounds__((gemm_max_waves<T, MA, MB>() * kWave)) void gemm_ke
     if (i < nbatch) mma_batch(i, f0);
 
     T *C = reinterpret_cast<T *>(g.C);
+    T *P = reinterpret_cast<T *>(g.part);
     const T *bias = reinterpret_cast<const T *>(g.bias);
-    if (nw == 1) {  // one wave: no partial tiles to add
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int ii = i0 + MF::row(lane, r), j = j0 + li;
-            if (ii < g.M && j < g.N) {
-                T v = acc[r];
-                if (bias) v += bias[j];
-                C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
-            }
+    const T *xm = reinterpret_cast<const T *>(g.xmask);
+    auto store = [&](int ii, int j, T v) {
+        if (ii >= g.M || j >= g.N) return;
+        if (splits == 1) {
+            if (bias) v += bias[j];
+            v = relu_if(v, g.relu);
+            if (xm && !(xm[(long long)ii * g.ldc + j] > T(0))) v = T(0);
+            C[(long long)ii * g.ldc + j] = v;
+        } else {
+            P[((long long)split * g.M + ii) * g.N + j] = v;
         }
+    };
+    if (nk == 1) {  // one wave: no partial tiles to add
+#pragma unroll
+        for (int x = 0; x < WT; ++x)
+#pragma unroll
+            for (int y = 0; y < WT; ++y)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    store(i0 + 16 * x + MF::row(lane, rr), j0 + 16 * y + li, acc[x][y][rr]);
         return;
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) s_red[wave * 16 * kTJ + MF::row(lane, r) * kTJ + li] = acc[r];
+    for (int x = 0; x < WT; ++x)
+#pragma unroll
+        for (int y = 0; y < WT; ++y)
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                s_red[wave * TE * TE + (16 * x + MF::row(lane, rr)) * TE + 16 * y + li] =
+                    acc[x][y][rr];
     __syncthreads();
-    for (int e = tid; e < 16 * kTJ; e += blockDim.x) {
-        const int ii = i0 + e / kTJ, j = j0 + e % kTJ;
-        if (ii < g.M && j < g.N) {
-            T v = s_red[e];
-            for (int w = 1; w < nw; ++w) v += s_red[w * 16 * kTJ + e];
-            if (bias) v += bias[j];
-            C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
-        }
+    for (int e = threadIdx.x; e < TE * TE; e += blockDim.x) {
+        T v = s_red[e];
+        for (int w = 1; w < nk; ++w) v += s_red[w * TE * TE + e];
+        store(i0 + e / TE, j0 + e % TE, v);
     }
 }
 
-// Products with a moderate K and many columns (the LeNet dX = g W^T: 64 x 3136
-// from K = 512): the 16 x K strip of A (masked) is staged in LDS once per
-// block, and the block's four waves each stream their own 16 columns of B
-// over the whole K.  Splitting K across waves instead (above) makes every
-// 16-column tile re-read A and its mask from L2: for dX that is 100 MB of
-// 32-byte row pieces, and the L1 throughput on those pieces bounds the time.
-// k is walked in the same permuted 16-groups as above (A from LDS at the
-// permuted positions, B with 16-byte loads when k-contiguous), four groups
-// per batch, loaded one batch ahead.  Each column block has two waves, one
-// per half of the k groups, so twice as many B loads are in flight per CU
-// (the product has too few tiles for more than one block per CU); the second
-// half's partial tile is added to the first's through LDS (fixed order).
-constexpr int kLdsACols = 4;                 // 16-column blocks per block
-constexpr int kLdsAWaves = 2 * kLdsACols;    // two k halves each
-constexpr int kLdsAMaxK = 1024;
-
-template <typename T, bool MA, bool VB>
-__global__ __launch_bounds__(kLdsAWaves * kWave) void gemm_lds_a_kernel(GemmArgs g)
+// C = act(sum over splits of the partial products + bias), splits added in
+// order; zero where xmask (if given) is not positive.
+template <typename T>
+__global__ __launch_bounds__(256) void gemm_split_reduce(const T *part, const T *bias,
+                                                         const T *xmask, T *C, int M, int N,
+                                                         long long ldc, int splits, int relu)
 {
-    using MF = Mfma<T>;
-    using FR = GemmFrag<T>;
-    extern __shared__ __align__(16) unsigned char smem[];
-    T *s_a = reinterpret_cast<T *>(smem);  // [16][SK], k past K zero
-
-    const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-    const int ntile = gridDim.x * gridDim.y, bl = blockIdx.x + gridDim.x * blockIdx.y;
-    const int per = ntile / 8, rem = ntile % 8, xcd = bl % 8;
-    const int t = xcd * per + min(xcd, rem) + bl / 8;
-    const int i0 = (t % gridDim.x) * 16;
-    const int cb = wave % kLdsACols, kh = wave / kLdsACols;  // column block, k half
-    const int j0 = (t / gridDim.x) * (16 * kLdsACols) + 16 * cb;
-    const int K16 = (g.K + 15) / 16 * 16;
-    const int SK = K16 + 2;  // 2 mod 4
-    const T *A = reinterpret_cast<const T *>(g.A);
-    const T *Am = reinterpret_cast<const T *>(g.Amask);
-    const T *B = reinterpret_cast<const T *>(g.B);
-
-    // Stage A: element (r, k) at s_a[r * SK + k].  With k contiguous in memory
-    // consecutive threads take consecutive k, else consecutive rows.  Eight
-    // branch-free loads per thread before any store (clamped rows and k).
-    const bool kfast = g.sAk == 1;
-    const int tot = 16 * K16;
-    for (int base = 0; base < tot; base += 8 * kLdsAWaves * kWave) {
-        T v[8], mv[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int e = min(base + u * kLdsAWaves * kWave + tid, tot - 1);
-            const int r = kfast ? e / K16 : e % 16, k = kfast ? e % K16 : e / 16;
-            const long long o = (long long)min(i0 + r, g.M - 1) * g.sAm +
-                                (long long)min(k, g.K - 1) * g.sAk;
-            v[u] = A[o];
-            mv[u] = MA ? Am[o] : T(1);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int e = base + u * kLdsAWaves * kWave + tid;
-            if (e < tot) {
-                const int r = kfast ? e / K16 : e % 16, k = kfast ? e % K16 : e / 16;
-                s_a[r * SK + k] = (k < g.K && mv[u] > T(0)) ? v[u] : T(0);
-            }
-        }
-    }
-    __syncthreads();
-
-    const int li = lane & 15, q = lane >> 4;
-    const long long bcol = (long long)min(j0 + li, g.N - 1) * g.sBn;
-    const T *arow = s_a + li * SK;
-    constexpr int kG = 4;  // groups per batch
-    // this wave's groups: [g_lo, g_hi) of the K16 / 16
-    const int ngrp_all = K16 / 16, nh = (ngrp_all + 1) / 2;
-    const int g_lo = kh ? nh : 0, g_hi = kh ? ngrp_all : nh;
-    const int ngrp = g_hi - g_lo, nbatch = (ngrp + kG - 1) / kG;
-    auto load_b = [&](int b, T (&f)[kG][4]) {
-#pragma unroll
-        for (int gg = 0; gg < kG; ++gg) {
-            const int k0 = (g_lo + min(b * kG + gg, max(ngrp - 1, 0))) * 16;
-            if (VB && k0 + 16 <= g.K) {
-                FR::vload(B + bcol + k0, q, f[gg]);
-            } else {
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int k = k0 + FR::kpos(q, u);
-                    const T bv = B[(long long)min(k, g.K - 1) * g.sBk + bcol];
-                    f[gg][u] = k < g.K ? bv : T(0);
-                }
-            }
-        }
-    };
-    typename MF::acc_t acc = MF::zero();
-    auto mma_b = [&](int b, const T (&f)[kG][4]) {
-#pragma unroll
-        for (int gg = 0; gg < kG; ++gg) {
-            if (b * kG + gg >= ngrp) break;
-            const int k0 = (g_lo + b * kG + gg) * 16;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) acc = MF::mma(arow[k0 + FR::kpos(q, u)], f[gg][u], acc);
-        }
-    };
-    T f0[kG][4], f1[kG][4];
-    if (nbatch > 0) load_b(0, f0);
-    int b = 0;
-    for (; b + 1 < nbatch; b += 2) {
-        load_b(b + 1, f1);
-        mma_b(b, f0);
-        if (b + 2 < nbatch) load_b(b + 2, f0);
-        mma_b(b + 1, f1);
-    }
-    if (b < nbatch) mma_b(b, f0);
-
-    // the second k half hands its partial tile to the first (past the A strip)
-    T *s_red = s_a + 16 * SK;  // [kLdsACols][4][64]
-    if (kh == 1)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) s_red[(cb * 4 + r) * kWave + lane] = acc[r];
-    __syncthreads();
-    if (kh == 1) return;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] += s_red[(cb * 4 + r) * kWave + lane];
-
-    T *C = reinterpret_cast<T *>(g.C);
-    const T *bias = reinterpret_cast<const T *>(g.bias);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int ii = i0 + MF::row(lane, r), j = j0 + li;
-        if (ii < g.M && j < g.N) {
-            T v = acc[r];
-            if (bias) v += bias[j];
-            C[(long long)ii * g.ldc + j] = relu_if(v, g.relu);
-        }
-    }
+    const long long MN = (long long)M * N;
+    const long long e = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (e >= MN) return;
+    const int ii = (int)(e / N), j = (int)(e - (long long)ii * N);
+    T v = part[e];
+    for (int s = 1; s < splits; ++s) v += part[s * MN + e];
+    if (bias) v += bias[j];
+    v = relu_if(v, relu);
+    if (xmask && !(xmask[(long long)ii * ldc + j] > T(0))) v = T(0);
+    C[(long long)ii * ldc + j] = v;
 }
 
 // db[j] = sum_i g[i, j], g masked by out_fwd > 0 if given.  A block covers 16
@@ -385,55 +319,99 @@ bool vec_ok(const void *p, long long s_row, long long s_k)
     return s_k == 1 && s_row % e == 0 && reinterpret_cast<uintptr_t>(p) % 16 == 0;
 }
 
-template <typename T, bool MA, bool MB>
+template <typename T, bool MA, bool MB, int BATCH, int WT>
 auto pick_gemm(bool va, bool vb)
 {
-    return va ? (vb ? gemm_kernel<T, MA, MB, true, true> : gemm_kernel<T, MA, MB, true, false>)
-              : (vb ? gemm_kernel<T, MA, MB, false, true> : gemm_kernel<T, MA, MB, false, false>);
+    return va ? (vb ? gemm_kernel<T, MA, MB, true, true, BATCH, WT>
+                    : gemm_kernel<T, MA, MB, true, false, BATCH, WT>)
+              : (vb ? gemm_kernel<T, MA, MB, false, true, BATCH, WT>
+                    : gemm_kernel<T, MA, MB, false, false, BATCH, WT>);
 }
 
-// Waves per block: enough that each walks about 16 k-steps (two batches), at
-// most 16; the per-wave k range is a multiple of 16.
+template <typename T, int WT>
+auto pick_masked(const GemmArgs &g, bool va, bool vb)
+{
+    // fp64 with a mask holds one group per batch (registers); the rest two
+    constexpr int BM = sizeof(T) == 8 ? 1 : 2;
+    return g.Amask ? pick_gemm<T, true, false, BM, WT>(va, vb)
+                   : (g.Bmask ? pick_gemm<T, false, true, BM, WT>(va, vb)
+                              : pick_gemm<T, false, false, 2, WT>(va, vb));
+}
+
+}  // namespace
+
+// Tile, waves per block and block k splits of an M x N x K product.
+//   wt: 32 x 32 tiles (wt = 2) when both output edges are 32 or more and K
+//       has four 16-k groups or more; else 16 x 16;
+//   nk: up to 8 waves per tile while the tiles alone give fewer than 2048
+//       waves (eight per CU), two groups or more each;
+//   splits: only when a wave would otherwise walk more than 8 groups and the
+//       grid is still short of 2048 waves: about four groups per wave, at most
+//       what the workspace holds (splits x M x N elements).
+GemmPlan gemm_plan(int M, int N, int K, size_t elem, size_t workspace_bytes)
+{
+    GemmPlan p;
+    const long long G = (K + 15) / 16;
+    p.wt = (M >= 32 && N >= 32 && G >= 4) ? 2 : 1;
+    const int te = 16 * p.wt;
+    const long long tiles = (long long)((M + te - 1) / te) * ((N + te - 1) / te);
+    const long long want = 2048;
+    long long nk = std::min<long long>(kMaxNK, std::max<long long>(1, G / 2));
+    nk = std::max<long long>(1, std::min(nk, (want + tiles - 1) / tiles));
+    long long s = 1;
+    if (G > 8 * nk && tiles * nk < want) {
+        s = std::min((G + 4 * nk - 1) / (4 * nk), (want + tiles * nk - 1) / (tiles * nk));
+        const long long fit = (long long)(workspace_bytes / ((size_t)M * N * elem));
+        s = std::min(std::min(s, fit), 65535LL);
+        if (s < 2) s = 1;
+    }
+    p.nk = (int)nk;
+    p.splits = (int)s;
+    p.workspace_bytes = s > 1 ? (size_t)s * M * N * elem : 0;
+    return p;
+}
+
+namespace {
+
 template <typename T>
-hipError_t gemm(GemmArgs g, hipStream_t s)
+hipError_t gemm(GemmArgs g, void *workspace, size_t workspace_bytes, hipStream_t s)
 {
     if (g.Amask && g.Bmask) return hipErrorInvalidValue;  // one masked operand at most
-    // A strip in LDS: K up to 1024, no mask on B, and enough 16 x 64 tiles
-    const long long tiles64 = (long long)((g.M + 15) / 16) * ((g.N + 63) / 64);
-    if (!g.Bmask && g.K <= kLdsAMaxK && g.K >= 64 && tiles64 >= 128) {
-        const bool vb = vec_ok<T>(g.B, g.sBn, g.sBk);
-        auto k = g.Amask ? (vb ? gemm_lds_a_kernel<T, true, true> : gemm_lds_a_kernel<T, true, false>)
-                         : (vb ? gemm_lds_a_kernel<T, false, true> : gemm_lds_a_kernel<T, false, false>);
-        const size_t lds = sizeof(T) * (16 * ((size_t)(g.K + 15) / 16 * 16 + 2) +
-                                         (size_t)kLdsACols * 4 * kWave);
-        hipError_t e = allow_dynamic_lds(k, lds);
-        if (e != hipSuccess) return e;
-        dim3 grid((g.M + 15) / 16, (g.N + 16 * kLdsACols - 1) / (16 * kLdsACols));
-        hipLaunchKernelGGL(k, grid, dim3(kLdsAWaves * kWave), lds, s, g);
-        return hipGetLastError();
-    }
-    const int grps = (g.K + 15) / 16;
-    const int max_w = g.Amask ? gemm_max_waves<T, true, false>()
-                              : (g.Bmask ? gemm_max_waves<T, false, true>() : kMaxKW);
-    int nw = (grps + 3) / 4;
-    nw = nw < 1 ? 1 : (nw > max_w ? max_w : nw);
-    g.kw_len = ((grps + nw - 1) / nw) * 16;
+    const GemmPlan p = gemm_plan(g.M, g.N, g.K, sizeof(T), workspace ? workspace_bytes : 0);
+    g.part = p.splits > 1 ? workspace : nullptr;
     const bool va = vec_ok<T>(g.A, g.sAm, g.sAk) && (!g.Amask || vec_ok<T>(g.Amask, g.sAm, g.sAk));
     const bool vb = vec_ok<T>(g.B, g.sBn, g.sBk) && (!g.Bmask || vec_ok<T>(g.Bmask, g.sBn, g.sBk));
-    const size_t lds = nw > 1 ? (size_t)nw * 16 * kTJ * sizeof(T) : 0;
-    auto k = g.Amask ? pick_gemm<T, true, false>(va, vb)
-                     : (g.Bmask ? pick_gemm<T, false, true>(va, vb) : pick_gemm<T, false, false>(va, vb));
+    auto k = p.wt == 2 ? pick_masked<T, 2>(g, va, vb) : pick_masked<T, 1>(g, va, vb);
+    const int te = 16 * p.wt;
+    const size_t lds = p.nk > 1 ? (size_t)p.nk * te * te * sizeof(T) : 0;
     hipError_t e = allow_dynamic_lds(k, lds);
     if (e != hipSuccess) return e;
-    dim3 grid((g.M + 15) / 16, (g.N + kTJ - 1) / kTJ);
-    hipLaunchKernelGGL(k, grid, dim3(nw * kWave), lds, s, g);
+    const int tiles = ((g.M + te - 1) / te) * ((g.N + te - 1) / te);
+    hipLaunchKernelGGL(k, dim3(tiles, p.splits), dim3(p.nk * kWave), lds, s, g);
+    if ((e = hipGetLastError()) != hipSuccess || p.splits == 1) return e;
+    const long long MN = (long long)g.M * g.N;
+    hipLaunchKernelGGL(gemm_split_reduce<T>, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s,
+                       reinterpret_cast<const T *>(g.part), reinterpret_cast<const T *>(g.bias),
+                       reinterpret_cast<const T *>(g.xmask), reinterpret_cast<T *>(g.C), g.M,
+                       g.N, g.ldc, p.splits, g.relu);
     return hipGetLastError();
 }
 
 }  // namespace
 
+size_t affine_workspace_bytes(int dtype, int N, int D, int M)
+{
+    const size_t el = dtype == 0 ? 8 : 4;
+    const size_t big = ~(size_t)0;
+    size_t w = gemm_plan(N, M, D, el, big).workspace_bytes;                  // out = X W
+    w = std::max(w, gemm_plan(N, D, M, el, big).workspace_bytes);            // dX = g W^T
+    w = std::max(w, gemm_plan(D, M, N, el, big).workspace_bytes);            // dW = X^T g
+    return w;
+}
+
 hipError_t launch_affine_fwd(int dtype, const void *X, const void *W, const void *b, void *out,
-                             int N, int D, int M, int relu, hipStream_t s)
+                             int N, int D, int M, int relu, void *workspace,
+                             size_t workspace_bytes, hipStream_t s)
 {
     GemmArgs g = {};
     g.A = X;
@@ -449,16 +427,19 @@ hipError_t launch_affine_fwd(int dtype, const void *X, const void *W, const void
     g.N = M;
     g.K = D;
     g.relu = relu;
-    return dtype == 0 ? gemm<double>(g, s) : gemm<float>(g, s);
+    return dtype == 0 ? gemm<double>(g, workspace, workspace_bytes, s)
+                      : gemm<float>(g, workspace, workspace_bytes, s);
 }
 
 hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const void *W,
                              const void *out_fwd, void *dX, void *dW, void *db, int N, int D,
-                             int M, hipStream_t s)
+                             int M, int relu_input, void *workspace, size_t workspace_bytes,
+                             hipStream_t s)
 {
     hipError_t e;
-    if (dX) {  // dX[n, d] = sum_m g[n, m] W[d, m]
+    if (dX) {  // dX[n, d] = sum_m g[n, m] W[d, m]  (times X[n, d] > 0 with relu_input)
         GemmArgs g = {};
+        g.xmask = relu_input ? X : nullptr;
         g.A = dout;
         g.Amask = out_fwd;
         g.sAm = M;
@@ -471,7 +452,8 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
         g.M = N;
         g.N = D;
         g.K = M;
-        e = dtype == 0 ? gemm<double>(g, s) : gemm<float>(g, s);
+        e = dtype == 0 ? gemm<double>(g, workspace, workspace_bytes, s)
+                       : gemm<float>(g, workspace, workspace_bytes, s);
         if (e != hipSuccess) return e;
     }
     if (dW) {  // dW[d, m] = sum_n X[n, d] g[n, m]
@@ -488,7 +470,8 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
         g.M = D;
         g.N = M;
         g.K = N;
-        e = dtype == 0 ? gemm<double>(g, s) : gemm<float>(g, s);
+        e = dtype == 0 ? gemm<double>(g, workspace, workspace_bytes, s)
+                       : gemm<float>(g, workspace, workspace_bytes, s);
         if (e != hipSuccess) return e;
     }
     if (db) {

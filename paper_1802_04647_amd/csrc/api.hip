@@ -9,6 +9,8 @@
 #include <cstdlib>
 #include <cmath>
 #include <cstdint>
+#include <initializer_list>
+#include <utility>
 #include <cstring>
 #include <mutex>
 
@@ -648,29 +650,68 @@ int conv2d_backward_data_pooled(dmlnn_dtype dtype, const void *W, const void *dp
                     name);
 }
 
+size_t affine_workspace_size(dmlnn_dtype dtype, int N, int D, int M)
+{
+    if (!dtype_ok(dtype) || !count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M)) return 0;
+    return dmlnn::affine_workspace_bytes(dtype, N, D, M);
+}
+
+// An affine workspace is optional; when given it must be element aligned and
+// must not overlap the tensors the call reads or writes.
+static int affine_workspace_ok(const char *name, dmlnn_dtype dtype, void *ws, size_t ws_bytes,
+                               std::initializer_list<std::pair<const void *, size_t>> tensors)
+{
+    if (!ws || ws_bytes == 0) return DMLNN_OK;
+    const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
+    if ((uintptr_t)ws % esz) return fail(DMLNN_ERR_ARG, "%s: workspace is not element aligned", name);
+    for (const auto &t : tensors)
+        if (t.first && overlaps(ws, ws_bytes, t.first, t.second))
+            return fail(DMLNN_ERR_ARG, "%s: workspace overlaps a tensor of the call", name);
+    return DMLNN_OK;
+}
+
 int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out, int N,
-               int D, int M, int relu, void *stream)
+               int D, int M, int relu, void *workspace, size_t workspace_bytes, void *stream)
 {
     if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_fwd: bad dtype %d", (int)dtype);
     if (!X || !W || !out) return fail(DMLNN_ERR_NULL, "affine_fwd: X, W and out are required");
     if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M))
         return fail(DMLNN_ERR_ARG, "affine_fwd: bad sizes N=%d D=%d M=%d", N, D, M);
     if (relu != 0 && relu != 1) return fail(DMLNN_ERR_ARG, "affine_fwd: relu must be 0 or 1");
+    const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
+    if (int r = affine_workspace_ok("affine_fwd", dtype, workspace, workspace_bytes,
+                                    {{X, (size_t)N * D * esz}, {W, (size_t)D * M * esz},
+                                     {b, (size_t)M * esz}, {out, (size_t)N * M * esz}}))
+        return r;
     if (int r = device_check()) return r;
-    return launched(dmlnn::launch_affine_fwd(dtype, X, W, b, out, N, D, M, relu, (hipStream_t)stream),
+    return launched(dmlnn::launch_affine_fwd(dtype, X, W, b, out, N, D, M, relu, workspace,
+                                             workspace_bytes, (hipStream_t)stream),
                     "affine_fwd");
 }
 
 int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W,
-               const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M, void *stream)
+               const void *out_fwd, void *dX, void *dW, void *db, int N, int D, int M,
+               int relu_input, void *workspace, size_t workspace_bytes, void *stream)
 {
     if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_bwd: bad dtype %d", (int)dtype);
     if (!dout || !X || !W) return fail(DMLNN_ERR_NULL, "affine_bwd: dout, X and W are required");
     if (!dX && !dW && !db) return fail(DMLNN_ERR_NULL, "affine_bwd: no output (dX, dW, db all NULL)");
     if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M))
         return fail(DMLNN_ERR_ARG, "affine_bwd: bad sizes N=%d D=%d M=%d", N, D, M);
+    if (relu_input != 0 && relu_input != 1)
+        return fail(DMLNN_ERR_ARG, "affine_bwd: relu_input must be 0 or 1");
+    const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
+    if (int r = affine_workspace_ok("affine_bwd", dtype, workspace, workspace_bytes,
+                                    {{dout, (size_t)N * M * esz}, {X, (size_t)N * D * esz},
+                                     {W, (size_t)D * M * esz}, {out_fwd, (size_t)N * M * esz},
+                                     {dX, (size_t)N * D * esz}, {dW, (size_t)D * M * esz},
+                                     {db, (size_t)M * esz}}))
+        return r;
+    if (dX && relu_input && overlaps(dX, (size_t)N * D * esz, X, (size_t)N * D * esz))
+        return fail(DMLNN_ERR_ARG, "affine_bwd: with relu_input, dX may not overlap X");
     if (int r = device_check()) return r;
     return launched(dmlnn::launch_affine_bwd(dtype, dout, X, W, out_fwd, dX, dW, db, N, D, M,
+                                             relu_input, workspace, workspace_bytes,
                                              (hipStream_t)stream),
                     "affine_bwd");
 }

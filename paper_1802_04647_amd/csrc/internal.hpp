@@ -104,11 +104,24 @@ hipError_t launch_max_pool_bwd(int dtype, const void *dout, const int32_t *argma
                                const void *pooled, void *dX, int N, int C, int Hin, int Win,
                                int Hf, int Wf, int stride, int pad, int Hout, int Wout,
                                hipStream_t s);
+// Launch shape of one affine product C (M x N) = A (M x K) B (K x N): the
+// output tile of a block (wt x wt tiles of 16 x 16), the waves splitting its
+// k range, and the block k splits, whose partial products take
+// splits x M x N elements of workspace when splits > 1.
+struct GemmPlan {
+    int wt = 1, nk = 1, splits = 1;
+    size_t workspace_bytes = 0;
+};
+GemmPlan gemm_plan(int M, int N, int K, size_t elem, size_t workspace_bytes);
+// The largest workspace any of the affine layer's three products splits into.
+size_t affine_workspace_bytes(int dtype, int N, int D, int M);
 hipError_t launch_affine_fwd(int dtype, const void *X, const void *W, const void *b, void *out,
-                             int N, int D, int M, int relu, hipStream_t s);
+                             int N, int D, int M, int relu, void *workspace,
+                             size_t workspace_bytes, hipStream_t s);
 hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const void *W,
                              const void *out_fwd, void *dX, void *dW, void *db, int N, int D,
-                             int M, hipStream_t s);
+                             int M, int relu_input, void *workspace, size_t workspace_bytes,
+                             hipStream_t s);
 hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
                                void *loss, int N, int K, hipStream_t s);
 hipError_t launch_softmax(int dtype, const void *S, void *P, int N, int K, hipStream_t s);

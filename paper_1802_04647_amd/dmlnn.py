@@ -85,8 +85,10 @@ def load():
         "bias_add_relu": (_i, [_i, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
         "max_pool2d_fwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "max_pool2d_bwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
-        "affine_fwd": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 4 + [_vp]),
-        "affine_bwd": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 3 + [_vp]),
+        "affine_workspace_size": (ctypes.c_size_t, [_i] * 4),
+        "affine_fwd": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 4 + [_vp, ctypes.c_size_t, _vp]),
+        "affine_bwd": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 4
+                       + [_vp, ctypes.c_size_t, _vp]),
         "softmax_xent": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _vp]),
         "sgd_momentum_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_longlong, _vp]),
@@ -527,7 +529,23 @@ def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, 
     return dX
 
 
-def affine_fwd(X, W, b, relu=False, out=None):
+def affine_workspace_size(dtype, N, D, M) -> int:
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return int(load().affine_workspace_size(dt, N, D, M))
+
+
+def _affine_ws(X, N, D, M, workspace):
+    """The caller's workspace (None: a fresh one of the full size; an empty
+    tensor: none, the products run unsplit) as (pointer, bytes)."""
+    if workspace is None:
+        nb = affine_workspace_size(X.dtype, N, D, M)
+        workspace = torch.empty(nb, dtype=torch.uint8, device=X.device) if nb else None
+    if workspace is None or workspace.numel() == 0:
+        return None, 0
+    return _p(workspace), workspace.numel() * workspace.element_size()
+
+
+def affine_fwd(X, W, b, relu=False, out=None, workspace=None):
     dt = _dtype(X, W, b, out)
     N, D = X.shape
     M = W.shape[1]
@@ -536,14 +554,16 @@ def affine_fwd(X, W, b, relu=False, out=None):
     _need(W, D * M, "W")
     _need(b, M, "b")
     _need(out, N * M, "out")
+    ws, nb = _affine_ws(X, N, D, M, workspace)
     _check("affine_fwd", load().affine_fwd(dt, _p(X), _p(W), _p(b), _p(out), N, D, M,
-                                            int(bool(relu)), _stream()))
+                                            int(bool(relu)), ws, nb, _stream()))
     return out
 
 
 def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW=None, db=None,
-               want_dW=True):
-    """Returns [dX, dW, db] (each None when not wanted)."""
+               want_dW=True, workspace=None, relu_input=False):
+    """Returns [dX, dW, db] (each None when not wanted).  relu_input: dX is
+    also multiplied by (X > 0) (X is a relu output)."""
     dt = _dtype(dout, X, W, out_fwd, dX, dW, db)
     N, D = X.shape
     M = W.shape[1]
@@ -559,8 +579,10 @@ def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW
     _need(dX, N * D, "dX")
     _need(dW, D * M, "dW")
     _need(db, M, "db")
+    ws, nb = _affine_ws(X, N, D, M, workspace) if (dX is not None or dW is not None) else (None, 0)
     _check("affine_bwd", load().affine_bwd(dt, _p(dout), _p(X), _p(W), _p(out_fwd), _p(dX),
-                                            _p(dW), _p(db), N, D, M, _stream()))
+                                            _p(dW), _p(db), N, D, M, int(bool(relu_input)), ws,
+                                            nb, _stream()))
     return dX, dW, db
 
 

@@ -10,8 +10,8 @@ take the pool's gradient, argmax and pooled values directly (the relu mask and
 the pool routing built while staging), so neither the conv outputs nor their
 gradients are ever stored.
 
-All activations, gradients and the backward-filter workspaces are allocated
-once; ``step`` only enqueues library calls (about twenty launches, one of them
+All activations, gradients and the workspaces (backward-filter partials,
+affine split partials) are allocated once; ``step`` only enqueues library calls (about twenty launches, one of them
 the optimizer update over the flat parameter buffer) on the current stream and,
 for the weight gradients of affine 1 and conv2, on a second stream that joins
 the current one before the step returns; it returns the loss as a device
@@ -67,6 +67,12 @@ class LeNetTrainer:
         ws2 = dmlnn.conv2d_backward_filter_workspace_size(dtype, N, 32, 14, 14, 64, 5, 5, 1, 2)
         self.ws1 = torch.empty(ws1, dtype=torch.uint8, device=device)
         self.ws2 = torch.empty(ws2, dtype=torch.uint8, device=device)
+        # split-reduction partials of the affine products: one buffer for the
+        # current stream's products, one for the second stream's (affine 1 dW)
+        wa = max(dmlnn.affine_workspace_size(dtype, N, 3136, 512),
+                 dmlnn.affine_workspace_size(dtype, N, 512, 10))
+        self.wsa = torch.empty(wa, dtype=torch.uint8, device=device)
+        self.wsa_side = torch.empty(wa, dtype=torch.uint8, device=device)
         # The weight gradients of affine 1 and conv2 run on a second stream
         # (default priority), beside the data-gradient chain (affine 1 dX, pool
         # backward, conv2 backward_data, ...): they only share read-only inputs,
@@ -80,19 +86,22 @@ class LeNetTrainer:
                                   pooled=self.p1, argmax=self.i1)
         dmlnn.conv2d_forward_pool(self.p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, 2, 2, 2, 0,
                                   pooled=self.p2, argmax=self.i2)
-        dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h)
-        dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s)
+        dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h, workspace=self.wsa)
+        dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s, workspace=self.wsa)
         dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds)
-        dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"])
+        # dh comes out masked by h > 0 (the relu backward of affine 1, folded
+        # into this product), so affine 1's backward reads no mask
+        dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"],
+                         workspace=self.wsa, relu_input=True)
         main = torch.cuda.current_stream()
         side = self.side if self.two_streams else main
         if side is not main:
             side.wait_stream(main)  # dh is ready
         with torch.cuda.stream(side):
-            dmlnn.affine_bwd(self.dh, self.p2, p["W3"], self.h, want_dX=False, dW=g["W3"],
-                             db=g["b3"])
-        dmlnn.affine_bwd(self.dh, self.p2, p["W3"], self.h, dX=self.dp2, want_dW=False,
-                         want_db=False)
+            dmlnn.affine_bwd(self.dh, self.p2, p["W3"], None, want_dX=False, dW=g["W3"],
+                             db=g["b3"], workspace=self.wsa_side)
+        dmlnn.affine_bwd(self.dh, self.p2, p["W3"], None, dX=self.dp2, want_dW=False,
+                         want_db=False, workspace=self.wsa)
         if self.fused_pool_backward:
             if side is not main:
                 side.wait_stream(main)  # dp2 is ready
@@ -184,9 +193,13 @@ class LeNetScorer:
         e = lambda *s: torch.empty(*s, **kw)  # noqa: E731
         i32 = lambda *s: torch.empty(*s, dtype=torch.int32, device=device)  # noqa: E731
         B = batch
+        wa = max(dmlnn.affine_workspace_size(dtype, B, 3136, 512),
+                 dmlnn.affine_workspace_size(dtype, B, 512, 10))
         self.buf = [dict(p1=e(B, 32 * 196), i1=i32(B, 32 * 196),
                          p2=e(B, 64 * 49), i2=i32(B, 64 * 49),
-                         h=e(B, 512), s=e(B, 10)) for _ in range(streams)]
+                         h=e(B, 512), s=e(B, 10),
+                         ws=torch.empty(wa, dtype=torch.uint8, device=device))
+                    for _ in range(streams)]
 
     def _forward(self, X, out, b):
         p = self.p
@@ -194,8 +207,8 @@ class LeNetScorer:
                                   pooled=b["p1"], argmax=b["i1"])
         dmlnn.conv2d_forward_pool(b["p1"], p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, 2, 2, 2, 0,
                                   pooled=b["p2"], argmax=b["i2"])
-        dmlnn.affine_fwd(b["p2"], p["W3"], p["b3"], relu=True, out=b["h"])
-        dmlnn.affine_fwd(b["h"], p["W4"], p["b4"], relu=False, out=b["s"])
+        dmlnn.affine_fwd(b["p2"], p["W3"], p["b3"], relu=True, out=b["h"], workspace=b["ws"])
+        dmlnn.affine_fwd(b["h"], p["W4"], p["b4"], relu=False, out=b["s"], workspace=b["ws"])
         dmlnn.softmax_fwd(b["s"], probs=out)
 
     def score(self, X):

@@ -24,6 +24,7 @@ def test_exports_every_declared_symbol(lib):
     expected = {"conv2d_out_dim", "conv2d_forward", "conv2d_backward_filter_workspace_size",
                 "conv2d_backward_filter", "conv2d_backward_data", "dmlnn_set_zero_skip",
                 "bias_add_relu", "max_pool2d_fwd", "max_pool2d_bwd", "affine_fwd", "affine_bwd",
+                "affine_workspace_size",
                 "softmax_xent", "sgd_momentum_update", "count_nonzero", "dmlnn_last_error"}
     assert expected <= set(names)
     for n in names:
@@ -106,12 +107,38 @@ def test_other_validation(lib):
     assert lib.max_pool2d_fwd(0, FAKE, FAKE, None, 1, 1, 4, 4, 2, 2, 2, 0, None) == ERR_NULL
     assert lib.max_pool2d_fwd(0, FAKE, FAKE, FAKE, 1, 1, 4, 4, 2, 2, 2, 2, None) == ERR_ARG
     assert lib.max_pool2d_bwd(1, FAKE, FAKE, FAKE, 1, 1, 4, 4, 2, 2, 0, 0, None) == ERR_ARG
-    assert lib.affine_fwd(0, FAKE, FAKE, None, FAKE, 0, 3, 4, 0, None) == ERR_ARG
-    assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, None, None, None, 2, 3, 4, None) == ERR_NULL
-    assert lib.affine_bwd(0, None, FAKE, FAKE, None, FAKE, FAKE, None, 2, 3, 4, None) == ERR_NULL
+    assert lib.affine_fwd(0, FAKE, FAKE, None, FAKE, 0, 3, 4, 0, None, 0, None) == ERR_ARG
+    assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, None, None, None, 2, 3, 4, 0, None, 0,
+                          None) == ERR_NULL
+    assert lib.affine_bwd(0, None, FAKE, FAKE, None, FAKE, FAKE, None, 2, 3, 4, 0, None, 0,
+                          None) == ERR_NULL
     assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None) == ERR_NULL
     assert lib.sgd_momentum_update(0, FAKE, FAKE, FAKE, 0.1, 0.9, 0, None) == ERR_ARG
     assert lib.count_nonzero(3, FAKE, 10, FAKE, None) == ERR_DTYPE
+
+
+def test_affine_workspace(lib):
+    """The split-reduction workspace: sized from the products that split (the
+    batch-64 3136 -> 512 forward: seven splits of 64 x 512 partials), none for
+    products whose tiles fill the GPU, and a workspace that is misaligned or
+    overlaps a tensor of the call is rejected before anything runs."""
+    assert lib.affine_workspace_size(0, 64, 3136, 512) == 7 * 64 * 512 * 8
+    assert lib.affine_workspace_size(1, 64, 3136, 512) == 7 * 64 * 512 * 4
+    assert lib.affine_workspace_size(0, 64, 512, 10) == 0
+    assert lib.affine_workspace_size(0, 0, 3, 4) == 0
+    assert lib.affine_workspace_size(4, 2, 3, 4) == 0
+    X, W, out, ws = 0x100000, 0x200000, 0x300000, 0x400000
+    assert lib.affine_fwd(0, X, W, None, out, 2, 3, 4, 0, ws + 4, 64, None) == ERR_ARG
+    assert lib.affine_fwd(0, X, W, None, out, 2, 3, 4, 0, out - 32, 64, None) == ERR_ARG
+    assert lib.affine_bwd(0, X, W, out, None, ws, None, None, 2, 3, 4, 0, ws + 8, 64,
+                          None) == ERR_ARG
+    assert "workspace" in dmlnn.last_error()
+    # relu_input: a flag, and dX may not overlap the X it is masked by
+    assert lib.affine_bwd(0, X, W, out, None, ws, None, None, 2, 3, 4, 2, None, 0,
+                          None) == ERR_ARG
+    assert lib.affine_bwd(0, X, W, out, None, W + 8, None, None, 2, 3, 4, 1, None, 0,
+                          None) == ERR_ARG
+    assert "relu_input" in dmlnn.last_error()
 
 
 def test_zero_skip_mode(lib):
@@ -144,7 +171,8 @@ def test_affine_bwd_accepts_any_single_output(lib):
     # the device check (no GPU here) stops the call.
     _skip_on_gpu_host()
     for outs in ((FAKE, None, None), (None, FAKE, None), (None, None, FAKE)):
-        assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, *outs, 2, 3, 4, None) == ERR_DEVICE
+        assert lib.affine_bwd(0, FAKE, FAKE, FAKE, None, *outs, 2, 3, 4, 0, None, 0,
+                              None) == ERR_DEVICE
 
 
 def test_binding_rejects_host_tensors():

@@ -120,6 +120,69 @@ def test_affine_parity(shape, dt):
     assert dWj is not None and torch.equal(dXs, dXj) and torch.equal(dbs, dbj)
 
 
+# products whose reduction splits over blocks: the batch-64 3136 -> 512 forward
+# (32 x 32 tiles, seven splits), a dX from K = 3000 and a 17 x 20 forward from
+# K = 4099 (16 x 16 tiles, nine splits, a partial last 16-group)
+SPLIT = [(64, 3136, 512), (48, 300, 3000), (17, 4099, 20)]
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("shape", SPLIT, ids=str)
+def test_affine_split_workspace(shape, dt):
+    """The full workspace, a workspace for two splits and none all match the
+    oracle; each is bitwise reproducible run to run (the split count, and so
+    the order of the additions, depends only on the sizes and the workspace
+    size)."""
+    N, D, M = shape
+    print(f"\n[gpu] affine split {shape} {dt}", flush=True)
+    g = rng(45)
+    X = rounded(np.maximum(g.standard_normal((N, D)), 0.0), dt)
+    W = rounded(g.standard_normal((D, M)) * np.sqrt(2.0 / D), dt)
+    b = rounded(g.standard_normal(M) * 0.1, dt)
+    dout = rounded(g.standard_normal((N, M)), dt)
+    tdt = torch.float64 if dt == "f64" else torch.float32
+    full = dmlnn.affine_workspace_size(tdt, N, D, M)
+    assert full > 0
+    ref_out = oracle.affine_fwd(X, W, b, relu=True)
+    mask = rounded(ref_out, dt)
+    rdX, rdW, rdb = oracle.affine_bwd(dout, X, W, mask)
+    esz = 8 if dt == "f64" else 4
+    for nb in (full, 2 * max(N * M, N * D) * esz, 0):
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        runs = []
+        for _ in range(2):
+            out = dmlnn.affine_fwd(dev(X, dt), dev(W, dt), dev(b, dt), relu=True, workspace=ws)
+            dX, dW, db = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), dev(mask, dt),
+                                          workspace=ws)
+            runs.append((out, dX, dW, db))
+        assert_close(host(runs[0][0]), ref_out, dt, f"affine out ws={nb}")
+        assert_close(host(runs[0][1]), rdX, dt, f"affine dX ws={nb}")
+        assert_close(host(runs[0][2]), rdW, dt, f"affine dW ws={nb}")
+        assert_close(host(runs[0][3]), rdb, dt, f"affine db ws={nb}")
+        for a, c in zip(*runs):
+            assert torch.equal(a, c)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("shape", [(64, 512, 10), (64, 3136, 512), (33, 70, 65), (5, 7, 3)],
+                         ids=str)
+def test_affine_relu_input(shape, dt):
+    """relu_input folds the relu backward of the layer below into dX: dX times
+    (X > 0), X a relu output with exact zeros; dW and db are unchanged."""
+    N, D, M = shape
+    print(f"\n[gpu] affine relu_input {shape} {dt}", flush=True)
+    g = rng(46)
+    X = rounded(np.maximum(g.standard_normal((N, D)), 0.0), dt)
+    W = rounded(g.standard_normal((D, M)) * np.sqrt(2.0 / D), dt)
+    dout = rounded(g.standard_normal((N, M)), dt)
+    rdX, rdW, rdb = oracle.affine_bwd(dout, X, W, None)
+    dX, dW, db = dmlnn.affine_bwd(dev(dout, dt), dev(X, dt), dev(W, dt), None, relu_input=True)
+    assert_close(host(dX), rdX * (X > 0), dt, "affine dX relu_input")
+    assert_close(host(dW), rdW, dt, "affine dW")
+    assert_close(host(db), rdb, dt, "affine db")
+    assert np.all(host(dX)[X == 0] == 0)
+
+
 @pytest.mark.parametrize("dt", ["f64", "f32"])
 def test_affine_misaligned_operands_bitwise(dt):
     # Operands whose rows are not 16-byte aligned take per-element loads instead

@@ -167,8 +167,13 @@ def _need(t, n, name):
         raise ValueError(f"{name} has {t.numel()} elements, the call needs {n}")
 
 
-def _stream():
-    return torch.cuda.current_stream().cuda_stream
+def _stream(stream=None):
+    """The HIP stream a call is enqueued on: `stream` (a torch.cuda.Stream) when
+    given, else the current stream.  Every call takes an optional stream=, so a
+    caller that switches streams per call need not enter a stream context."""
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream
 
 
 def _empty(shape, like, dtype=None):
@@ -230,7 +235,7 @@ def conv2d_zero_skip_choice(dtype, pass_name, nnz, N, C, Hin, Win, F, Hf, Wf, st
 
 
 # ------------------------------------------------------------------------- conv2d
-def conv2d_forward(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True, out=None):
+def conv2d_forward(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True, out=None, stream=None):
     """out = relu(conv2d(X, W) + b): N x (F*Hout*Wout).  Returns (out, Hout, Wout)."""
     dt = _dtype(X, W, b, out)
     N, F = X.shape[0], W.shape[0]
@@ -243,7 +248,7 @@ def conv2d_forward(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True, out=Non
     _need(out, N * F * max(Hout, 0) * max(Wout, 0), "out")
     _check("conv2d_forward", load().conv2d_forward(
         dt, _p(X), _p(W), _p(b), _p(out), N, C, Hin, Win, F, Hf, Wf, stride, pad,
-        int(bool(relu)), _stream()))
+        int(bool(relu)), _stream(stream)))
     return out, Hout, Wout
 
 
@@ -254,7 +259,8 @@ def conv2d_backward_filter_workspace_size(dtype, N, C, Hin, Win, F, Hf, Wf, stri
 
 
 def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F,
-                           want_db=True, workspace=None, dW=None, db=None, g_out=None):
+                           want_db=True, workspace=None, dW=None, db=None, g_out=None,
+                           stream=None):
     """Returns (dW F x C*Hf*Wf, db F or None); out_fwd None means no relu mask.
     With g_out (an N x F*Hout*Wout buffer, possibly dout itself) the masked
     gradient is written there too (conv2d_backward_filter_emit), ready to be
@@ -279,15 +285,16 @@ def conv2d_backward_filter(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F
         _check("conv2d_backward_filter_emit", load().conv2d_backward_filter_emit(
             dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), _p(g_out), N, C, Hin, Win, F, Hf,
             Wf, stride, pad, _p(workspace), workspace.numel() * workspace.element_size(),
-            _stream()))
+            _stream(stream)))
         return dW, db
     _check("conv2d_backward_filter", load().conv2d_backward_filter(
         dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
-        stride, pad, _p(workspace), workspace.numel() * workspace.element_size(), _stream()))
+        stride, pad, _p(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
     return dW, db
 
 
-def conv2d_backward_filter_noalloc(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F, dW, db=None):
+def conv2d_backward_filter_noalloc(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, F, dW,
+                                   db=None, stream=None):
     """conv2d_backward_filter with the library's own device scratch instead of a
     workspace: allocates nothing (dW, and db if wanted, are supplied)."""
     dt = _dtype(X, dout, out_fwd, dW, db)
@@ -300,7 +307,7 @@ def conv2d_backward_filter_noalloc(X, dout, out_fwd, C, Hin, Win, Hf, Wf, stride
     _need(db, F, "db")
     _check("conv2d_backward_filter_noalloc", load().conv2d_backward_filter_noalloc(
         dt, _p(X), _p(dout), _p(out_fwd), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf, stride, pad,
-        _stream()))
+        _stream(stream)))
     return dW, db
 
 
@@ -311,7 +318,7 @@ def _pool_out(Hout, Wout, pool_h, pool_w, pool_stride, pool_pad):
 
 def conv2d_backward_filter_pooled(X, dpool, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, F,
                                   pool_h, pool_w, pool_stride, pool_pad, want_db=True,
-                                  workspace=None, dW=None, db=None):
+                                  workspace=None, dW=None, db=None, stream=None):
     """Filter and bias gradients of conv -> relu -> max-pool from the pool's
     upstream gradient (dpool), argmax and pooled values.  Returns (dW, db)."""
     dt = _dtype(X, dpool, pooled, dW, db)
@@ -335,12 +342,12 @@ def conv2d_backward_filter_pooled(X, dpool, argmax, pooled, C, Hin, Win, Hf, Wf,
     _check("conv2d_backward_filter_pooled", load().conv2d_backward_filter_pooled(
         dt, _p(X), _p(dpool), _p(argmax), _p(pooled), _p(dW), _p(db), N, C, Hin, Win, F, Hf, Wf,
         stride, pad, pool_h, pool_w, pool_stride, pool_pad, _p(workspace),
-        workspace.numel() * workspace.element_size(), _stream()))
+        workspace.numel() * workspace.element_size(), _stream(stream)))
     return dW, db
 
 
 def conv2d_backward_data_pooled(W, dpool, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad,
-                                pool_h, pool_w, pool_stride, pool_pad, dX=None):
+                                pool_h, pool_w, pool_stride, pool_pad, dX=None, stream=None):
     """Input gradient of conv -> relu -> max-pool from the pool's upstream
     gradient (dpool), argmax and pooled values: N x C*Hin*Win."""
     dt = _dtype(W, dpool, pooled, dX)
@@ -357,11 +364,11 @@ def conv2d_backward_data_pooled(W, dpool, argmax, pooled, C, Hin, Win, Hf, Wf, s
     _need(dX, N * C * Hin * Win, "dX")
     _check("conv2d_backward_data_pooled", load().conv2d_backward_data_pooled(
         dt, _p(W), _p(dpool), _p(argmax), _p(pooled), _p(dX), N, C, Hin, Win, F, Hf, Wf, stride,
-        pad, pool_h, pool_w, pool_stride, pool_pad, _stream()))
+        pad, pool_h, pool_w, pool_stride, pool_pad, _stream(stream)))
     return dX
 
 
-def conv2d_backward_data(W, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+def conv2d_backward_data(W, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, dX=None, stream=None):
     """Returns dX, N x (C*Hin*Win)."""
     dt = _dtype(W, dout, out_fwd, dX)
     N, F = dout.shape[0], W.shape[0]
@@ -374,12 +381,12 @@ def conv2d_backward_data(W, dout, out_fwd, C, Hin, Win, Hf, Wf, stride, pad, dX=
     _need(dX, N * C * Hin * Win, "dX")
     _check("conv2d_backward_data", load().conv2d_backward_data(
         dt, _p(W), _p(dout), _p(out_fwd), _p(dX), N, C, Hin, Win, F, Hf, Wf, stride, pad,
-        _stream()))
+        _stream(stream)))
     return dX
 
 
 # -------------------------------------------------------------------------- others
-def bias_add_relu(X, b, C, HW, relu=True, out=None):
+def bias_add_relu(X, b, C, HW, relu=True, out=None, stream=None):
     dt = _dtype(X, b, out)
     if out is None:
         out = torch.empty_like(X)
@@ -387,11 +394,11 @@ def bias_add_relu(X, b, C, HW, relu=True, out=None):
     _need(b, C, "b")
     _need(out, X.numel(), "out")
     _check("bias_add_relu", load().bias_add_relu(dt, _p(X), _p(b), _p(out), X.shape[0], C, HW,
-                                                  int(bool(relu)), _stream()))
+                                                  int(bool(relu)), _stream(stream)))
     return out
 
 
-def max_pool2d_fwd(X, C, Hin, Win, Hf, Wf, stride, pad, out=None, argmax=None):
+def max_pool2d_fwd(X, C, Hin, Win, Hf, Wf, stride, pad, out=None, argmax=None, stream=None):
     """Returns (out, argmax int32, Hout, Wout)."""
     dt = _dtype(X, out)
     N = X.shape[0]
@@ -405,11 +412,11 @@ def max_pool2d_fwd(X, C, Hin, Win, Hf, Wf, stride, pad, out=None, argmax=None):
     _need(out, N * cols, "out")
     _need(argmax, N * cols, "argmax")
     _check("max_pool2d_fwd", load().max_pool2d_fwd(dt, _p(X), _p(out), _p(argmax), N, C, Hin,
-                                                    Win, Hf, Wf, stride, pad, _stream()))
+                                                    Win, Hf, Wf, stride, pad, _stream(stream)))
     return out, argmax, Hout, Wout
 
 
-def max_pool2d_bwd(dout, argmax, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+def max_pool2d_bwd(dout, argmax, C, Hin, Win, Hf, Wf, stride, pad, dX=None, stream=None):
     dt = _dtype(dout, dX)
     if argmax.dtype != torch.int32:
         raise TypeError("argmax must be int32")
@@ -421,12 +428,13 @@ def max_pool2d_bwd(dout, argmax, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
     _need(argmax, N * C * max(Hout, 0) * max(Wout, 0), "argmax")
     _need(dX, N * C * Hin * Win, "dX")
     _check("max_pool2d_bwd", load().max_pool2d_bwd(dt, _p(dout), _p(argmax), _p(dX), N, C, Hin,
-                                                    Win, Hf, Wf, stride, pad, _stream()))
+                                                    Win, Hf, Wf, stride, pad, _stream(stream)))
     return dX
 
 
 def conv2d_forward_pool(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, pool_h, pool_w, pool_stride,
-                        pool_pad, relu=True, out=None, pooled=None, argmax=None, keep_out=False):
+                        pool_pad, relu=True, out=None, pooled=None, argmax=None, keep_out=False,
+                        stream=None):
     """relu(conv + b) then max-pool in one call.  Returns (out or None, pooled, argmax,
     Hp, Wp); the conv output is only materialised when out is given or keep_out."""
     dt = _dtype(X, W, b, out, pooled)
@@ -449,12 +457,12 @@ def conv2d_forward_pool(X, W, b, C, Hin, Win, Hf, Wf, stride, pad, pool_h, pool_
     _need(argmax, N * F * max(Hp, 0) * max(Wp, 0), "argmax")
     _check("conv2d_forward_pool", load().conv2d_forward_pool(
         dt, _p(X), _p(W), _p(b), _p(out), _p(pooled), _p(argmax), N, C, Hin, Win, F, Hf, Wf,
-        stride, pad, int(relu), pool_h, pool_w, pool_stride, pool_pad, _stream()))
+        stride, pad, int(relu), pool_h, pool_w, pool_stride, pool_pad, _stream(stream)))
     return out, pooled, argmax, Hp, Wp
 
 
 def conv2d_forward_csr(rowptr, colidx, vals, W, b, C, Hin, Win, Hf, Wf, stride, pad, relu=True,
-                       out=None, row_index=None):
+                       out=None, row_index=None, stream=None):
     """conv2d forward of a CSR input (N x C*Hin*Win; int32 rowptr/colidx on the device)."""
     dt = _dtype(vals, W, b, out)
     N, F = rowptr.numel() - 1, W.shape[0]
@@ -475,12 +483,12 @@ def conv2d_forward_csr(rowptr, colidx, vals, W, b, C, Hin, Win, Hf, Wf, stride, 
     _check("conv2d_forward_csr", load().conv2d_forward_csr(
         dt, _p(rowptr), _p(colidx) if nnz else None, _p(vals) if nnz else None, nnz,
         _p(row_index), _p(W), _p(b), _p(out), N, C, Hin, Win, F, Hf, Wf, stride, pad,
-        int(relu), _stream()))
+        int(relu), _stream(stream)))
     return out
 
 
 def conv2d_forward_multi(X, Ws, bs, C, Hin, Win, Hf, Wf, stride, pad, relu=True, outs=None,
-                         Wcat=None, bcat=None):
+                         Wcat=None, bcat=None, stream=None):
     """Several filter banks over one input in one launch.  Ws / bs: lists of the
     banks' filters (F_b x C*Hf*Wf) and biases (or None).  Wcat / bcat may pass the
     stacked copies already made; returns the list of outputs."""
@@ -506,11 +514,12 @@ def conv2d_forward_multi(X, Ws, bs, C, Hin, Win, Hf, Wf, stride, pad, relu=True,
     _check("conv2d_forward_multi", load().conv2d_forward_multi(
         dt, _p(X), _p(Wcat), _p(bcat), ctypes.cast(ptrs, ctypes.c_void_p),
         ctypes.cast(fs, ctypes.c_void_p), nb, N, C, Hin, Win, Hf, Wf, stride, pad, int(relu),
-        _stream()))
+        _stream(stream)))
     return outs
 
 
-def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, dX=None):
+def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, dX=None,
+                        stream=None):
     """Pool backward with the preceding relu's mask (pooled > 0) folded in."""
     dt = _dtype(dout, pooled, dX)
     N = dout.shape[0]
@@ -525,7 +534,7 @@ def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, 
     _need(dX, N * C * Hin * Win, "dX")
     _check("max_pool2d_bwd_relu", load().max_pool2d_bwd_relu(
         dt, _p(dout), _p(argmax), _p(pooled), _p(dX), N, C, Hin, Win, Hf, Wf, stride, pad,
-        _stream()))
+        _stream(stream)))
     return dX
 
 
@@ -545,7 +554,7 @@ def _affine_ws(X, N, D, M, workspace):
     return _p(workspace), workspace.numel() * workspace.element_size()
 
 
-def affine_fwd(X, W, b, relu=False, out=None, workspace=None):
+def affine_fwd(X, W, b, relu=False, out=None, workspace=None, stream=None):
     dt = _dtype(X, W, b, out)
     N, D = X.shape
     M = W.shape[1]
@@ -556,12 +565,12 @@ def affine_fwd(X, W, b, relu=False, out=None, workspace=None):
     _need(out, N * M, "out")
     ws, nb = _affine_ws(X, N, D, M, workspace)
     _check("affine_fwd", load().affine_fwd(dt, _p(X), _p(W), _p(b), _p(out), N, D, M,
-                                            int(bool(relu)), ws, nb, _stream()))
+                                            int(bool(relu)), ws, nb, _stream(stream)))
     return out
 
 
 def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW=None, db=None,
-               want_dW=True, workspace=None, relu_input=False):
+               want_dW=True, workspace=None, relu_input=False, stream=None):
     """Returns [dX, dW, db] (each None when not wanted).  relu_input: dX is
     also multiplied by (X > 0) (X is a relu output)."""
     dt = _dtype(dout, X, W, out_fwd, dX, dW, db)
@@ -582,11 +591,11 @@ def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW
     ws, nb = _affine_ws(X, N, D, M, workspace) if (dX is not None or dW is not None) else (None, 0)
     _check("affine_bwd", load().affine_bwd(dt, _p(dout), _p(X), _p(W), _p(out_fwd), _p(dX),
                                             _p(dW), _p(db), N, D, M, int(bool(relu_input)), ws,
-                                            nb, _stream()))
+                                            nb, _stream(stream)))
     return dX, dW, db
 
 
-def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None):
+def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None, stream=None):
     """Returns (loss as a 1-element device tensor, dscores, probs-or-None)."""
     dt = _dtype(scores, Y, loss, dscores, probs)
     N, K = scores.shape
@@ -601,72 +610,72 @@ def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None
     _need(probs, N * K, "probs")
     _need(loss, 1, "loss")
     _check("softmax_xent", load().softmax_xent(dt, _p(scores), _p(Y), _p(probs), _p(dscores),
-                                                _p(loss), N, K, _stream()))
+                                                _p(loss), N, K, _stream(stream)))
     return loss, dscores, probs
 
 
-def softmax_fwd(scores, probs=None):
+def softmax_fwd(scores, probs=None, stream=None):
     """Row-wise softmax of an N x K matrix."""
     dt = _dtype(scores, probs)
     N, K = scores.shape
     if probs is None:
         probs = _empty((N, K), scores)
     _need(probs, N * K, "probs")
-    _check("softmax_fwd", load().softmax_fwd(dt, _p(scores), _p(probs), N, K, _stream()))
+    _check("softmax_fwd", load().softmax_fwd(dt, _p(scores), _p(probs), N, K, _stream(stream)))
     return probs
 
 
-def sgd_momentum_update(theta, grad, v, lr, mu):
+def sgd_momentum_update(theta, grad, v, lr, mu, stream=None):
     """In place: v <- mu v - lr grad; theta <- theta + v."""
     dt = _dtype(theta, grad, v)
     _need(grad, theta.numel(), "grad")
     _need(v, theta.numel(), "v")
     _check("sgd_momentum_update", load().sgd_momentum_update(
-        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream()))
+        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream(stream)))
     return theta, v
 
 
-def sgd_update(theta, grad, lr):
+def sgd_update(theta, grad, lr, stream=None):
     """In place: theta <- theta - lr grad."""
     dt = _dtype(theta, grad)
     _need(grad, theta.numel(), "grad")
     _check("sgd_update", load().sgd_update(dt, _p(theta), _p(grad), float(lr), theta.numel(),
-                                           _stream()))
+                                           _stream(stream)))
     return theta
 
 
-def sgd_nesterov_update(theta, grad, v, lr, mu):
+def sgd_nesterov_update(theta, grad, v, lr, mu, stream=None):
     """In place: v' = mu v - lr grad; theta <- theta - mu v + (1 + mu) v'; v <- v'."""
     dt = _dtype(theta, grad, v)
     _need(grad, theta.numel(), "grad")
     _need(v, theta.numel(), "v")
     _check("sgd_nesterov_update", load().sgd_nesterov_update(
-        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream()))
+        dt, _p(theta), _p(grad), _p(v), float(lr), float(mu), theta.numel(), _stream(stream)))
     return theta, v
 
 
-def adagrad_update(theta, grad, cache, lr, eps=1e-6):
+def adagrad_update(theta, grad, cache, lr, eps=1e-6, stream=None):
     """In place: cache += grad^2; theta -= lr grad / (sqrt(cache) + eps)."""
     dt = _dtype(theta, grad, cache)
     _need(grad, theta.numel(), "grad")
     _need(cache, theta.numel(), "cache")
     _check("adagrad_update", load().adagrad_update(
-        dt, _p(theta), _p(grad), _p(cache), float(lr), float(eps), theta.numel(), _stream()))
+        dt, _p(theta), _p(grad), _p(cache), float(lr), float(eps), theta.numel(), _stream(stream)))
     return theta, cache
 
 
-def rmsprop_update(theta, grad, cache, lr, decay=0.99, eps=1e-6):
+def rmsprop_update(theta, grad, cache, lr, decay=0.99, eps=1e-6, stream=None):
     """In place: cache = decay cache + (1-decay) grad^2; theta -= lr grad / (sqrt(cache) + eps)."""
     dt = _dtype(theta, grad, cache)
     _need(grad, theta.numel(), "grad")
     _need(cache, theta.numel(), "cache")
     _check("rmsprop_update", load().rmsprop_update(
         dt, _p(theta), _p(grad), _p(cache), float(lr), float(decay), float(eps), theta.numel(),
-        _stream()))
+        _stream(stream)))
     return theta, cache
 
 
-def adam_update(theta, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, t=1):
+def adam_update(theta, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, t=1, stream=None):
     """In place, step t >= 1: m, v moments; theta -= lr_t m / (sqrt(v) + eps),
     lr_t = lr sqrt(1 - beta2^t) / (1 - beta1^t)."""
     dt = _dtype(theta, grad, m, v)
@@ -675,16 +684,16 @@ def adam_update(theta, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, t=1):
     _need(v, theta.numel(), "v")
     _check("adam_update", load().adam_update(
         dt, _p(theta), _p(grad), _p(m), _p(v), float(lr), float(beta1), float(beta2), float(eps),
-        int(t), theta.numel(), _stream()))
+        int(t), theta.numel(), _stream(stream)))
     return theta, m, v
 
 
-def count_nonzero(X, out=None):
+def count_nonzero(X, out=None, stream=None):
     """Number of non-zero entries, as a 1-element int64 device tensor."""
     dt = _dtype(X)
     if out is None:
         out = _empty((1,), X, dtype=torch.int64)
     if out.dtype != torch.int64 or out.numel() < 1:
         raise ValueError("out must be an int64 tensor with at least one element")
-    _check("count_nonzero", load().count_nonzero(dt, _p(X), X.numel(), _p(out), _stream()))
+    _check("count_nonzero", load().count_nonzero(dt, _p(X), X.numel(), _p(out), _stream(stream)))
     return out

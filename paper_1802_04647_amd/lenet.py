@@ -78,60 +78,70 @@ class LeNetTrainer:
         # backward, conv2 backward_data, ...): they only share read-only inputs,
         # and each kernel is too small to fill the GPU alone
         self.side = torch.cuda.Stream(device=device)
+        self.ev_fork1, self.ev_fork2, self.ev_join = (torch.cuda.Event() for _ in range(3))
         self.two_streams = True
 
     def forward_backward(self, X, Y):
         p, g = self.p, self.g
+        # Streams and events are passed explicitly (no stream contexts, no
+        # events created per step): the step is a few dozen short launches, and
+        # the host time to enqueue them is part of its time.
+        ms = torch.cuda.current_stream()
+        two = self.two_streams
+        ss = self.side if two else ms
         dmlnn.conv2d_forward_pool(X, p["W1"], p["b1"], 1, 28, 28, 5, 5, 1, 2, 2, 2, 2, 0,
-                                  pooled=self.p1, argmax=self.i1)
+                                  pooled=self.p1, argmax=self.i1, stream=ms)
         dmlnn.conv2d_forward_pool(self.p1, p["W2"], p["b2"], 32, 14, 14, 5, 5, 1, 2, 2, 2, 2, 0,
-                                  pooled=self.p2, argmax=self.i2)
-        dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h, workspace=self.wsa)
-        dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s, workspace=self.wsa)
-        dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds)
+                                  pooled=self.p2, argmax=self.i2, stream=ms)
+        dmlnn.affine_fwd(self.p2, p["W3"], p["b3"], relu=True, out=self.h, workspace=self.wsa,
+                         stream=ms)
+        dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s, workspace=self.wsa,
+                         stream=ms)
+        dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds,
+                           stream=ms)
         # dh comes out masked by h > 0 (the relu backward of affine 1, folded
         # into this product), so affine 1's backward reads no mask
         dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"],
-                         workspace=self.wsa, relu_input=True)
-        main = torch.cuda.current_stream()
-        side = self.side if self.two_streams else main
-        if side is not main:
-            side.wait_stream(main)  # dh is ready
-        with torch.cuda.stream(side):
-            dmlnn.affine_bwd(self.dh, self.p2, p["W3"], None, want_dX=False, dW=g["W3"],
-                             db=g["b3"], workspace=self.wsa_side)
+                         workspace=self.wsa, relu_input=True, stream=ms)
+        if two:  # fork: dh is ready
+            self.ev_fork1.record(ms)
+            ss.wait_event(self.ev_fork1)
+        dmlnn.affine_bwd(self.dh, self.p2, p["W3"], None, want_dX=False, dW=g["W3"],
+                         db=g["b3"], workspace=self.wsa_side, stream=ss)
         dmlnn.affine_bwd(self.dh, self.p2, p["W3"], None, dX=self.dp2, want_dW=False,
-                         want_db=False, workspace=self.wsa)
+                         want_db=False, workspace=self.wsa, stream=ms)
         if self.fused_pool_backward:
-            if side is not main:
-                side.wait_stream(main)  # dp2 is ready
-            with torch.cuda.stream(side):
-                dmlnn.conv2d_backward_filter_pooled(self.p1, self.dp2, self.i2, self.p2, 32, 14,
-                                                    14, 5, 5, 1, 2, 64, 2, 2, 2, 0,
-                                                    workspace=self.ws2, dW=g["W2"], db=g["b2"])
+            if two:  # fork: dp2 is ready
+                self.ev_fork2.record(ms)
+                ss.wait_event(self.ev_fork2)
+            dmlnn.conv2d_backward_filter_pooled(self.p1, self.dp2, self.i2, self.p2, 32, 14,
+                                                14, 5, 5, 1, 2, 64, 2, 2, 2, 0,
+                                                workspace=self.ws2, dW=g["W2"], db=g["b2"],
+                                                stream=ss)
             dmlnn.conv2d_backward_data_pooled(p["W2"], self.dp2, self.i2, self.p2, 32, 14, 14, 5,
-                                              5, 1, 2, 2, 2, 2, 0, dX=self.dp1)
+                                              5, 1, 2, 2, 2, 2, 0, dX=self.dp1, stream=ms)
             dmlnn.conv2d_backward_filter_pooled(X, self.dp1, self.i1, self.p1, 1, 28, 28, 5, 5, 1,
                                                 2, 32, 2, 2, 2, 0, workspace=self.ws1,
-                                                dW=g["W1"], db=g["b1"])
+                                                dW=g["W1"], db=g["b1"], stream=ms)
         else:
             dmlnn.max_pool2d_bwd_relu(self.dp2, self.i2, self.p2, 64, 14, 14, 2, 2, 2, 0,
-                                      dX=self.dc2)
-            if side is not main:
-                side.wait_stream(main)  # dc2 is ready
-            with torch.cuda.stream(side):
-                dmlnn.conv2d_backward_filter(self.p1, self.dc2, None, 32, 14, 14, 5, 5, 1, 2, 64,
-                                             workspace=self.ws2, dW=g["W2"], db=g["b2"])
+                                      dX=self.dc2, stream=ms)
+            if two:  # fork: dc2 is ready
+                self.ev_fork2.record(ms)
+                ss.wait_event(self.ev_fork2)
+            dmlnn.conv2d_backward_filter(self.p1, self.dc2, None, 32, 14, 14, 5, 5, 1, 2, 64,
+                                         workspace=self.ws2, dW=g["W2"], db=g["b2"], stream=ss)
             dmlnn.conv2d_backward_data(p["W2"], self.dc2, None, 32, 14, 14, 5, 5, 1, 2,
-                                       dX=self.dp1)
+                                       dX=self.dp1, stream=ms)
             dmlnn.max_pool2d_bwd_relu(self.dp1, self.i1, self.p1, 32, 28, 28, 2, 2, 2, 0,
-                                      dX=self.dc1)
+                                      dX=self.dc1, stream=ms)
             dmlnn.conv2d_backward_filter(X, self.dc1, None, 1, 28, 28, 5, 5, 1, 2, 32,
-                                         workspace=self.ws1, dW=g["W1"], db=g["b1"])
+                                         workspace=self.ws1, dW=g["W1"], db=g["b1"], stream=ms)
         # join: the optimizer reads the side stream's gradients, and the next
         # step's forward overwrites p1 and p2, which the side stream reads
-        if side is not main:
-            main.wait_stream(side)
+        if two:
+            self.ev_join.record(ss)
+            ms.wait_event(self.ev_join)
         return self.loss
 
     def step(self, X, Y):

@@ -164,7 +164,15 @@ def lenet_timing(steps=50, warmup=10):
     # the conv backward passes reading the pool gradients directly (the
     # step's form), and the pool backward as its own kernel, for comparison
     ms = eager_ms(LeNetTrainer(params))
-    unfused_ms = eager_ms(LeNetTrainer(params, fused_pool_backward=False))
+    # the step's forms: conv backward from the pool gradients (fused) or after
+    # the pool backward kernel (unfused), on one stream or two
+    forms = {}
+    for fused in (True, False):
+        for two in (True, False):
+            tr = LeNetTrainer(params, fused_pool_backward=fused)
+            tr.two_streams = two
+            forms[f"{'fused' if fused else 'unfused'}_{'two' if two else 'one'}_streams"] = \
+                eager_ms(tr)
     # the same step recorded once as a HIP graph and replayed
     gtr = LeNetTrainer(params)
     gtr.capture(Xd, Yd, warmup=2)
@@ -178,7 +186,7 @@ def lenet_timing(steps=50, warmup=10):
     torch.cuda.synchronize()
     gms = e0.elapsed_time(e1) / steps
     return dict(ms_per_step=ms, images_per_s=64.0 / (ms / 1e3), graph_ms_per_step=gms,
-                graph_images_per_s=64.0 / (gms / 1e3), unfused_pool_backward_ms_per_step=unfused_ms)
+                graph_images_per_s=64.0 / (gms / 1e3), forms_ms_per_step=forms)
 
 
 def lenet_trace(fused, steps, warmup):
@@ -694,7 +702,10 @@ def main():
         return
     if args.only_lenet:
         lt = lenet_timing()
-        print(json.dumps({"lenet_training": {k: round(v, 4) for k, v in lt.items()}}), flush=True)
+        forms = lt.pop("forms_ms_per_step")
+        out = {k: round(v, 4) for k, v in lt.items()}
+        out["forms_ms_per_step"] = {k: round(v, 4) for k, v in forms.items()}
+        print(json.dumps({"lenet_training": out}), flush=True)
         return
     r = conv_step_timing("f64", args.steps, args.warmup, emit=not args.separate_mask)
     N, F3 = r["N"], 3 * r["flops_per_pass"]
@@ -756,8 +767,8 @@ def main():
                                  "images_per_s": round(lt["images_per_s"], 1),
                                  "hip_graph_ms_per_step": round(lt["graph_ms_per_step"], 4),
                                  "hip_graph_images_per_s": round(lt["graph_images_per_s"], 1),
-                                 "unfused_pool_backward_ms_per_step":
-                                     round(lt["unfused_pool_backward_ms_per_step"], 4)}
+                                 "forms_ms_per_step": {k: round(v, 4) for k, v in
+                                                       lt["forms_ms_per_step"].items()}}
         rec["lenet_scoring"] = scoring_timing()
         rec["conv_configs"] = conv_config_timing()
         rec["horizontal_fusion"] = horizontal_fusion_timing()

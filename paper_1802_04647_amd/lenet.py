@@ -5,17 +5,19 @@ max-pool 2x2/2 -> affine 3136->512 + relu -> affine 512->10 -> softmax +
 cross-entropy; backward in reverse order; then v <- mu v - lr g and
 theta <- theta + v for the eight parameter tensors (paper, Section 2: the NN
 library's layers, its minibatch training loop and SGD with momentum).  Each
-conv+relu+pool runs as one fused call forward, and backward the conv passes
-take the pool's gradient, argmax and pooled values directly (the relu mask and
-the pool routing built while staging), so neither the conv outputs nor their
-gradients are ever stored.
+conv+relu+pool runs as one fused call forward.  Backward, the pool backward
+(relu mask folded in) writes the conv-output gradient and the plain conv
+backward passes read it; with fused_pool_backward=True the conv passes
+instead take the pool's gradient, argmax and pooled values directly (the
+relu mask and the pool routing built while staging), so the conv-output
+gradients are never stored (less memory, a slower step at this size).
 
 All activations, gradients and the workspaces (backward-filter partials,
-affine split partials) are allocated once; ``step`` only enqueues library calls (about twenty launches, one of them
-the optimizer update over the flat parameter buffer) on the current stream and,
-for the weight gradients of affine 1 and conv2, on a second stream that joins
-the current one before the step returns; it returns the loss as a device
-scalar.
+affine split partials) are allocated once; ``step`` only enqueues library
+calls (about twenty launches, one of them the optimizer update over the flat
+parameter buffer) on the current stream and, for the weight gradients of
+affine 1 and conv2, on a second stream that joins the current one before the
+step returns; it returns the loss as a device scalar.
 """
 from __future__ import annotations
 
@@ -28,11 +30,12 @@ PARAM_ORDER = ("W1", "b1", "W2", "b2", "W3", "b3", "W4", "b4")
 
 class LeNetTrainer:
     def __init__(self, params: dict, N: int = 64, lr: float = 0.01, mu: float = 0.9,
-                 dtype=torch.float64, device="cuda", fused_pool_backward: bool = True):
+                 dtype=torch.float64, device="cuda", fused_pool_backward: bool = False):
         self.N, self.lr, self.mu = N, lr, mu
         # False: the pool backward runs as its own kernel (max_pool2d_bwd_relu)
         # into a stored conv-output gradient, which the plain conv backward
-        # calls read (kept to measure the fusion against)
+        # calls read (the faster step at batch 64); True: the conv backward
+        # passes read the pool gradients directly (no conv-output gradients)
         self.fused_pool_backward = fused_pool_backward
         kw = dict(dtype=dtype, device=device)
         # Parameters, gradients and velocities each live in one flat buffer (the

@@ -588,6 +588,7 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     // loaded into (before the next tile's loads reuse them), so the stores
     // leave the phase in which the matrix pipe idles.
     T *const gout = (!PB && a.g_out && kr == 0) ? reinterpret_cast<T *>(a.g_out) : nullptr;
+    constexpr bool kLoadInLoop = sizeof(T) == 8;  // where the next tile's loads issue (below)
     auto emit_g = [&](int n, int oh) {
         if (PB || !gout) return;
         const int tid = opaque(threadIdx.x);
@@ -668,7 +669,7 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         stage_x_full(n0, oh0);
         __syncthreads();
         emit_g(n0, oh0);
-        if (t_begin + 1 < t_end) {
+        if (!kLoadInLoop && t_begin + 1 < t_end) {
             const long long t1 = t_begin + 1;
             const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
             load_g(n1, oh1);
@@ -702,7 +703,19 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         }
 
         const T *grow = s_g + (lane & 15) * a.SG + lq;
+        // fp64: the next tile's loads are issued inside this tile's MFMA loop,
+        // at a k-step that differs per wave (the g tile and the X row at steps
+        // six waves apart): the three waves of a SIMD then do their address
+        // work at different times and the other two keep the matrix pipe fed
+        // (all at once after the barrier, it idled: 1-2% of the pass).  fp32
+        // (half the matrix time per tile) issues them after the barrier,
+        // which measured faster there.
+        const bool pf = kLoadInLoop && tt + 1 < t_end;
+        const int pfg = min(4 * wave, a.RQ - 4);
+        const int pfx = min(4 * ((wave + kRingWaves / 2) % kRingWaves), a.RQ - 4);
         for (int qq = 0; qq < a.RQ; qq += 4) {
+            if (qq == pfg && pf) load_g(n1, oh1);
+            if (qq == pfx && pf && oh1 != 0) load_x(n1, oh1);
             const int qx = qq + lq;
             const int qo = qx < a.Wout ? qx * a.S : 0;
             T av[4];
@@ -730,7 +743,7 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
                 stage_x_full(n1, oh1);
             __syncthreads();
             emit_g(n1, oh1);
-            if (tt + 2 < t_end) {
+            if (!kLoadInLoop && tt + 2 < t_end) {
                 const int n2 = oh1 + 1 < a.Hout ? n1 : n1 + 1, oh2 = oh1 + 1 < a.Hout ? oh1 + 1 : 0;
                 load_g(n2, oh2);
                 if (oh2 != 0) load_x(n2, oh2);

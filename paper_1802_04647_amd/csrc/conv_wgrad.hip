@@ -500,10 +500,13 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     const long long t_end = (long long)(split + 1) * a.T_total / a.splits;
 
     // Input row yr (from the top padding row) of channel c_lo + c, or zeros.
+    // (The offset inside an image is 32-bit: an image holds fewer than 2^31
+    // elements, which the host validates.)
     auto x_at = [&](int n, int c, int yr, int u) -> T {
         const int cg = c_lo + c, y = yr - a.P, x = u - a.P;
+        const T *xi = X + (size_t)n * a.C * a.Hin * a.Win;  // the image (uniform)
         if (cg < a.C && y >= 0 && y < a.Hin && x >= 0 && x < a.Win)
-            return X[(((size_t)n * a.C + cg) * a.Hin + y) * a.Win + x];
+            return xi[(cg * a.Hin + y) * a.Win + x];
         return T(0);
     };
 
@@ -543,7 +546,7 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             if (e < kBM * a.RQ) {
                 const int r = div_magic(e, a.magic_rq), u = e - r * a.RQ;
                 if (ft * kBM + r < a.F && u < a.Wout) {
-                    const size_t o = gbase + (size_t)r * a.Q + u;
+                    const size_t o = gbase + (unsigned)(r * a.Q + u);  // < F*Q < 2^31
                     v = dout[o];
                     if (mask) mv = mask[o];
                 }

@@ -409,6 +409,17 @@ DMLNN_API int conv2d_backward_data_pooled(dmlnn_dtype dtype, const void *W, cons
  * Returns 0 for invalid arguments. */
 DMLNN_API size_t affine_workspace_size(dmlnn_dtype dtype, int N, int D, int M);
 
+/* Host-only plan query (no device access), like conv2d_plan: the launch shape
+ * one affine product takes for these sizes and workspace_bytes.  product: 0 =
+ * out = X W (M_out = N rows, N_out = M columns, reduction D), 1 = dX = g W^T,
+ * 2 = dW = X^T g.  *tile: the edge of a block's output tile (16 or 32);
+ * *waves: waves per block, each a k range of that tile; *splits: blocks per
+ * tile along k (partials in the workspace when above 1).  Returns
+ * DMLNN_ERR_ARG for invalid sizes or product, DMLNN_ERR_NULL for a NULL
+ * output pointer. */
+DMLNN_API int affine_plan(dmlnn_dtype dtype, int product, int N, int D, int M,
+                          size_t workspace_bytes, int *tile, int *waves, int *splits);
+
 /* out = X W + b, then max(., 0) if relu.  b may be NULL. */
 DMLNN_API int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, void *out,
                          int N, int D, int M, int relu, void *workspace,

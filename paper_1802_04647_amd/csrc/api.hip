@@ -656,6 +656,25 @@ size_t affine_workspace_size(dmlnn_dtype dtype, int N, int D, int M)
     return dmlnn::affine_workspace_bytes(dtype, N, D, M);
 }
 
+int affine_plan(dmlnn_dtype dtype, int product, int N, int D, int M, size_t workspace_bytes,
+                int *tile, int *waves, int *splits)
+{
+    if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "affine_plan: bad dtype %d", (int)dtype);
+    if (!tile || !waves || !splits) return fail(DMLNN_ERR_NULL, "affine_plan: NULL output");
+    if (!count_ok(N, D) || !count_ok(D, M) || !count_ok(N, M) || product < 0 || product > 2)
+        return fail(DMLNN_ERR_ARG, "affine_plan: bad product %d or sizes N=%d D=%d M=%d",
+                    product, N, D, M);
+    const size_t el = dtype == DMLNN_F64 ? 8 : 4;
+    // (rows, columns, reduction) of the product
+    const int r = product == 2 ? D : N, c = product == 1 ? D : M, k = product == 0 ? D
+                                                                 : (product == 1 ? M : N);
+    const dmlnn::GemmPlan p = dmlnn::gemm_plan(r, c, k, el, workspace_bytes);
+    *tile = 16 * p.wt;
+    *waves = p.nk;
+    *splits = p.splits;
+    return DMLNN_OK;
+}
+
 // An affine workspace is optional; when given it must be element aligned and
 // must not overlap the tensors the call reads or writes.
 static int affine_workspace_ok(const char *name, dmlnn_dtype dtype, void *ws, size_t ws_bytes,

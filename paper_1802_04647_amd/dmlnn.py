@@ -86,6 +86,7 @@ def load():
         "max_pool2d_fwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "max_pool2d_bwd": (_i, [_i, _vp, _vp, _vp] + [_i] * 8 + [_vp]),
         "affine_workspace_size": (ctypes.c_size_t, [_i] * 4),
+        "affine_plan": (_i, [_i] * 5 + [ctypes.c_size_t] + [ctypes.POINTER(_i)] * 3),
         "affine_fwd": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 4 + [_vp, ctypes.c_size_t, _vp]),
         "affine_bwd": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 4
                        + [_vp, ctypes.c_size_t, _vp]),
@@ -541,6 +542,21 @@ def max_pool2d_bwd_relu(dout, argmax, pooled, C, Hin, Win, Hf, Wf, stride, pad, 
 def affine_workspace_size(dtype, N, D, M) -> int:
     dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
     return int(load().affine_workspace_size(dt, N, D, M))
+
+
+AFFINE_PRODUCTS = {"forward": 0, "dX": 1, "dW": 2}
+
+
+def affine_plan(dtype, product, N, D, M, workspace_bytes):
+    """The launch shape of one affine product (host only): a dict of tile
+    (output tile edge), waves (per block, splitting its k range) and splits
+    (blocks per tile along k)."""
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    t, w, s = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check("affine_plan", load().affine_plan(dt, AFFINE_PRODUCTS[product], N, D, M,
+                                              workspace_bytes, ctypes.byref(t), ctypes.byref(w),
+                                              ctypes.byref(s)))
+    return {"tile": t.value, "waves": w.value, "splits": s.value}
 
 
 def _affine_ws(X, N, D, M, workspace):

@@ -17,7 +17,7 @@
 namespace dmlnn {
 namespace {
 
-constexpr int kMaxNK = 8;    // waves per block of the small-product kernel, each a k range
+constexpr int kMaxNK = 8;    // waves per block, each a k range of the block's tile
 
 struct GemmArgs {
     const void *A, *Amask;  // A(i,k) = A[i*sAm + k*sAk]; mask has the same strides

@@ -366,6 +366,7 @@ static int plan_query(const char *name, dmlnn_dtype dtype, int pass, int form, i
     plan->row_slices = info.row_slices;
     plan->pipelined = info.pipelined;
     plan->fused = info.fused;
+    plan->row_staged = info.row_staged;
     g_err[0] = '\0';
     return DMLNN_OK;
 }

@@ -463,8 +463,16 @@ constexpr int kRingWaves = kRingThreads / kWave;
 constexpr int kRG = 5;  // g-tile elements each thread stages per tile
 constexpr int kRX = 5;  // new X-row elements each thread stages per tile
 constexpr int kRGP = 5; // pooled source: pool windows each thread stages per tile (64 x 60 / 768)
+// Row-mapped staging (RM: one new input row a tile, rows of at most 64
+// elements, at most 72 channels): wave w stages rows w, w + 12, ... of the g
+// tile and channels w, w + 12, ... of the new input row, a lane per element,
+// so each row's offsets are a wave-uniform base plus the lane: no division
+// and no per-element branch, where the element mapping above pays a magic
+// division per element and a branch per staged element.
+constexpr int kRMG = (kBM + kRingWaves - 1) / kRingWaves;  // g rows a wave stages (6)
+constexpr int kRMX = 6;                                     // channels a wave stages
 
-template <typename T, int NBW, bool ZSKIP, bool PB>
+template <typename T, int NBW, bool ZSKIP, bool PB, bool RM>
 __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
@@ -510,8 +518,11 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         return T(0);
     };
 
-    constexpr int NG = PB ? 1 : kRG, NP = PB ? kRGP : 1;
-    T vg[NG], vm[NG], vx[kRX];
+    static_assert(!(PB && RM), "the pooled source has its own staging");
+    // fp64 row-maps the input rows only: a sixth g row a wave would spill
+    constexpr bool RMG = RM && sizeof(T) == 4;
+    constexpr int NG = PB ? 1 : (RMG ? kRMG : kRG), NP = PB ? kRGP : 1, NX = RM ? kRMX : kRX;
+    T vg[NG], vm[NG], vx[NX];
     // Pooled source: element e of a row is (filter row r, pool column px): the
     // window's three values are loaded once and its PS cells of the row written
     // from them (the gradient at the argmax, zeros elsewhere).
@@ -536,6 +547,23 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
                 pd[it] = reinterpret_cast<const T *>(a.pool.dpool)[o];
                 pa[it] = a.pool.argmax[o];
                 pp[it] = reinterpret_cast<const T *>(a.pool.pooled)[o];
+            }
+            return;
+        }
+        if constexpr (RMG) {
+            const int ln = tid & (kWave - 1);
+            const T *gb = dout + gbase, *mbp = mask ? mask + gbase : nullptr;
+#pragma unroll
+            for (int it = 0; it < NG; ++it) {
+                const int r = wave + kRingWaves * it;  // wave-uniform
+                T v = T(0), mv = T(1);
+                if (r < kBM && ft * kBM + r < a.F && ln < a.Wout) {
+                    const unsigned o = (unsigned)(r * a.Q) + ln;  // < F*Q < 2^31
+                    v = gb[o];
+                    if (mask) mv = mbp[o];
+                }
+                vg[it] = v;
+                vm[it] = mv;
             }
             return;
         }
@@ -577,6 +605,15 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             return;
         }
         (void)n;
+        if constexpr (RMG) {
+            const int ln = tid & (kWave - 1);
+#pragma unroll
+            for (int it = 0; it < NG; ++it) {
+                const int r = wave + kRingWaves * it;
+                if (r < kBM && ln < a.RQ) s_g[r * a.SG + ln] = (vm[it] > T(0)) ? vg[it] : T(0);
+            }
+            return;
+        }
 #pragma unroll
         for (int it = 0; it < NG; ++it) {
             const int e = tid + kRingThreads * it;
@@ -595,6 +632,17 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     auto emit_g = [&](int n, int oh) {
         if (PB || !gout) return;
         const int tid = opaque(threadIdx.x);
+        if constexpr (RMG) {
+            const int ln = tid & (kWave - 1);
+            T *gb = gout + ((size_t)n * a.F + ft * kBM) * a.Q + (size_t)oh * a.Wout;
+#pragma unroll
+            for (int it = 0; it < NG; ++it) {
+                const int r = wave + kRingWaves * it;
+                if (r < kBM && ft * kBM + r < a.F && ln < a.Wout)
+                    gb[(unsigned)(r * a.Q) + ln] = (vm[it] > T(0)) ? vg[it] : T(0);
+            }
+            return;
+        }
 #pragma unroll
         for (int it = 0; it < NG; ++it) {
             const int e = tid + kRingThreads * it;
@@ -610,6 +658,20 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     const int nrw = nr * a.Wpad;
     auto load_x = [&](int n, int oh) {
         const int tid = opaque(threadIdx.x);
+        if constexpr (RM) {  // the one new row yr = oh*S + Hf - 1, channel c_lo + c a wave-row
+            const int ln = tid & (kWave - 1);
+            const int y = oh * a.S + a.Hf - 1 - a.P, x = ln - a.P;
+            const bool ok = ln < a.Wpad && x >= 0 && x < a.Win && y >= 0 && y < a.Hin;
+            const T *xi = X + (size_t)n * a.C * a.Hin * a.Win;  // the image
+#pragma unroll
+            for (int it = 0; it < NX; ++it) {
+                const int c = wave + kRingWaves * it, cg = c_lo + c;
+                T v = T(0);
+                if (c < nch && cg < a.C && ok) v = xi[(unsigned)((cg * a.Hin + y) * a.Win) + x];
+                vx[it] = v;
+            }
+            return;
+        }
 #pragma unroll
         for (int it = 0; it < kRX; ++it) {
             const int e = tid + kRingThreads * it;
@@ -630,6 +692,15 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     auto store_x = [&](int oh) {
         const int tid = opaque(threadIdx.x);
         const int s0 = (oh * a.S + a.Hf - nr) % a.Hf;
+        if constexpr (RM) {
+            const int ln = tid & (kWave - 1);
+#pragma unroll
+            for (int it = 0; it < NX; ++it) {
+                const int c = wave + kRingWaves * it;
+                if (c < nch && ln < a.Wpad) s_x[c * a.CH + s0 * a.Wpad + ln] = vx[it];
+            }
+            return;
+        }
         const int base = s0 * a.Wpad, wrap = (a.Hf - s0) * a.Wpad, ring = a.Hf * a.Wpad;
 #pragma unroll
         for (int it = 0; it < kRX; ++it) {
@@ -801,6 +872,7 @@ long long split_bound(size_t lds, int threads, int per_split, long long T_total)
 
 struct WPlan {
     int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined, spr;
+    int rowmap = 0;  // ring: row-mapped staging (one new row a tile, rows <= 64, <= 72 channels)
     long long T_total;
     size_t lds;
 };
@@ -911,6 +983,7 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     if ((long long)nch_alloc * nr * p.Wpad > (long long)kRingThreads * kRX) return false;
     p.lds = tsz * ((size_t)kBM * p.SG + (size_t)nch_alloc * p.CH);
     if (p.lds > 160 * 1024) return false;
+    p.rowmap = nr == 1 && p.Wpad <= kWave && p.RQ <= kWave && nch_alloc <= kRingWaves * kRMX;
     p.pipelined = 1;
     p.tiles_per_img = d.Hout;
     p.T_total = (long long)d.N * d.Hout;
@@ -918,12 +991,22 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     return true;
 }
 
+template <typename T, bool ZSKIP, bool PB, bool RM>
+void (*ring_kernel(int nbw))(WgradArgs)
+{
+    return nbw == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP, PB, RM>
+                    : (nbw == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP, PB, RM>
+                                : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB, RM>);
+}
+
 template <typename T, bool ZSKIP, bool PB>
 hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    auto k = p.NBW == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP, PB>
-                        : (p.NBW == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP, PB>
-                                      : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB>);
+    void (*k)(WgradArgs);
+    if constexpr (PB)
+        k = ring_kernel<T, ZSKIP, PB, false>(p.NBW);
+    else
+        k = p.rowmap ? ring_kernel<T, ZSKIP, PB, true>(p.NBW) : ring_kernel<T, ZSKIP, PB, false>(p.NBW);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
@@ -1234,6 +1317,7 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanIn
     info.pipelined = p.pipelined;
     if (pool_ps && !ring && kBM * max_regions(p, d, pool_ps) > kThreads * kMGP) info.pipelined = 0;
     info.fused = pool_ps ? 1 : 0;
+    info.row_staged = ring && !pool_ps && p.rowmap ? (tsz == 4 ? 3 : 1) : 0;
     return hipSuccess;
 }
 

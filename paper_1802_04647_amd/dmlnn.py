@@ -47,7 +47,7 @@ class ConvPlan(ctypes.Structure):
                                            ("workspace_bytes", ctypes.c_size_t)] + [
         (n, ctypes.c_int) for n in ("tile_stride", "k_chunk", "slice_stride", "stage_bytes",
                                     "window_bytes", "slice_bytes", "slice_vec", "g_stride",
-                                    "row_slices", "pipelined", "fused")]
+                                    "row_slices", "pipelined", "fused", "row_staged")]
 
 
 KERNELS = {1: "igemm_dma", 2: "igemm_reg", 3: "small_m", 4: "resident", 5: "wgrad_ring",

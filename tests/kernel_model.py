@@ -897,11 +897,29 @@ def model_wgrad_ring(g, p, tsz, form):
     lq, l16 = lane >> 4, lane & 15
     nr = min(S, Hf)
     pb = form == "pooled_source"
-    # g tile staging
-    need(BM * RQ <= 768 * 5, f"{kernel}: g tile exceeds the staging registers")
-    e = np.arange(BM * RQ)
-    r = div_magic(e, RQ, f"{kernel} g row")
-    lds.access("g", r * SG + (e - r * RQ), tsz, "g tile store")
+    # row-mapped staging: bit 0 the new input row, bit 1 the g tile (fp32 only)
+    rs = p["row_staged"]
+    rm_ok = not pb and nr == 1 and Wpad <= 64 and RQ <= 64 and nch_alloc <= 12 * 6
+    need(rs == ((3 if tsz == 4 else 1) if rm_ok else 0), f"{kernel}: row staging {rs}")
+    w_it = (np.arange(12)[:, None] + 12 * np.arange(6)[None, :]).ravel()  # rows of wave w, step it
+    if rs & 2:
+        # wave w, step it: g row w + 12 it (< 64), lane u (< RQ); every cell once
+        r = np.repeat(w_it[w_it < BM], 64)
+        u = np.tile(lane, int((w_it < BM).sum()))
+        ok = u < RQ
+        cells = r[ok] * RQ + u[ok]
+        need(np.array_equal(np.sort(cells), np.arange(BM * RQ)), f"{kernel}: g rows not staged once")
+        lds.access("g", r[ok] * SG + u[ok], tsz, "g tile store")
+        f = np.arange(cdiv(g["F"], BM))[:, None] * BM + r[ok][None, :]
+        live = (f < g["F"]) & (u[ok][None, :] < Wout)
+        for n, oh in ((0, 0), (g["N"] - 1, g["Hout"] - 1)):
+            glob(kernel, "dout (row-mapped)", ((n * g["F"] + f) * g["Q"] + oh * Wout + u[ok])[live],
+                 g["N"] * g["F"] * g["Q"])
+    else:
+        need(BM * RQ <= 768 * 5, f"{kernel}: g tile exceeds the staging registers")
+        e = np.arange(BM * RQ)
+        r = div_magic(e, RQ, f"{kernel} g row")
+        lds.access("g", r * SG + (e - r * RQ), tsz, "g tile store")
     if pb:
         PS = g["PS"]
         npx = int(div_magic(Wout + PS - 1, PS))
@@ -922,11 +940,27 @@ def model_wgrad_ring(g, p, tsz, form):
     for kbeg, kend, c_lo, nch in ranges:
         # new-row staging
         nrw = nr * Wpad
-        need(nch * nrw <= 768 * 5, f"{kernel}: new rows exceed the staging registers")
-        e = np.arange(nch * nrw)
-        c = div_magic(e, nrw, f"{kernel} new-row channel")
-        rem = e - c * nrw
-        div_magic(rem, Wpad, f"{kernel} new-row row")
+        if rs & 1:
+            # wave w, step it: channel w + 12 it (< nch), lane u (< Wpad); each cell once
+            c = np.repeat(w_it[w_it < nch], 64)
+            rem = np.tile(lane, int((w_it < nch).sum()))
+            keep = rem < Wpad
+            c, rem = c[keep], rem[keep]
+            need(np.array_equal(np.sort(c * Wpad + rem), np.arange(nch * Wpad)),
+                 f"{kernel}: new-row cells not staged once")
+            cg, x = c_lo + c, rem - g["P"]
+            for n, oh in ((0, 1), (g["N"] - 1, g["Hout"] - 1)):
+                y = oh * S + Hf - 1 - g["P"]
+                live = (cg < g["C"]) & (x >= 0) & (x < g["Win"]) & (0 <= y < g["Hin"])
+                glob(kernel, "X new row (row-mapped)",
+                     (n * g["C"] * g["Hin"] * g["Win"] + (cg * g["Hin"] + y) * g["Win"] + x)[live],
+                     g["N"] * g["C"] * g["Hin"] * g["Win"])
+        else:
+            need(nch * nrw <= 768 * 5, f"{kernel}: new rows exceed the staging registers")
+            e = np.arange(nch * nrw)
+            c = div_magic(e, nrw, f"{kernel} new-row channel")
+            rem = e - c * nrw
+            div_magic(rem, Wpad, f"{kernel} new-row row")
         for oh in range(min(g["Hout"], 2 * Hf + 2)):
             s0 = (oh * S + Hf - nr) % Hf
             wrap, ring = (Hf - s0) * Wpad, Hf * Wpad

@@ -132,6 +132,8 @@ PLANTS = [
     ("lenet_conv2", "backward_filter", "window_rows", -1, "LDS size"),
     ("lenet_conv1", "backward_data", "window_rows", -1, "LDS size"),
     ("lenet_conv2", "forward", "slice_stride", -2, "slice layout"),
+    ("resnet_conv", "backward_filter", "row_staged", 2, "row staging"),
+    ("resnet_conv", "backward_filter", "row_staged", -1, "row staging"),
 ]
 
 

@@ -999,18 +999,34 @@ void (*ring_kernel(int nbw))(WgradArgs)
                                 : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB, RM>);
 }
 
+// Blocks resident at once for a launch of kernel k, taken as the smaller of k's
+// and its other zero-skip instantiation's (kz, or null): the two can differ in
+// registers and so in occupancy, and the split count -- with it the summation
+// order -- then stays the same under either zero-skip mode.
+int common_slots(void (*k)(WgradArgs), void (*kz)(WgradArgs), int threads, size_t lds)
+{
+    int slots = resident_slots(k, threads, lds);
+    if (kz && allow_dynamic_lds(kz, lds) == hipSuccess)
+        slots = std::min(slots, resident_slots(kz, threads, lds));
+    return slots;
+}
+
 template <typename T, bool ZSKIP, bool PB>
 hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
     void (*k)(WgradArgs);
-    if constexpr (PB)
+    void (*kz)(WgradArgs) = nullptr;
+    if constexpr (PB) {
         k = ring_kernel<T, ZSKIP, PB, false>(p.NBW);
-    else
+    } else {
         k = p.rowmap ? ring_kernel<T, ZSKIP, PB, true>(p.NBW) : ring_kernel<T, ZSKIP, PB, false>(p.NBW);
+        kz = p.rowmap ? ring_kernel<T, !ZSKIP, PB, true>(p.NBW)
+                      : ring_kernel<T, !ZSKIP, PB, false>(p.NBW);
+    }
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
-    int splits = resident_slots(k, kRingThreads, p.lds) / per_split;
+    int splits = common_slots(k, kz, kRingThreads, p.lds) / per_split;
     if (splits > p.splits) splits = p.splits;
     if (splits < 1) splits = 1;
     a.splits = splits;
@@ -1031,12 +1047,17 @@ hipError_t launch_w(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t
     auto k = p.NBW == 3 ? conv_wgrad_kernel<T, 3, ZSKIP, PB>
                         : (p.NBW == 2 ? conv_wgrad_kernel<T, 2, ZSKIP, PB>
                                       : conv_wgrad_kernel<T, 1, ZSKIP, PB>);
+    void (*kz)(WgradArgs) = nullptr;  // the other zero-skip form (the pooled source has none)
+    if constexpr (!PB)
+        kz = p.NBW == 3 ? conv_wgrad_kernel<T, 3, !ZSKIP, PB>
+                        : (p.NBW == 2 ? conv_wgrad_kernel<T, 2, !ZSKIP, PB>
+                                      : conv_wgrad_kernel<T, 1, !ZSKIP, PB>);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     // One resident round: as many splits as the device holds blocks at once (a
     // second, partial round would nearly double the time), within the workspace.
     const int per_split = p.nkr * p.nft;
-    int slots = resident_slots(k, kThreads, p.lds);
+    int slots = common_slots(k, kz, kThreads, p.lds);
     int splits = slots / per_split;
     // at most p.splits: at least kMinTiles tiles per split (tiny layers would
     // otherwise spend their time in block start-up and in the split reduction)

@@ -4,9 +4,9 @@
  *
  * Source of the semantics: "Deep Learning with Apache SystemML" (Pansare et
  * al., arXiv 1802.04647).
- *   - Section 3, "Tensor Representation": a tensor [N, C, H, W] is stored as a
- *     matrix with N rows and C*H*W columns (all but the first dimension are
- *     linearised).  Reading used throughout: row-major, column index
+ *   - Section 3, "Tensor Representation": a tensor [N, C, H, W] is stored as an
+ *     N x (C*H*W) matrix, the dimensions after the first folded into the
+ *     column index.  Reading used throughout: row-major, column index
  *     c*H*W + h*W + w.  Filters are F x (C*Hf*Wf) with column c*Hf*Wf + i*Wf + j.
  *   - Section 3, "Builtin NN Functions": conv2d and pooling, and their backward
  *     functions, are builtins.

@@ -12,8 +12,8 @@
  * independent output elements, so results do not depend on the thread count.
  *
  * Data layout (paper, Section 3 "Tensor Representation"): a 4-d tensor
- * [N, C, H, W] is a matrix with N rows and C*H*W columns; all but the first
- * dimension are linearised.  Reading used here: row-major in the listed order,
+ * [N, C, H, W] is an N x (C*H*W) matrix: the dimensions after the first are
+ * folded into the column index.  Reading used here: row-major in the listed order,
  * i.e. column index c*H*W + h*W + w.  Filters are F x (C*Hf*Wf) with column
  * c*Hf*Wf + i*Wf + j; the conv bias has one entry per filter.
  *

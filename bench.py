@@ -676,8 +676,9 @@ def cpu_baselines_lenet(target_s=4.0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the data-parallel "
-              "multi-GPU path is a design note, not part of this build.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this library has "
+              "no multi-GPU path (how the layer would shard is described in its design notes).",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():

@@ -543,6 +543,18 @@ def aux_kernel_timing():
     hbm("softmax_xent", 4 * S.numel() * 8 + 8,
         lambda: dmlnn.softmax_xent(S, Y, loss=loss, dscores=dS, probs=P),
         "64 x 10 fp64 (config 4): latency-bound")
+    # the same op over a large batch: the rows spread over 2048 blocks
+    NL = 1 << 21
+    SL = torch.randn((NL, 10), dtype=f64, device="cuda", generator=g)
+    YL = torch.zeros((NL, 10), dtype=f64, device="cuda")
+    YL[torch.arange(NL, device="cuda"), torch.arange(NL, device="cuda") % 10] = 1.0
+    dSL, PL = torch.empty_like(SL), torch.empty_like(SL)
+    wsl = torch.empty(dmlnn.softmax_xent_workspace_size(f64, NL, 10), dtype=torch.uint8,
+                      device="cuda")
+    hbm("softmax_xent_large", 4 * SL.numel() * 8 + 8,
+        lambda: dmlnn.softmax_xent(SL, YL, loss=loss, dscores=dSL, probs=PL, workspace=wsl),
+        f"{NL} x 10 fp64, scores and labels read, probs and dscores written")
+    del SL, YL, dSL, PL
     # affine 3136 -> 512 of the LeNet step (config 4), fp64 MFMA
     A = torch.randn((64, 3136), dtype=f64, device="cuda", generator=g)
     Wa = torch.randn((3136, 512), dtype=f64, device="cuda", generator=g) * 0.02

@@ -451,9 +451,28 @@ DMLNN_API int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, con
  *   loss    = -(1/N) sum_{n,k} Y[n,k] * log p[n,k]   (one device scalar)
  *   dscores = (p * sum_k Y[n,k] - Y) / N
  * scores, Y, probs, dscores are N x K; probs may be NULL; loss points to one
- * element of dtype in device memory.  Deterministic reduction order. */
+ * element of dtype in device memory.
+ * workspace (optional, workspace_bytes long): without one, a single block of
+ * 1024 threads does the whole call, which suits small batches.  With one, the
+ * rows are spread over as many blocks as the workspace has elements, up to the
+ * number softmax_xent_workspace_size asks room for (2048 at most).  Each block
+ * writes its share of the loss there, and a second pass adds the shares in
+ * block order.  The result is deterministic for a given block count, which
+ * depends only on N, K and workspace_bytes.  The one-block and many-block forms
+ * add the row losses in different orders, so the last bits of the loss can
+ * differ between them; dscores and probs are the same in both.  The workspace
+ * must be element aligned and overlap none of the call's tensors (DMLNN_ERR_ARG);
+ * its contents on entry are ignored.  Calls that may run at the same time need
+ * separate workspaces. */
 DMLNN_API int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *probs,
-                 void *dscores, void *loss, int N, int K, void *stream);
+                 void *dscores, void *loss, int N, int K, void *workspace,
+                 size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace softmax_xent uses at most for these sizes: one element of
+ * dtype per block.  A block takes 16 x (64 / sw) rows, sw being the smallest
+ * power of two >= K (at most 64), so the size is 0 when one block covers all N
+ * rows (for K = 10, N <= 64).  Returns 0 for invalid arguments. */
+DMLNN_API size_t softmax_xent_workspace_size(dmlnn_dtype dtype, int N, int K);
 
 /* ------------------------------------------------------------- softmax_fwd ----
  * Paper: Section 2 (the softmax layer's forward), used alone for forward-only

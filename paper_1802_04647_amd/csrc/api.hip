@@ -678,8 +678,8 @@ int affine_plan(dmlnn_dtype dtype, int product, int N, int D, int M, size_t work
 
 // An affine workspace is optional; when given it must be element aligned and
 // must not overlap the tensors the call reads or writes.
-static int affine_workspace_ok(const char *name, dmlnn_dtype dtype, void *ws, size_t ws_bytes,
-                               std::initializer_list<std::pair<const void *, size_t>> tensors)
+static int workspace_ok(const char *name, dmlnn_dtype dtype, void *ws, size_t ws_bytes,
+                        std::initializer_list<std::pair<const void *, size_t>> tensors)
 {
     if (!ws || ws_bytes == 0) return DMLNN_OK;
     const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
@@ -699,7 +699,7 @@ int affine_fwd(dmlnn_dtype dtype, const void *X, const void *W, const void *b, v
         return fail(DMLNN_ERR_ARG, "affine_fwd: bad sizes N=%d D=%d M=%d", N, D, M);
     if (relu != 0 && relu != 1) return fail(DMLNN_ERR_ARG, "affine_fwd: relu must be 0 or 1");
     const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
-    if (int r = affine_workspace_ok("affine_fwd", dtype, workspace, workspace_bytes,
+    if (int r = workspace_ok("affine_fwd", dtype, workspace, workspace_bytes,
                                     {{X, (size_t)N * D * esz}, {W, (size_t)D * M * esz},
                                      {b, (size_t)M * esz}, {out, (size_t)N * M * esz}}))
         return r;
@@ -721,7 +721,7 @@ int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W
     if (relu_input != 0 && relu_input != 1)
         return fail(DMLNN_ERR_ARG, "affine_bwd: relu_input must be 0 or 1");
     const size_t esz = dtype == DMLNN_F64 ? 8 : 4;
-    if (int r = affine_workspace_ok("affine_bwd", dtype, workspace, workspace_bytes,
+    if (int r = workspace_ok("affine_bwd", dtype, workspace, workspace_bytes,
                                     {{dout, (size_t)N * M * esz}, {X, (size_t)N * D * esz},
                                      {W, (size_t)D * M * esz}, {out_fwd, (size_t)N * M * esz},
                                      {dX, (size_t)N * D * esz}, {dW, (size_t)D * M * esz},
@@ -736,16 +736,26 @@ int affine_bwd(dmlnn_dtype dtype, const void *dout, const void *X, const void *W
                     "affine_bwd");
 }
 
+size_t softmax_xent_workspace_size(dmlnn_dtype dtype, int N, int K)
+{
+    if (!dtype_ok(dtype) || !count_ok(N, K)) return 0;
+    return dmlnn::softmax_xent_workspace_bytes(dtype, N, K);
+}
+
 int softmax_xent(dmlnn_dtype dtype, const void *scores, const void *Y, void *probs, void *dscores,
-                 void *loss, int N, int K, void *stream)
+                 void *loss, int N, int K, void *workspace, size_t workspace_bytes, void *stream)
 {
     if (!dtype_ok(dtype)) return fail(DMLNN_ERR_DTYPE, "softmax_xent: bad dtype %d", (int)dtype);
     if (!scores || !Y || !dscores || !loss)
         return fail(DMLNN_ERR_NULL, "softmax_xent: scores, Y, dscores and loss are required");
     if (!count_ok(N, K)) return fail(DMLNN_ERR_ARG, "softmax_xent: bad sizes N=%d K=%d", N, K);
+    const size_t esz = dtype == DMLNN_F64 ? 8 : 4, nk = (size_t)N * K * esz;
+    if (int r = workspace_ok("softmax_xent", dtype, workspace, workspace_bytes,
+                             {{scores, nk}, {Y, nk}, {probs, nk}, {dscores, nk}, {loss, esz}}))
+        return r;
     if (int r = device_check()) return r;
     return launched(dmlnn::launch_softmax_xent(dtype, scores, Y, probs, dscores, loss, N, K,
-                                               (hipStream_t)stream),
+                                               workspace, workspace_bytes, (hipStream_t)stream),
                     "softmax_xent");
 }
 

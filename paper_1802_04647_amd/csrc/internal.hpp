@@ -123,8 +123,11 @@ hipError_t launch_affine_bwd(int dtype, const void *dout, const void *X, const v
                              const void *out_fwd, void *dX, void *dW, void *db, int N, int D,
                              int M, int relu_input, void *workspace, size_t workspace_bytes,
                              hipStream_t s);
+// ws: null, or ws_bytes of scratch for the blocks' loss shares (see softmax.hip)
 hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
-                               void *loss, int N, int K, hipStream_t s);
+                               void *loss, int N, int K, void *ws, size_t ws_bytes,
+                               hipStream_t s);
+size_t softmax_xent_workspace_bytes(int dtype, int N, int K);
 hipError_t launch_softmax(int dtype, const void *S, void *P, int N, int K, hipStream_t s);
 hipError_t launch_sgd_momentum(int dtype, void *theta, const void *grad, void *v, double lr,
                                double mu, long long n, hipStream_t s);

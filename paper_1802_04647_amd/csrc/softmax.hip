@@ -5,8 +5,10 @@
 //   p = exp(s - m) / sum exp(s - m)
 //   row loss = -sum_k y (s - m - log sum exp(s - m))
 //   ds = (p * sum_k y - y) / N
-// and loss = (1/N) * sum of row losses.  One block of 16 waves; lanes run across
-// the K columns of a row with butterfly-shuffle reductions.
+// and loss = (1/N) * sum of row losses.  Blocks of 16 waves; lanes run across
+// the K columns of a row with butterfly-shuffle reductions.  One block does the
+// whole call, or (with a workspace) up to kSmMaxBlocks blocks each write their
+// share of the loss to the workspace and a one-wave pass adds the shares.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -14,9 +16,10 @@ namespace dmlnn {
 namespace {
 
 // Rows are processed by lane segments of width sw (a power of two >= K, at most
-// 64): a wave holds 64/sw rows at once and the 16 waves of the block take
-// consecutive row groups.  Per-row losses are summed per segment in row order,
-// then over (wave, segment) in order: the loss is deterministic.
+// 64): a wave holds 64/sw rows at once and the waves of the grid (16 a block)
+// take consecutive row groups.  Per-row losses are summed per segment in row
+// order, then over (wave, segment) in order within a block, then over blocks in
+// block order: the loss is deterministic for a given block count.
 template <typename T>
 __device__ __forceinline__ T seg_sum(T v, int sw)
 {
@@ -36,22 +39,26 @@ __device__ __forceinline__ T seg_max(T v, int sw)
 
 constexpr int kSmThreads = 1024;
 constexpr int kSmWaves = kSmThreads / kWave;
+constexpr int kSmMaxBlocks = 2048;  // blocks of a call with a workspace (one loss share each)
 
+// part: null (one block: the loss goes to *loss) or one element a block (the
+// block's share of the sum of row losses, before the 1/N).
 template <typename T>
 __global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, const T *Y, T *P,
-                                                                  T *dS, T *loss, int N, int K,
-                                                                  int sw)
+                                                                  T *dS, T *loss, T *part, int N,
+                                                                  int K, int sw)
 {
     __shared__ T s_part[kSmThreads];
     const int lane = lane_id(), wave = wave_id();
     const int rpw = kWave / sw, seg = lane / sw, sl = lane - seg * sw;
+    const int wave_g = blockIdx.x * kSmWaves + wave, nwaves = gridDim.x * kSmWaves;
     const T invN = T(1) / T(N);
     T total = T(0);
     if (K <= sw) {
         // At most one column per lane: s and y are loaded once, into registers,
         // and each exponential is taken once (the same values and reduction
         // order as the general loop below).
-        for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
+        for (int r0 = wave_g * rpw; r0 < N; r0 += nwaves * rpw) {
             const int n = r0 + seg;
             const bool ok = n < N && sl < K;
             const size_t o = ok ? (size_t)n * K + sl : 0;
@@ -70,7 +77,7 @@ __global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, co
             if (n < N) total += rl;
         }
     } else {
-        for (int r0 = wave * rpw; r0 < N; r0 += kSmWaves * rpw) {
+        for (int r0 = wave_g * rpw; r0 < N; r0 += nwaves * rpw) {
             const int n = r0 + seg;
             const bool ok = n < N;
             const T *s = S + (size_t)n * K;
@@ -117,8 +124,23 @@ __global__ __launch_bounds__(kSmThreads) void softmax_xent_kernel(const T *S, co
             for (int u = 0; u < 16; ++u)
                 if (i0 + u < nseg) t += v[u];
         }
-        *loss = t * invN;
+        if (part)
+            part[blockIdx.x] = t;
+        else
+            *loss = t * invN;
     }
+}
+
+// The loss from the blocks' shares: lane l adds shares l, l + 64, ... in order,
+// then a fixed butterfly adds the 64 lane sums (lane 0 ends with the total).
+template <typename T>
+__global__ __launch_bounds__(kWave) void softmax_loss_reduce(const T *part, int G, T *loss, int N)
+{
+    const int lane = threadIdx.x;
+    T t = T(0);
+    for (int b = lane; b < G; b += kWave) t += part[b];
+    for (int off = kWave / 2; off > 0; off >>= 1) t += __shfl_xor(t, off, kWave);
+    if (lane == 0) *loss = t * (T(1) / T(N));
 }
 
 // Row-wise softmax alone (forward-only scoring): same segment layout, no loss.
@@ -177,20 +199,58 @@ hipError_t launch_softmax(int dtype, const void *S, void *P, int N, int K, hipSt
     return hipGetLastError();
 }
 
-hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
-                               void *loss, int N, int K, hipStream_t s)
+namespace {
+
+int softmax_segment(int K)
 {
     int sw = 1;
     while (sw < K && sw < kWave) sw <<= 1;
-    if (dtype == 0)
-        hipLaunchKernelGGL(softmax_xent_kernel<double>, dim3(1), dim3(kSmThreads), 0, s,
-                           (const double *)S, (const double *)Y, (double *)P, (double *)dS,
-                           (double *)loss, N, K, sw);
-    else
-        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3(1), dim3(kSmThreads), 0, s,
-                           (const float *)S, (const float *)Y, (float *)P, (float *)dS,
-                           (float *)loss, N, K, sw);
+    return sw;
+}
+
+// Blocks a call would use with an unbounded workspace: one per 16 waves' rows,
+// at most kSmMaxBlocks.
+long long softmax_blocks(int N, int K)
+{
+    const long long rows_per_block = (long long)kSmWaves * (kWave / softmax_segment(K));
+    return std::min<long long>((N + rows_per_block - 1) / rows_per_block, kSmMaxBlocks);
+}
+
+template <typename T>
+hipError_t launch_xent(const void *S, const void *Y, void *P, void *dS, void *loss, int N, int K,
+                       void *ws, size_t ws_bytes, hipStream_t s)
+{
+    const int sw = softmax_segment(K);
+    long long G = ws ? std::min<long long>(softmax_blocks(N, K), (long long)(ws_bytes / sizeof(T)))
+                     : 1;
+    if (G <= 1) {
+        hipLaunchKernelGGL(softmax_xent_kernel<T>, dim3(1), dim3(kSmThreads), 0, s,
+                           (const T *)S, (const T *)Y, (T *)P, (T *)dS, (T *)loss, (T *)nullptr,
+                           N, K, sw);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(softmax_xent_kernel<T>, dim3((int)G), dim3(kSmThreads), 0, s, (const T *)S,
+                       (const T *)Y, (T *)P, (T *)dS, (T *)loss, (T *)ws, N, K, sw);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(softmax_loss_reduce<T>, dim3(1), dim3(kWave), 0, s, (const T *)ws, (int)G,
+                       (T *)loss, N);
     return hipGetLastError();
+}
+
+}  // namespace
+
+size_t softmax_xent_workspace_bytes(int dtype, int N, int K)
+{
+    const long long G = softmax_blocks(N, K);
+    return G > 1 ? (size_t)G * (dtype == 0 ? sizeof(double) : sizeof(float)) : 0;
+}
+
+hipError_t launch_softmax_xent(int dtype, const void *S, const void *Y, void *P, void *dS,
+                               void *loss, int N, int K, void *ws, size_t ws_bytes, hipStream_t s)
+{
+    return dtype == 0 ? launch_xent<double>(S, Y, P, dS, loss, N, K, ws, ws_bytes, s)
+                      : launch_xent<float>(S, Y, P, dS, loss, N, K, ws, ws_bytes, s);
 }
 
 }  // namespace dmlnn

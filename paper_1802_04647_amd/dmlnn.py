@@ -90,7 +90,8 @@ def load():
         "affine_fwd": (_i, [_i, _vp, _vp, _vp, _vp] + [_i] * 4 + [_vp, ctypes.c_size_t, _vp]),
         "affine_bwd": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _vp, _vp] + [_i] * 4
                        + [_vp, ctypes.c_size_t, _vp]),
-        "softmax_xent": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _vp]),
+        "softmax_xent": (_i, [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _vp, ctypes.c_size_t, _vp]),
+        "softmax_xent_workspace_size": (ctypes.c_size_t, [_i, _i, _i]),
         "sgd_momentum_update": (_i, [_i, _vp, _vp, _vp, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_longlong, _vp]),
         "softmax_fwd": (_i, [_i, _vp, _vp, _i, _i, _vp]),
@@ -611,8 +612,17 @@ def affine_bwd(dout, X, W, out_fwd=None, want_dX=True, want_db=True, dX=None, dW
     return dX, dW, db
 
 
-def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None, stream=None):
-    """Returns (loss as a 1-element device tensor, dscores, probs-or-None)."""
+def softmax_xent_workspace_size(dtype, N, K) -> int:
+    """Bytes of workspace softmax_xent spreads its rows over (0: one block)."""
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return int(load().softmax_xent_workspace_size(dt, N, K))
+
+
+def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None, stream=None,
+                 workspace=None):
+    """Returns (loss as a 1-element device tensor, dscores, probs-or-None).
+    workspace: None (a fresh one of the full size), a byte tensor, or an
+    empty tensor (none: one block does the call)."""
     dt = _dtype(scores, Y, loss, dscores, probs)
     N, K = scores.shape
     if loss is None:
@@ -625,8 +635,13 @@ def softmax_xent(scores, Y, want_probs=True, loss=None, dscores=None, probs=None
     _need(dscores, N * K, "dscores")
     _need(probs, N * K, "probs")
     _need(loss, 1, "loss")
+    if workspace is None:
+        nb = softmax_xent_workspace_size(dt, N, K)
+        workspace = torch.empty(nb, dtype=torch.uint8, device=scores.device) if nb else None
+    ws, nb = (None, 0) if workspace is None or workspace.numel() == 0 else (
+        _p(workspace), workspace.numel() * workspace.element_size())
     _check("softmax_xent", load().softmax_xent(dt, _p(scores), _p(Y), _p(probs), _p(dscores),
-                                                _p(loss), N, K, _stream(stream)))
+                                                _p(loss), N, K, ws, nb, _stream(stream)))
     return loss, dscores, probs
 
 

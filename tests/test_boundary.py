@@ -24,7 +24,7 @@ def test_exports_every_declared_symbol(lib):
     expected = {"conv2d_out_dim", "conv2d_forward", "conv2d_backward_filter_workspace_size",
                 "conv2d_backward_filter", "conv2d_backward_data", "dmlnn_set_zero_skip",
                 "bias_add_relu", "max_pool2d_fwd", "max_pool2d_bwd", "affine_fwd", "affine_bwd",
-                "affine_workspace_size",
+                "affine_workspace_size", "softmax_xent_workspace_size",
                 "softmax_xent", "sgd_momentum_update", "count_nonzero", "dmlnn_last_error"}
     assert expected <= set(names)
     for n in names:
@@ -112,7 +112,7 @@ def test_other_validation(lib):
                           None) == ERR_NULL
     assert lib.affine_bwd(0, None, FAKE, FAKE, None, FAKE, FAKE, None, 2, 3, 4, 0, None, 0,
                           None) == ERR_NULL
-    assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None) == ERR_NULL
+    assert lib.softmax_xent(0, FAKE, FAKE, None, FAKE, None, 2, 3, None, 0, None) == ERR_NULL
     assert lib.sgd_momentum_update(0, FAKE, FAKE, FAKE, 0.1, 0.9, 0, None) == ERR_ARG
     assert lib.count_nonzero(3, FAKE, 10, FAKE, None) == ERR_DTYPE
 
@@ -139,6 +139,25 @@ def test_affine_workspace(lib):
     assert lib.affine_bwd(0, X, W, out, None, W + 8, None, None, 2, 3, 4, 1, None, 0,
                           None) == ERR_ARG
     assert "relu_input" in dmlnn.last_error()
+
+
+def test_softmax_xent_workspace(lib):
+    """One element per block of 16 x (64 / sw) rows (sw = the power of two
+    segment a row takes), up to 2048 blocks; none when one block covers the
+    batch (the LeNet step's 64 x 10); bad workspaces rejected before any launch."""
+    f = lib.softmax_xent_workspace_size
+    assert f(0, 64, 10) == 0                        # 64 rows a block at K = 10
+    assert f(0, 65, 10) == 2 * 8
+    assert f(1, 65, 10) == 2 * 4
+    assert f(0, 1024, 1) == 0 and f(0, 1025, 1) == 2 * 8
+    assert f(0, 17, 130) == 2 * 8                   # 16 rows a block at K > 64
+    assert f(0, 1 << 20, 10) == 2048 * 8            # capped
+    assert f(0, 0, 10) == 0 and f(3, 100, 10) == 0  # bad sizes, bad dtype
+    S, Y, dS, loss, ws = 0x100000, 0x200000, 0x300000, 0x400000, 0x500000
+    assert lib.softmax_xent(0, S, Y, None, dS, loss, 100, 10, ws + 4, 64, None) == ERR_ARG
+    assert "workspace" in dmlnn.last_error()
+    assert lib.softmax_xent(0, S, Y, None, dS, loss, 100, 10, dS + 800, 64, None) == ERR_ARG
+    assert lib.softmax_xent(0, S, Y, None, dS, loss, 100, 10, loss - 8, 64, None) == ERR_ARG
 
 
 def test_zero_skip_mode(lib):

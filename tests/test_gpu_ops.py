@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import assert_close, dev, host, rounded
+from gpu_util import TORCH_DT, assert_close, dev, host, rounded
 from paper_1802_04647_amd import dmlnn
 from paper_1802_04647_amd.inputs import rng
 
@@ -223,6 +223,36 @@ def test_softmax_xent_parity(NK, dt):
     assert abs(host(loss)[0] - rl) <= {"f64": 1e-10, "f32": 1e-4}[dt] * max(abs(rl), 1e-300)
     assert_close(host(dS), rdS, dt, "dscores")
     assert_close(host(P), rP, dt, "probs")
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("NK", [(100003, 10), (3001, 130), (5000, 1)], ids=str)
+def test_softmax_xent_many_blocks(NK, dt):
+    """Batches past one block: with the workspace the rows spread over many
+    blocks and the loss shares are added in block order.  Against the oracle,
+    bitwise the same on a second call, and dscores / probs bitwise equal to the
+    one-block form (only the loss's summation order differs between forms)."""
+    N, K = NK
+    g = rng(45)
+    S = rounded(g.standard_normal((N, K)) * 3, dt)
+    Y = np.eye(K)[g.integers(0, K, N)]
+    nb = dmlnn.softmax_xent_workspace_size(TORCH_DT[dt], N, K)
+    assert nb > 8
+    print(f"\n[gpu] softmax_xent N={N} K={K} {dt} workspace {nb} B", flush=True)
+    Sd, Yd = dev(S, dt), dev(Y, dt)
+    loss, dS, P = dmlnn.softmax_xent(Sd, Yd)
+    loss2, dS2, P2 = dmlnn.softmax_xent(Sd, Yd)
+    loss1, dS1, P1 = dmlnn.softmax_xent(Sd, Yd, workspace=torch.empty(0, dtype=torch.uint8,
+                                                                         device=Sd.device))
+    torch.cuda.synchronize()
+    rl, rdS, rP = oracle.softmax_xent(S, Y)
+    tol = {"f64": 1e-10, "f32": 1e-4}[dt]
+    for got in (loss, loss1):
+        assert abs(host(got)[0] - rl) <= tol * max(abs(rl), 1e-300)
+    assert_close(host(dS), rdS, dt, "dscores")
+    assert_close(host(P), rP, dt, "probs")
+    assert torch.equal(loss, loss2) and torch.equal(dS, dS2) and torch.equal(P, P2)
+    assert torch.equal(dS, dS1) and torch.equal(P, P1)
 
 
 def test_softmax_uniform_scores_closed_form():

@@ -76,6 +76,9 @@ class LeNetTrainer:
                  dmlnn.affine_workspace_size(dtype, N, 512, 10))
         self.wsa = torch.empty(wa, dtype=torch.uint8, device=device)
         self.wsa_side = torch.empty(wa, dtype=torch.uint8, device=device)
+        # the loss shares of softmax_xent's blocks (none at batch <= 64: one block)
+        self.wss = torch.empty(dmlnn.softmax_xent_workspace_size(dtype, N, 10), dtype=torch.uint8,
+                               device=device)
         # The weight gradients of affine 1 and conv2 run on a second stream
         # (default priority), beside the data-gradient chain (affine 1 dX, pool
         # backward, conv2 backward_data, ...): they only share read-only inputs,
@@ -101,7 +104,7 @@ class LeNetTrainer:
         dmlnn.affine_fwd(self.h, p["W4"], p["b4"], relu=False, out=self.s, workspace=self.wsa,
                          stream=ms)
         dmlnn.softmax_xent(self.s, Y, want_probs=False, loss=self.loss, dscores=self.ds,
-                           stream=ms)
+                           workspace=self.wss, stream=ms)
         # dh comes out masked by h > 0 (the relu backward of affine 1, folded
         # into this product), so affine 1's backward reads no mask
         dmlnn.affine_bwd(self.ds, self.h, p["W4"], None, dX=self.dh, dW=g["W4"], db=g["b4"],

@@ -10,6 +10,7 @@ from paper_1802_04647_amd import dmlnn
 from test_gpu_ops import AFFINE, SPLIT
 
 SHAPES = sorted(set(AFFINE) | set(SPLIT) | {(20, 96, 40), (64, 512, 10), (64, 3136, 512),
+                                             (100, 512, 10), (100, 3136, 512),
                                              (33, 70, 65), (5, 7, 3)})
 DT = {"f64": torch.float64, "f32": torch.float32}
 

@@ -47,6 +47,25 @@ def test_lenet_training_steps(steps, fused):
         assert_close(host(tr.v[k]).reshape(v[k].shape), v[k], "f64", "velocity " + k)
 
 
+def test_lenet_training_step_batch_100():
+    """A batch past one softmax block (100 rows of 10 classes: two blocks and
+    their loss shares in the trainer's workspace), and past the 64-image tiles
+    of the conv and affine kernels, against the oracle step."""
+    print("\n[gpu] lenet training step, batch 100", flush=True)
+    X, Y, params = lenet_train_inputs(100)
+    assert dmlnn.softmax_xent_workspace_size(torch.float64, 100, 10) == 2 * 8
+    tr = LeNetTrainer(params, N=100)
+    loss = tr.step(dev(X, "f64"), dev(Y, "f64"))
+    torch.cuda.synchronize()
+    ref_loss, p, v, g, a = lenet_oracle.train_step(X, Y, params,
+                                                   lenet_oracle.zero_velocities(params))
+    assert abs(host(loss)[0] - ref_loss) <= 1e-10 * abs(ref_loss)
+    assert np.array_equal(tr.i2.cpu().numpy(), a["i2"])
+    for k in PARAM_ORDER:
+        assert_close(host(tr.g[k]).reshape(g[k].shape), g[k], "f64", "grad " + k)
+        assert_close(host(tr.p[k]).reshape(p[k].shape), p[k], "f64", "param " + k)
+
+
 def test_lenet_conv2_pool_chain():
     s = SHAPES["lenet_conv2"]
     X, W, b, dP = conv_layer_inputs("lenet_conv2")

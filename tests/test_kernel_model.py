@@ -61,9 +61,12 @@ def _cases():
     for s, _ in SPARSE_CASES:
         cases.add((s, "csr_input", None))
     cases.add((SHAPES["lenet_conv1"], "csr_input", None))
-    for name in ("lenet_conv1", "lenet_conv2"):  # the fused LeNet step
-        cases.add((SHAPES[name], "pool_epilogue", (2, 2, 2, 0)))
-        cases.add((SHAPES[name], "pooled_source", (2, 2, 2, 0)))
+    for name in ("lenet_conv1", "lenet_conv2"):  # the fused LeNet step, batch 64 and 100
+        for n in (SHAPES[name].N, 100):
+            s = ConvShape(n, *SHAPES[name].args()[1:])
+            cases.add((s, "plain", None))
+            cases.add((s, "pool_epilogue", (2, 2, 2, 0)))
+            cases.add((s, "pooled_source", (2, 2, 2, 0)))
     return sorted(cases, key=lambda c: (str(c[0]), c[1]))
 
 

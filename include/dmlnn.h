@@ -162,9 +162,12 @@ DMLNN_API int conv2d_backward_data(dmlnn_dtype dtype, const void *W, const void 
 /* Zero-skip mode for the conv2d kernels (paper, Section 3 "Sparse Operations":
  * a sparse-input / dense-filter operator does fewer floating-point operations).
  * mode 0 = dense (default), 1 = skip every MFMA step whose staged input
- * fragment is entirely zero (a wavefront ballot).  Results are bitwise equal
- * to the dense path up to the sign of zero results.  Process-wide setting;
- * returns the previous mode, or -1 for an invalid mode. */
+ * fragment is entirely zero (a wavefront ballot).  Where both modes run the
+ * same kernel, results are bitwise equal up to the sign of zero results.  The
+ * filter-resident forward has no skip form: with the skip on, that pass runs
+ * the LDS-DMA kernel, whose summation order differs (equal within rounding);
+ * conv2d_plan reports which kernel runs.  Process-wide setting; returns the
+ * previous mode, or -1 for an invalid mode. */
 DMLNN_API int dmlnn_set_zero_skip(int mode);
 
 /* ------------------------------------------------------------ conv2d_plan ----

@@ -224,9 +224,12 @@ typedef struct {
                           registers across the previous tile's MFMAs, 0 when staged directly */
     int fused;         /* conv2d_plan_fused: 1 when the fused kernel runs, 0 when the call
                           falls back to the plain kernels (then described here) */
-    int row_staged;    /* backward_filter row ring: tile staging a row per wave (each row a
-                          wave-uniform base plus the lane): bit 0 the new input row, bit 1
-                          the gradient tile; 0 where elements are dealt out to threads */
+    int row_staged;    /* backward_filter row ring, how a tile is staged: bit 0 the new
+                          input row a row per wave through registers (each row a
+                          wave-uniform base plus the lane), bit 1 the gradient tile the
+                          same way, bit 2 the new input row by LDS DMA into the one free
+                          slot of an Hf + 1 slot ring (then window_rows = Hf + 1); 0
+                          where elements are dealt out to threads */
 } dmlnn_conv_plan;
 
 DMLNN_API int conv2d_plan(dmlnn_dtype dtype, int pass, int N, int C, int Hin, int Win, int F,

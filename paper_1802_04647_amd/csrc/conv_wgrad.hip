@@ -60,6 +60,7 @@ struct WgradArgs {
     int rows_max;
     int spr;        // 0: tiles are runs of whole output rows; else slices per output row
     unsigned long long magic_rq, magic_wpad, magic_ch, magic_wout, magic_hwf, magic_wf;
+    int x_dma_insts;  // ring with the X rows by LDS DMA: 64-dword instructions a slot
     PoolSrc pool;   // PB kernels: g comes from a following max-pool's backward
     void *g_out;    // or null: g (dout masked to out_fwd > 0) is also written here
                     // (by the k-range-0 blocks, each element once)
@@ -471,14 +472,27 @@ constexpr int kRGP = 5; // pooled source: pool windows each thread stages per ti
 // division per element and a branch per staged element.
 constexpr int kRMG = (kBM + kRingWaves - 1) / kRingWaves;  // g rows a wave stages (6)
 constexpr int kRMX = 6;                                     // channels a wave stages
+// X rows by LDS DMA (XM = 2; stride 1, where the LDS holds it): the ring has
+// Hf + 1 slots, slot-major ([slot][channel][Wpad], the slot stride a whole
+// number of 64-dword DMA instructions plus a bank-spreading pad), so the next tile's new
+// row lands in the one slot the current tile does not read, straight from
+// global memory during the current tile's MFMAs: no staging registers, no LDS
+// stores, and no new-row work between the barriers.
 
-template <typename T, int NBW, bool ZSKIP, bool PB, bool RM>
+// XM: how the next tile's input row is staged: 0 an element a thread, 1 a row
+// a wave through registers, 2 by LDS DMA.
+template <typename T, int NBW, bool ZSKIP, bool PB, int XM>
 __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradArgs a)
 {
     using MF = Mfma<T>;
     extern __shared__ __align__(16) unsigned char smem[];
     T *s_g = reinterpret_cast<T *>(smem);
-    T *s_x = s_g + kBM * a.SG;  // [channel][slot][Wpad]
+    // XM < 2: [channel][slot][Wpad], CH = Hf * Wpad a channel; XM = 2:
+    // [slot][channel][Wpad], CH the slot stride
+    T *s_x = s_g + kBM * a.SG;
+    constexpr bool RM = XM == 1, XD = XM == 2;
+    const int R = XD ? a.rows_max : a.Hf;  // ring slots: Hf, or Hf + 1 with the DMA
+    auto xoff = [&](int c, int sl) { return XD ? sl * a.CH + c * a.Wpad : c * a.CH + sl * a.Wpad; };
 
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
     const int L = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -519,9 +533,10 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     };
 
     static_assert(!(PB && RM), "the pooled source has its own staging");
-    // fp64 row-maps the input rows only: a sixth g row a wave would spill
-    constexpr bool RMG = RM && sizeof(T) == 4;
-    constexpr int NG = PB ? 1 : (RMG ? kRMG : kRG), NP = PB ? kRGP : 1, NX = RM ? kRMX : kRX;
+    // fp64 keeps the element mapping for the g tile: a sixth g row a wave would spill
+    constexpr bool RMG = XM != 0 && !PB && sizeof(T) == 4;
+    constexpr int NG = PB ? 1 : (RMG ? kRMG : kRG), NP = PB ? kRGP : 1;
+    constexpr int NX = RM ? kRMX : kRX;  // (unused with the DMA)
     T vg[NG], vm[NG], vx[NX];
     // Pooled source: element e of a row is (filter row r, pool column px): the
     // window's three values are loaded once and its PS cells of the row written
@@ -717,14 +732,37 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
     // once it reaches Hf.  Magic and reciprocal divisions (e < 2^16, rw < 2^22):
     // this runs between the barriers with the matrix pipe idle.
     auto stage_x_full = [&](int n, int oh) {
-        const int tot = nch * a.CH;
-        const int rot0 = (oh * a.S) % a.Hf;
+        const int tot = XD ? nch * a.Hf * a.Wpad : nch * a.CH;  // (CH = Hf * Wpad without the DMA)
+        const int rot0 = (oh * a.S) % R;
         const float rcp_hf = 1.0f / (float)a.Hf;
         for (int e = tid; e < tot; e += kRingThreads) {
             const int rw = div_magic(e, a.magic_wpad), u = e - rw * a.Wpad;
             const int c = div_small(rw, a.Hf, rcp_hf), t = rw - c * a.Hf;
-            const int sl = rot0 + t - (rot0 + t >= a.Hf ? a.Hf : 0);
-            s_x[c * a.CH + sl * a.Wpad + u] = x_at(n, c, oh * a.S + t, u);
+            const int sl = rot0 + t - (rot0 + t >= R ? R : 0);
+            s_x[xoff(c, sl) + u] = x_at(n, c, oh * a.S + t, u);
+        }
+    };
+    // XD: the new row yr = oh + Hf - 1 of tile oh (stride 1) into slot yr mod R,
+    // every channel of the k range: dword d of the slot (instruction d / 64,
+    // taken by wave (d / 64) mod 12) is element d / (sizeof(T) / 4) = (channel c,
+    // column u); the padding columns, the channels past the range and the
+    // rows outside the image load zeros (an offset past the buffer).
+    auto dma_x = [&](int n, int oh) {
+        const int yr = oh + a.Hf - 1, y = yr - a.P, sl = yr % R;
+        const size_t img = (size_t)a.C * a.Hin * a.Win;
+        const i32x4 rs = buffer_rsrc(X + (size_t)n * img, (unsigned)(img * sizeof(T)));
+        const int ln = opaque(threadIdx.x) & (kWave - 1);
+        constexpr int EPI = kWave * 4 / (int)sizeof(T);  // elements an instruction moves
+        for (int i = wave; i < a.x_dma_insts; i += kRingWaves) {
+            const int d = i * kWave + ln;
+            const int e = sizeof(T) == 8 ? d >> 1 : d;
+            const int half = sizeof(T) == 8 ? (d & 1) : 0;
+            const int c = div_magic(e, a.magic_wpad), u = e - c * a.Wpad;
+            const int cg = c_lo + c, x = u - a.P;
+            const bool ok = c < nch && cg < a.C && x >= 0 && x < a.Win && y >= 0 && y < a.Hin;
+            const int vo = ok ? (int)(((cg * a.Hin + y) * a.Win + x) * (int)sizeof(T)) + 4 * half
+                              : kDmaZero;  // < the image's bytes < 2^31
+            dma_dword(rs, s_x + sl * a.CH + i * EPI, vo, 0);
         }
     };
 
@@ -747,7 +785,12 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             const long long t1 = t_begin + 1;
             const int n1 = (int)(t1 / a.Hout), oh1 = (int)(t1 - (long long)n1 * a.Hout);
             load_g(n1, oh1);
-            if (oh1 != 0) load_x(n1, oh1);
+            if (oh1 != 0) {
+                if constexpr (XD)
+                    dma_x(n1, oh1);
+                else
+                    load_x(n1, oh1);
+            }
         }
     }
     const int lq = lane >> 4;
@@ -758,8 +801,8 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         const int n = cn, oh = coh;
         const int n1 = oh + 1 < a.Hout ? n : n + 1, oh1 = oh + 1 < a.Hout ? oh + 1 : 0;
         // LDS offset of column k = (c, i, j) of this lane's blocks: filter row i
-        // of this tile sits in slot (oh*S + i) mod Hf.
-        const int rot = (oh * a.S) % a.Hf;
+        // of this tile sits in slot (oh*S + i) mod R.
+        const int rot = (oh * a.S) % R;
         int kof[NBW];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb) {
@@ -767,8 +810,8 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
             const int c = div_magic(k, a.magic_hwf), t = k - c * a.HfWf;
             const int i = div_magic(t, a.magic_wf), j = t - i * a.Wf;
             int sl = rot + i;
-            sl -= sl >= a.Hf ? a.Hf : 0;
-            kof[nb] = k < kend ? (c - c_lo) * a.CH + sl * a.Wpad + j : 0;
+            sl -= sl >= R ? R : 0;
+            kof[nb] = k < kend ? xoff(c - c_lo, sl) + j : 0;
         }
 
         if (kr == 0) {  // bias gradient: thread (f = tid/12, phase = tid%12), fixed order
@@ -789,7 +832,12 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         const int pfx = min(4 * ((wave + kRingWaves / 2) % kRingWaves), a.RQ - 4);
         for (int qq = 0; qq < a.RQ; qq += 4) {
             if (qq == pfg && pf) load_g(n1, oh1);
-            if (qq == pfx && pf && oh1 != 0) load_x(n1, oh1);
+            if (qq == pfx && pf && oh1 != 0) {
+                if constexpr (XD)
+                    dma_x(n1, oh1);
+                else
+                    load_x(n1, oh1);
+            }
             const int qx = qq + lq;
             const int qo = qx < a.Wout ? qx * a.S : 0;
             T av[4];
@@ -811,16 +859,22 @@ __global__ __launch_bounds__(kRingThreads, 1) void conv_wgrad_ring_kernel(WgradA
         if (tt + 1 < t_end) {
             __syncthreads();
             store_g(n1, oh1);
-            if (oh1 != 0)
-                store_x(oh1);
-            else
+            if (oh1 == 0)
                 stage_x_full(n1, oh1);
+            else if constexpr (!XD)
+                store_x(oh1);
+            if constexpr (XD) wait_dma();  // this wave's DMA of the new row has landed
             __syncthreads();
             emit_g(n1, oh1);
             if (!kLoadInLoop && tt + 2 < t_end) {
                 const int n2 = oh1 + 1 < a.Hout ? n1 : n1 + 1, oh2 = oh1 + 1 < a.Hout ? oh1 + 1 : 0;
                 load_g(n2, oh2);
-                if (oh2 != 0) load_x(n2, oh2);
+                if (oh2 != 0) {
+                    if constexpr (XD)
+                        dma_x(n2, oh2);
+                    else
+                        load_x(n2, oh2);
+                }
             }
         }
         cn = n1;
@@ -873,6 +927,8 @@ long long split_bound(size_t lds, int threads, int per_split, long long T_total)
 struct WPlan {
     int NBW, KR, nkr, nft, RQ, tiles_per_img, splits, Wpad, CH, SG, rows_max, pipelined, spr;
     int rowmap = 0;  // ring: row-mapped staging (one new row a tile, rows <= 64, <= 72 channels)
+    int xdma = 0;    // ring: X rows by LDS DMA into Hf + 1 slot-major slots (stride 1)
+    int x_dma_insts = 0;
     long long T_total;
     size_t lds;
 };
@@ -984,6 +1040,30 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     p.lds = tsz * ((size_t)kBM * p.SG + (size_t)nch_alloc * p.CH);
     if (p.lds > 160 * 1024) return false;
     p.rowmap = nr == 1 && p.Wpad <= kWave && p.RQ <= kWave && nch_alloc <= kRingWaves * kRMX;
+    // X rows by LDS DMA, fp32 only: stride 1 (the new row misses the current
+    // tile's slots), an image under 2 GiB (32-bit buffer offsets), and the Hf +
+    // 1 slots in LDS.  (In fp64 the DMA measured slower than the row-mapped
+    // registers it replaces: the ResNet layer's backward_filter 1.084-1.088
+    // against 1.069-1.072 ms; fp32 0.684 against 0.691-0.694.)
+    {
+        const int epi = kWave * 4 / (int)tsz;  // elements a 64-dword instruction moves
+        const int insts = (nch_alloc * p.Wpad + epi - 1) / epi;
+        // The slot stride past the DMA'd extent: two taps a filter row apart
+        // (j = Wf - 1, then j = 0 of the next row) are slot - (Wf - 1) elements
+        // apart; half the 256-byte bank period puts their 16-lane pieces of a
+        // fragment read in disjoint banks.
+        const int period = 256 / (int)tsz;
+        const int slot = insts * epi + (d.Wf - 1 + period / 2) % period;
+        const size_t ldsx = tsz * ((size_t)kBM * p.SG + (size_t)(d.Hf + 1) * slot);
+        const size_t img = tsz * (size_t)d.C * d.Hin * d.Win;
+        if (tsz == 4 && d.stride == 1 && img < 0x80000000ull && ldsx <= 160 * 1024) {
+            p.xdma = 1;
+            p.x_dma_insts = insts;
+            p.rows_max = d.Hf + 1;
+            p.CH = slot;
+            p.lds = ldsx;
+        }
+    }
     p.pipelined = 1;
     p.tiles_per_img = d.Hout;
     p.T_total = (long long)d.N * d.Hout;
@@ -991,12 +1071,22 @@ bool make_rplan(size_t tsz, const ConvDims &d, WPlan &p)
     return true;
 }
 
-template <typename T, bool ZSKIP, bool PB, bool RM>
+template <typename T, bool ZSKIP, bool PB, int XM>
 void (*ring_kernel(int nbw))(WgradArgs)
 {
-    return nbw == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP, PB, RM>
-                    : (nbw == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP, PB, RM>
-                                : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB, RM>);
+    return nbw == 3 ? conv_wgrad_ring_kernel<T, 3, ZSKIP, PB, XM>
+                    : (nbw == 2 ? conv_wgrad_ring_kernel<T, 2, ZSKIP, PB, XM>
+                                : conv_wgrad_ring_kernel<T, 1, ZSKIP, PB, XM>);
+}
+
+// The ring kernel of a plan's X staging (the pooled source has no row-mapped form).
+template <typename T, bool ZSKIP, bool PB>
+void (*ring_kernel_for(const WPlan &p))(WgradArgs)
+{
+    if (p.xdma) return ring_kernel<T, ZSKIP, PB, 2>(p.NBW);
+    if constexpr (!PB)
+        if (p.rowmap) return ring_kernel<T, ZSKIP, PB, 1>(p.NBW);
+    return ring_kernel<T, ZSKIP, PB, 0>(p.NBW);
 }
 
 // Blocks resident at once for a launch of kernel k, taken as the smaller of k's
@@ -1014,15 +1104,9 @@ int common_slots(void (*k)(WgradArgs), void (*kz)(WgradArgs), int threads, size_
 template <typename T, bool ZSKIP, bool PB>
 hipError_t launch_ring(WgradArgs a, const WPlan &p, void *dW, void *db, hipStream_t s)
 {
-    void (*k)(WgradArgs);
-    void (*kz)(WgradArgs) = nullptr;
-    if constexpr (PB) {
-        k = ring_kernel<T, ZSKIP, PB, false>(p.NBW);
-    } else {
-        k = p.rowmap ? ring_kernel<T, ZSKIP, PB, true>(p.NBW) : ring_kernel<T, ZSKIP, PB, false>(p.NBW);
-        kz = p.rowmap ? ring_kernel<T, !ZSKIP, PB, true>(p.NBW)
-                      : ring_kernel<T, !ZSKIP, PB, false>(p.NBW);
-    }
+    void (*k)(WgradArgs) = ring_kernel_for<T, ZSKIP, PB>(p);
+    void (*kz)(WgradArgs) = nullptr;  // the other zero-skip form (the pooled source has none)
+    if constexpr (!PB) kz = ring_kernel_for<T, !ZSKIP, PB>(p);
     hipError_t e = allow_dynamic_lds(k, p.lds);
     if (e != hipSuccess) return e;
     const int per_split = p.nkr * p.nft;
@@ -1338,7 +1422,14 @@ hipError_t wgrad_plan_info(int dtype, const ConvDims &d, int pool_ps, ConvPlanIn
     info.pipelined = p.pipelined;
     if (pool_ps && !ring && kBM * max_regions(p, d, pool_ps) > kThreads * kMGP) info.pipelined = 0;
     info.fused = pool_ps ? 1 : 0;
-    info.row_staged = ring && !pool_ps && p.rowmap ? (tsz == 4 ? 3 : 1) : 0;
+    info.row_staged = 0;
+    if (ring) {
+        if (p.xdma)
+            info.row_staged |= 4;
+        else if (p.rowmap && !pool_ps)
+            info.row_staged |= 1;
+        if ((p.xdma || p.rowmap) && !pool_ps && tsz == 4) info.row_staged |= 2;
+    }
     return hipSuccess;
 }
 
@@ -1381,6 +1472,7 @@ hipError_t launch_conv_backward_filter(int dtype, const void *X, const void *dou
     a.CH = p.CH;
     a.SG = p.SG;
     a.rows_max = p.rows_max;
+    a.x_dma_insts = p.x_dma_insts;
     a.pipelined = p.pipelined;
     a.spr = p.spr;
     a.magic_rq = host_magic(p.RQ);

@@ -42,7 +42,8 @@ struct ConvPlanInfo {
     int g_stride, row_slices;
     int pipelined;  // register-staged kernels: loads held in registers across the MFMAs
     int fused;      // fused forms: 1 when the fused kernel runs, 0 for the unfused fallback
-    int row_staged; // row ring: a row per wave (bit 0 the new input row, bit 1 the g tile)
+    int row_staged; // row ring: bit 0 new input row a row per wave, bit 1 the g tile so,
+                    // bit 2 the new input row by LDS DMA
 };
 
 // Fused forms a plan query may ask about (the values of dmlnn_conv_form).

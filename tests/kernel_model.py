@@ -807,17 +807,21 @@ def x_cell(g, c, y, x):
     return np.where(ok, (c * g["Hin"] + y) * g["Win"] + x, -1)
 
 
-def wgrad_common(g, p, tsz, kernel, threads):
+def wgrad_common(g, p, tsz, kernel, threads, x_elems=None):
+    """x_elems: elements of the X region when it is not nch_alloc channels of
+    window_rows x window_width (the ring's slot-major DMA layout)."""
     HfWf, K = g["Hf"] * g["Wf"], g["K"]
     KR, SG, RQ = p["chunk"], p["g_stride"], p["tile_pixels"]
     Wpad, rows_max = p["window_width"], p["window_rows"]
     nch_alloc = (KR - 1) // HfWf + 2
     CH = rows_max * Wpad
+    if x_elems is None:
+        x_elems = nch_alloc * CH
     need(SG == RQ + 2 and RQ % 4 == 0, f"{kernel}: g tile layout")
-    need(p["lds_bytes"] == tsz * (BM * SG + nch_alloc * CH), f"{kernel}: LDS size")
+    need(p["lds_bytes"] == tsz * (BM * SG + x_elems), f"{kernel}: LDS size")
     lds = Lds(p["lds_bytes"], kernel)
     lds.region("g", 0, tsz * BM * SG)
-    lds.region("x", tsz * BM * SG, tsz * nch_alloc * CH)
+    lds.region("x", tsz * BM * SG, tsz * x_elems)
     lds.disjoint("g", "x")
     lds.region("all", 0, p["lds_bytes"])
     nkr, nft = cdiv(K, KR), cdiv(g["F"], BM)
@@ -859,27 +863,34 @@ def wgrad_outputs(g, p, tsz, kernel, ranges, NBW, nwaves, ws_elems):
         glob(kernel, "workspace (db)", p["splits"] * F * K + split * F + np.arange(F), ws_elems)
 
 
-def ring_contents_ok(g, kernel, T_total, splits):
-    """Walk every split's tiles: the ring slot (oh*S + i) mod Hf must hold input
-    row oh*S + i when tile oh reads it."""
+def ring_contents_ok(g, kernel, T_total, splits, R):
+    """Walk every split's tiles: the ring slot (oh*S + i) mod R must hold input
+    row oh*S + i when tile oh reads it.  With R = Hf + 1 slots (the DMA form)
+    a tile's new row lands while the previous tile still reads: it must miss
+    the slots that tile reads."""
     Hf, S, Hout = g["Hf"], g["S"], g["Hout"]
     nr = min(S, Hf)
     for sp in range(splits):
         t0, t1 = sp * T_total // splits, (sp + 1) * T_total // splits
         slots = None
+        prev_read = set()
         for tt in range(t0, t1):
             oh = tt % Hout
             if tt == t0 or oh == 0:
-                slots = {(oh * S + t) % Hf: oh * S + t for t in range(Hf)}
+                slots = {(oh * S + t) % R: oh * S + t for t in range(Hf)}
             else:
-                s0 = (oh * S + Hf - nr) % Hf
+                s0 = (oh * S + Hf - nr) % R
                 for r in range(nr):
                     yr = oh * S + Hf - nr + r
-                    sl = s0 + r - (Hf if s0 + r >= Hf else 0)
-                    need(sl == yr % Hf, f"{kernel}: new row {yr} goes to slot {sl}")
+                    sl = s0 + r - (R if s0 + r >= R else 0)
+                    need(sl == yr % R, f"{kernel}: new row {yr} goes to slot {sl}")
+                    if R > Hf:
+                        need(sl not in prev_read,
+                             f"{kernel}: new row {yr} lands in a slot the previous tile reads")
                     slots[sl] = yr
+            prev_read = {(oh * S + i) % R for i in range(Hf)}
             for i in range(Hf):
-                need(slots[(oh * S + i) % Hf] == oh * S + i,
+                need(slots[(oh * S + i) % R] == oh * S + i,
                      f"{kernel}: tile of output row {oh} reads a stale ring slot")
 
 
@@ -889,18 +900,37 @@ def model_wgrad_ring(g, p, tsz, form):
     KR, SG, RQ, Wpad = p["chunk"], p["g_stride"], p["tile_pixels"], p["window_width"]
     NBW = KR // (16 * 12)
     need(KR == 16 * NBW * 12 and NBW in (1, 2, 3), f"{kernel}: k range {KR}")
-    need(RQ == cdiv(Wout, 4) * 4 and p["window_rows"] == Hf and Wpad == (Wout - 1) * S + g["Wf"],
-         f"{kernel}: tile geometry")
-    lds, ranges, nch_alloc, CH, ws_elems = wgrad_common(g, p, tsz, kernel, 768)
+    need(RQ == cdiv(Wout, 4) * 4 and Wpad == (Wout - 1) * S + g["Wf"], f"{kernel}: tile geometry")
+    nch_alloc = (KR - 1) // HfWf + 2
+    nr = min(S, Hf)
+    pb = form == "pooled_source"
+    # X staging: bit 2 the new input row by LDS DMA into Hf + 1 slot-major slots
+    # (fp32, stride 1, image under 2 GiB, LDS within 160 KB), else bit 0 a row a
+    # wave through registers; bit 1 the g tile a row a wave (fp32, not the pooled
+    # source)
+    epi = 256 // tsz                                  # elements a DMA instruction moves
+    insts = cdiv(nch_alloc * Wpad, epi)
+    SLOT = insts * epi + (g["Wf"] - 1 + epi // 2) % epi  # (epi = the bank period in elements)
+    xd_ok = (tsz == 4 and S == 1 and tsz * g["C"] * g["Hin"] * g["Win"] < 2 ** 31
+             and tsz * (BM * SG + (Hf + 1) * SLOT) <= 160 * 1024)
+    rm_ok = nr == 1 and Wpad <= 64 and RQ <= 64 and nch_alloc <= 12 * 6
+    rs = p["row_staged"]
+    want = (4 if xd_ok else (1 if rm_ok and not pb else 0)) | \
+        (2 if (xd_ok or rm_ok) and not pb and tsz == 4 else 0)
+    need(rs == want, f"{kernel}: row staging {rs}, expected {want}")
+    XD = bool(rs & 4)
+    R = Hf + 1 if XD else Hf
+    need(p["window_rows"] == R, f"{kernel}: {p['window_rows']} ring slots")
+    lds, ranges, nch_alloc, CH, ws_elems = wgrad_common(
+        g, p, tsz, kernel, 768, x_elems=(R * SLOT if XD else None))
+    if XD:
+        CH = SLOT                                     # the slot stride
+
+    def xo(c, sl):                                    # a channel's row in a ring slot
+        return sl * SLOT + c * Wpad if XD else c * CH + sl * Wpad
     need(BM * SG >= 768, f"{kernel}: the db reduction needs 768 slots of the g tile")
     lane = np.arange(64)
     lq, l16 = lane >> 4, lane & 15
-    nr = min(S, Hf)
-    pb = form == "pooled_source"
-    # row-mapped staging: bit 0 the new input row, bit 1 the g tile (fp32 only)
-    rs = p["row_staged"]
-    rm_ok = not pb and nr == 1 and Wpad <= 64 and RQ <= 64 and nch_alloc <= 12 * 6
-    need(rs == ((3 if tsz == 4 else 1) if rm_ok else 0), f"{kernel}: row staging {rs}")
     w_it = (np.arange(12)[:, None] + 12 * np.arange(6)[None, :]).ravel()  # rows of wave w, step it
     if rs & 2:
         # wave w, step it: g row w + 12 it (< 64), lane u (< RQ); every cell once
@@ -940,7 +970,31 @@ def model_wgrad_ring(g, p, tsz, form):
     for kbeg, kend, c_lo, nch in ranges:
         # new-row staging
         nrw = nr * Wpad
-        if rs & 1:
+        if XD:
+            # dword d = 64 i + lane of slot sl (instruction i by wave i % 12): element
+            # d // (tsz / 4) = (channel c, column u); zeros (an offset past the
+            # image) for padding columns, channels past the range, rows outside
+            d = np.arange(insts * 64)
+            e = d // (tsz // 4)
+            half = d % (tsz // 4)
+            c = div_magic(e, Wpad, f"{kernel} DMA channel")
+            u = e - c * Wpad
+            need(np.array_equal(np.unique(e[(c < nch)]), np.arange(nch * Wpad)) and
+                 np.bincount(e[c < nch]).max() == tsz // 4, f"{kernel}: DMA cells not written once")
+            cg, x = c_lo + c, u - g["P"]
+            img = g["C"] * g["Hin"] * g["Win"]
+            for oh in (1, g["Hout"] - 1):
+                yr = oh + Hf - 1
+                y = yr - g["P"]
+                sl = yr % R
+                live = (c < nch) & (cg < g["C"]) & (x >= 0) & (x < g["Win"]) & (0 <= y < g["Hin"])
+                vo = ((cg * g["Hin"] + y) * g["Win"] + x) * tsz + 4 * half
+                need(np.all(vo[live] >= 0) & np.all(vo[live] + 4 <= img * tsz),
+                     f"{kernel}: DMA offset outside the image")
+                need(img * tsz < 2 ** 31, f"{kernel}: DMA range past 2^31")
+                lds.access("x", sl * SLOT + (d * 4) // tsz, tsz, "new-row DMA")
+                need(np.all((d * 4) // tsz < SLOT), f"{kernel}: DMA past its slot")
+        elif rs & 1:
             # wave w, step it: channel w + 12 it (< nch), lane u (< Wpad); each cell once
             c = np.repeat(w_it[w_it < nch], 64)
             rem = np.tile(lane, int((w_it < nch).sum()))
@@ -962,22 +1016,23 @@ def model_wgrad_ring(g, p, tsz, form):
             rem = e - c * nrw
             div_magic(rem, Wpad, f"{kernel} new-row row")
         for oh in range(min(g["Hout"], 2 * Hf + 2)):
-            s0 = (oh * S + Hf - nr) % Hf
-            wrap, ring = (Hf - s0) * Wpad, Hf * Wpad
-            idx = s0 * Wpad + rem - np.where(rem >= wrap, ring, 0)
-            need((idx >= 0) & (idx < CH), f"{kernel}: new row outside its channel's ring")
-            lds.access("x", c * CH + idx, tsz, "new-row store")
+            if not XD:
+                s0 = (oh * S + Hf - nr) % Hf
+                wrap, ring = (Hf - s0) * Wpad, Hf * Wpad
+                idx = s0 * Wpad + rem - np.where(rem >= wrap, ring, 0)
+                need((idx >= 0) & (idx < CH), f"{kernel}: new row outside its channel's ring")
+                lds.access("x", c * CH + idx, tsz, "new-row store")
             # full staging
-            e2 = np.arange(nch * CH)
+            e2 = np.arange(nch * Hf * Wpad)
             rw = div_magic(e2, Wpad, f"{kernel} window row")
             u = e2 - rw * Wpad
             c2 = div_small(rw, Hf, f"{kernel} window channel")
             t = rw - c2 * Hf
-            rot0 = (oh * S) % Hf
-            sl = rot0 + t - np.where(rot0 + t >= Hf, Hf, 0)
-            lds.access("x", c2 * CH + sl * Wpad + u, tsz, "window store")
+            rot0 = (oh * S) % R
+            sl = rot0 + t - np.where(rot0 + t >= R, R, 0)
+            lds.access("x", xo(c2, sl) + u, tsz, "window store")
             # fragment reads of tile oh
-            rot = (oh * S) % Hf
+            rot = (oh * S) % R
             for w in range(12):
                 for nb in range(NBW):
                     k = kbeg + (w * NBW + nb) * 16 + l16
@@ -986,18 +1041,22 @@ def model_wgrad_ring(g, p, tsz, form):
                     tp = kc - cc * HfWf
                     ii = div_magic(tp, g["Wf"], f"{kernel} column row")
                     jj = tp - ii * g["Wf"]
-                    slr = rot + ii - np.where(rot + ii >= Hf, Hf, 0)
-                    kof = np.where(k < kend, (cc - c_lo) * CH + slr * Wpad + jj, 0)
+                    slr = rot + ii - np.where(rot + ii >= R, R, 0)
+                    kof = np.where(k < kend, xo(cc - c_lo, slr) + jj, 0)
                     for qq in range(0, RQ, 4):
                         qx = qq + lq
                         qo = np.where(qx < Wout, qx * S, 0)
                         lds.access("x", kof + qo, tsz, "patch fragment read")
-                        # meaning: slot sl holds input row oh*S + ((sl - rot) mod Hf)
+                        # meaning: slot sl holds input row oh*S + ((sl - rot) mod R)
                         # (the ring walk below checks that), column u holds input
                         # column u - P
-                        sl = (kof % CH) // Wpad
-                        ucol = (kof % CH) % Wpad + qo
-                        got = x_cell(g, c_lo + kof // CH, oh * S + (sl - rot) % Hf - g["P"],
+                        if XD:
+                            sl, cx = kof // SLOT, (kof % SLOT) // Wpad
+                            ucol = (kof % SLOT) % Wpad + qo
+                        else:
+                            sl, cx = (kof % CH) // Wpad, kof // CH
+                            ucol = (kof % CH) % Wpad + qo
+                        got = x_cell(g, c_lo + cx, oh * S + (sl - rot) % R - g["P"],
                                      ucol - g["P"])
                         want = x_cell(g, cc, oh * S + ii - g["P"], qx * S + jj - g["P"])
                         live = (k < kend) & (qx < Wout)
@@ -1014,8 +1073,8 @@ def model_wgrad_ring(g, p, tsz, form):
     ok = (f < g["F"]) & (u < Wout)
     for n, oh in ((0, 0), (g["N"] - 1, g["Hout"] - 1)):
         glob(kernel, "g_out", ((n * g["F"] + f) * g["Q"] + oh * Wout + u)[ok], g["N"] * g["F"] * g["Q"])
-    ring_contents_ok(g, kernel, g["N"] * g["Hout"], p["splits"])
-    ring_contents_ok(g, kernel, g["N"] * g["Hout"], 1)
+    ring_contents_ok(g, kernel, g["N"] * g["Hout"], p["splits"], R)
+    ring_contents_ok(g, kernel, g["N"] * g["Hout"], 1, R)
     wgrad_outputs(g, p, tsz, kernel, ranges, NBW, 12, ws_elems)
 
 

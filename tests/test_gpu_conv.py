@@ -43,8 +43,8 @@ CASES = [
     ConvShape(3, 23, 11, 18, 3, 5, 5, 2, 2),    # 5x5 stride 2: splits start mid-image, ring slots wrap
     ConvShape(2, 23, 60, 60, 80, 5, 5, 1, 2),   # row-mapped staging at its limits: 64-element
                                                 # window rows, 60-pixel tiles; two filter tiles
-    ConvShape(1, 64, 60, 60, 8, 3, 3, 1, 1),    # fp64: the DMA ring would need 163 KB of LDS,
-                                                # so the new row goes through registers
+    ConvShape(1, 64, 60, 60, 8, 3, 3, 1, 1),    # 60-wide rows over 64 channels: past the row
+                                                # ring's staging, the tiled backward_filter
     # at most four output rows (forward F <= 4, backward_data C <= 4): direct kernel
     ConvShape(2, 3, 9, 11, 1, 7, 7, 1, 3),      # F = 1, 7x7 (any-width tap loop)
     ConvShape(1, 1, 16, 16, 6, 3, 3, 2, 1),     # backward_data C = 1, stride 2

@@ -67,6 +67,24 @@ def test_workspace_is_the_launchable_splits(name, dt):
     assert p["workspace_bytes"] == dmlnn.conv2d_backward_filter_workspace_size(DT[dt], *s.args())
 
 
+def test_ring_staging_forms():
+    """How the row ring stages its next input row: fp32 at stride 1 by LDS DMA
+    into an Hf + 1 slot ring (and the g tile a row a wave), fp64 at stride 1 a
+    row a wave through registers in an Hf slot ring, and any dtype at stride 2
+    an element a thread; the pooled source's g tile has its own staging."""
+    s1 = SHAPES["resnet_conv"]
+    s2 = ConvShape(2, 64, 6, 24, 5, 3, 3, 2, 1)
+    for s, dt, want_rs, want_rows in ((s1, "f32", 4 | 2, s1.Hf + 1), (s1, "f64", 1, s1.Hf),
+                                      (s2, "f32", 0, s2.Hf), (s2, "f64", 0, s2.Hf)):
+        p = dmlnn.conv2d_plan(DT[dt], "backward_filter", *s.args())
+        assert p["kernel"] == "wgrad_ring"
+        assert (p["row_staged"], p["window_rows"]) == (want_rs, want_rows), (s, dt, p)
+    s3 = ConvShape(2, 40, 12, 12, 48, 3, 3, 1, 1)
+    p = dmlnn.conv2d_plan_fused(DT["f32"], "backward_filter", "pooled_source", *s3.args(),
+                                pool=(2, 2, 2, 0))
+    assert p["kernel"] == "wgrad_ring" and p["row_staged"] == 4 and p["window_rows"] == 4
+
+
 def test_benchmark_layer_workspace_bound():
     s = SHAPES["resnet_conv"]
     for dt in DT.values():
